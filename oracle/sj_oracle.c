@@ -1,0 +1,287 @@
+/*
+ * sj_oracle.c -- reference (oracle) similarity join.  TEST INFRASTRUCTURE ONLY:
+ * the tests, the package smoke check and the benchmark's CPU-baseline leg use
+ * it to check and to time the GPU library; the library never calls it.
+ *
+ * It computes the plain definition of the similarity join of Ahle & Silvestri,
+ * "Similarity Search with Tensor Core Units", Section 4: given point sets P and
+ * Q in R^d, the set of pairs (x, y), x in P, y in Q, with D(x, y) <= r.  The
+ * brute-force method of Section 4 (all pair distances through one product of
+ * the n x d' matrices F_P and G_Q) returns exactly this set, so the oracle is
+ * the definition written out with nested loops:
+ *
+ *   inner product (cosine on unit rows, Section 4 ip-distance examples):
+ *       report (i, j)  iff  sum_k P[i][k] * Q[j][k]  >= s
+ *   squared Euclidean distance (Section 4, squared L2 example):
+ *       report (i, j)  iff  sum_k (P[i][k] - Q[j][k])^2  <= r2
+ *
+ * Readings taken where the paper is silent: both tests are inclusive; the L2
+ * threshold applies to the squared distance; pairs are ordered index pairs
+ * (duplicate rows are distinct points, a self-join includes (i, i)).
+ *
+ * Arithmetic: every stored element is decoded exactly to double (binary16,
+ * bfloat16 and int8 are all subsets of binary64), scores are accumulated in
+ * double in ascending k.  For integer-valued inputs whose partial sums stay
+ * below 2^53 this is exact.
+ *
+ * Plain C, no intrinsics, no blocking; OpenMP only splits the independent rows
+ * of P between threads.  Output pairs are in lexicographic (i, j) order.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { OR_F16 = 1, OR_BF16 = 2, OR_I8 = 3 };
+enum { OR_IP = 0, OR_L2 = 1 };
+
+/* IEEE 754 binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.
+ * Exponent field 0 holds zero and subnormals (fraction * 2^-24); 31 holds
+ * infinities and NaNs; otherwise the value is (1024 + fraction) * 2^(e - 25). */
+static double decode_f16(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1f;
+    int f = h & 0x3ff;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24);
+    else if (e == 31)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + f), e - 25);
+    return sign ? -v : v;
+}
+
+/* bfloat16: the upper 16 bits of an IEEE binary32: 1 sign bit, 8 exponent bits
+ * (bias 127), 7 fraction bits.  Exponent field 0 holds zero and subnormals
+ * (fraction * 2^-133); 255 holds infinities and NaNs; otherwise the value is
+ * (128 + fraction) * 2^(e - 134). */
+static double decode_bf16(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int e = (h >> 7) & 0xff;
+    int f = h & 0x7f;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -133);
+    else if (e == 255)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(128 + f), e - 134);
+    return sign ? -v : v;
+}
+
+static double elem(int dtype, const void *X, int64_t idx)
+{
+    switch (dtype) {
+    case OR_F16:
+        return decode_f16(((const uint16_t *)X)[idx]);
+    case OR_BF16:
+        return decode_bf16(((const uint16_t *)X)[idx]);
+    case OR_I8:
+        return (double)((const int8_t *)X)[idx];
+    default:
+        return NAN;
+    }
+}
+
+/* Decode `count` stored elements into doubles. */
+void or_decode(int dtype, const void *X, int64_t count, double *out)
+{
+    for (int64_t t = 0; t < count; ++t)
+        out[t] = elem(dtype, X, t);
+}
+
+/* <P_i, Q_j> in double, ascending k. */
+double or_score_ip(int dtype, const void *P, int64_t i, const void *Q, int64_t j, int64_t d)
+{
+    double s = 0.0;
+    for (int64_t k = 0; k < d; ++k)
+        s += elem(dtype, P, i * d + k) * elem(dtype, Q, j * d + k);
+    return s;
+}
+
+/* ||P_i - Q_j||^2 in double, ascending k, from the coordinate differences. */
+double or_score_l2(int dtype, const void *P, int64_t i, const void *Q, int64_t j, int64_t d)
+{
+    double s = 0.0;
+    for (int64_t k = 0; k < d; ++k) {
+        double t = elem(dtype, P, i * d + k) - elem(dtype, Q, j * d + k);
+        s += t * t;
+    }
+    return s;
+}
+
+/* Does the pair belong to the join? */
+static int matches(int metric, double score, double thr)
+{
+    return metric == OR_IP ? (score >= thr) : (score <= thr);
+}
+
+typedef struct {
+    uint32_t *pairs;   /* matches of this row: j values */
+    int64_t n, cap;
+    uint32_t *band;    /* boundary-band j values */
+    uint8_t *band_match;
+    int64_t nb, capb;
+} row_out;
+
+static int push_u32(uint32_t **buf, int64_t *n, int64_t *cap, uint32_t v)
+{
+    if (*n == *cap) {
+        int64_t nc = *cap ? 2 * *cap : 16;
+        uint32_t *nb = (uint32_t *)realloc(*buf, (size_t)nc * sizeof(uint32_t));
+        if (!nb)
+            return -1;
+        *buf = nb;
+        *cap = nc;
+    }
+    (*buf)[(*n)++] = v;
+    return 0;
+}
+
+/*
+ * The join over the rows `rows[0..n_rows)` of P (all rows 0..n_p-1 when rows is
+ * NULL) against every row of Q.
+ *
+ *   out_pairs: (i, j) uint32 pairs, lexicographic in (rows order, j); at most
+ *              `cap` are written.
+ *   band > 0 : pairs whose score lies within `band` of the threshold are also
+ *              listed in band_pairs / band_match (match flag), at most band_cap.
+ *   threads  : OpenMP threads (<= 0: the runtime default).
+ *
+ * Returns the total number of matches (which may exceed cap), -1 on bad
+ * arguments, -2 when out of host memory.  *n_band receives the band size.
+ */
+int64_t or_join(int metric, int dtype, const void *P, int64_t n_p, const void *Q, int64_t n_q,
+                int64_t d, double thr, const int64_t *rows, int64_t n_rows, double band,
+                uint32_t *out_pairs, int64_t cap, uint32_t *band_pairs, uint8_t *band_match,
+                int64_t band_cap, int64_t *n_band, int threads)
+{
+    if (n_p < 0 || n_q < 0 || d < 0 || (metric != OR_IP && metric != OR_L2))
+        return -1;
+    if (dtype != OR_F16 && dtype != OR_BF16 && dtype != OR_I8)
+        return -1;
+    if (!rows)
+        n_rows = n_p;
+    for (int64_t r = 0; rows && r < n_rows; ++r)
+        if (rows[r] < 0 || rows[r] >= n_p)
+            return -1;
+    row_out *ro = (row_out *)calloc((size_t)(n_rows ? n_rows : 1), sizeof(row_out));
+    if (!ro)
+        return -2;
+    int failed = 0;
+#ifdef _OPENMP
+    int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
+#endif
+    for (int64_t r = 0; r < n_rows; ++r) {
+        int64_t i = rows ? rows[r] : r;
+        row_out *o = &ro[r];
+        for (int64_t j = 0; j < n_q; ++j) {
+            double sc = metric == OR_IP ? or_score_ip(dtype, P, i, Q, j, d)
+                                        : or_score_l2(dtype, P, i, Q, j, d);
+            int m = matches(metric, sc, thr);
+            if (m && push_u32(&o->pairs, &o->n, &o->cap, (uint32_t)j))
+                failed = 1;
+            if (band > 0.0 && fabs(sc - thr) <= band) {
+                int64_t before = o->capb;
+                if (push_u32(&o->band, &o->nb, &o->capb, (uint32_t)j)) {
+                    failed = 1;
+                } else {
+                    if (o->capb != before) {
+                        uint8_t *nm = (uint8_t *)realloc(o->band_match, (size_t)o->capb);
+                        if (!nm) {
+                            failed = 1;
+                            continue;
+                        }
+                        o->band_match = nm;
+                    }
+                    o->band_match[o->nb - 1] = (uint8_t)m;
+                }
+            }
+        }
+    }
+    int64_t total = 0, nb = 0;
+    for (int64_t r = 0; r < n_rows; ++r) {
+        int64_t i = rows ? rows[r] : r;
+        for (int64_t t = 0; t < ro[r].n; ++t, ++total)
+            if (total < cap) {
+                out_pairs[2 * total] = (uint32_t)i;
+                out_pairs[2 * total + 1] = ro[r].pairs[t];
+            }
+        for (int64_t t = 0; t < ro[r].nb; ++t, ++nb)
+            if (nb < band_cap) {
+                band_pairs[2 * nb] = (uint32_t)i;
+                band_pairs[2 * nb + 1] = ro[r].band[t];
+                band_match[nb] = ro[r].band_match[t];
+            }
+        free(ro[r].pairs);
+        free(ro[r].band);
+        free(ro[r].band_match);
+    }
+    free(ro);
+    if (n_band)
+        *n_band = nb;
+    return failed ? -2 : total;
+}
+
+/* Number of matches of rows[0..n_rows) (all rows when NULL) against Q;
+ * per_row (optional) receives the count of each listed row. */
+int64_t or_count(int metric, int dtype, const void *P, int64_t n_p, const void *Q, int64_t n_q,
+                 int64_t d, double thr, const int64_t *rows, int64_t n_rows, int64_t *per_row,
+                 int threads)
+{
+    if (n_p < 0 || n_q < 0 || d < 0 || (metric != OR_IP && metric != OR_L2))
+        return -1;
+    if (dtype != OR_F16 && dtype != OR_BF16 && dtype != OR_I8)
+        return -1;
+    if (!rows)
+        n_rows = n_p;
+    for (int64_t r = 0; rows && r < n_rows; ++r)
+        if (rows[r] < 0 || rows[r] >= n_p)
+            return -1;
+    int64_t total = 0;
+#ifdef _OPENMP
+    int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt) reduction(+ : total)
+#endif
+    for (int64_t r = 0; r < n_rows; ++r) {
+        int64_t i = rows ? rows[r] : r;
+        int64_t c = 0;
+        for (int64_t j = 0; j < n_q; ++j) {
+            double sc = metric == OR_IP ? or_score_ip(dtype, P, i, Q, j, d)
+                                        : or_score_l2(dtype, P, i, Q, j, d);
+            c += matches(metric, sc, thr);
+        }
+        if (per_row)
+            per_row[r] = c;
+        total += c;
+    }
+    return total;
+}
+
+/* Scores of the listed (i, j) pairs (metric's score, not the match flag). */
+void or_scores(int metric, int dtype, const void *P, const void *Q, int64_t d,
+               const int64_t *pairs, int64_t n_pairs, double *out)
+{
+    for (int64_t t = 0; t < n_pairs; ++t) {
+        int64_t i = pairs[2 * t], j = pairs[2 * t + 1];
+        out[t] = metric == OR_IP ? or_score_ip(dtype, P, i, Q, j, d)
+                                 : or_score_l2(dtype, P, i, Q, j, d);
+    }
+}
+
+/* Threads the OpenMP runtime would use by default (1 without OpenMP). */
+int or_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

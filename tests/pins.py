@@ -1,0 +1,422 @@
+"""Pins for the oracle: checks that tie it to something other than itself.
+
+Each pin takes the loaded oracle library (so that the mutation tests can run
+the same pins against deliberately broken copies of the oracle) and raises
+AssertionError when the oracle disagrees with
+
+  * a library routine (numpy's integer matrix product, numpy/torch decoders),
+  * a closed form (binomial counts on the hypercube, one-hot and cluster
+    counts, identical rows),
+  * exact rational arithmetic within the recursive-summation error bound,
+  * the paper's own ip-distance transforms (Section 4: Hamming and squared L2
+    as f(x).g(y)), or
+  * an invariant of the join definition (Section 4: the set of pairs with
+    D(x, y) <= r): symmetry, monotonicity, permutation equivariance,
+    zero padding, translation, scaling, block decomposition, row subsets.
+
+The pins decode the stored values themselves (numpy float16, torch bfloat16),
+independently of the oracle's own decoder.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+from workloads import encode
+
+DT = ("f16", "bf16", "i8")
+
+
+def values(dtype, X):
+    """Exact float64 values of a storage array, decoded with numpy/torch."""
+    if dtype == "f16":
+        return X.astype(np.float64)
+    if dtype == "i8":
+        return X.astype(np.float64)
+    import torch
+    return torch.from_numpy(X.view(np.int16).copy()).view(torch.bfloat16).double().numpy()
+
+
+def pairset(pairs):
+    return set(map(tuple, np.asarray(pairs, dtype=np.int64).reshape(-1, 2).tolist()))
+
+
+def mask_to_pairs(mask):
+    i, j = np.nonzero(mask)
+    return np.stack([i, j], 1)
+
+
+def rand_int(rng, n, d, lo, hi, dtype):
+    return encode(rng.integers(lo, hi + 1, size=(n, d)), dtype)
+
+
+# ---------------------------------------------------------------- decoding
+
+def pin_decode_f16_exhaustive(lib):
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    X = bits.view(np.float16).reshape(1, -1)
+    got = oracle.decode("f16", X, lib=lib).ravel()
+    want = X.astype(np.float64).ravel()
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], want[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(want[~nan]))
+
+
+def pin_decode_bf16_exhaustive(lib):
+    X = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(1, -1)
+    got = oracle.decode("bf16", X, lib=lib).ravel()
+    want = values("bf16", X).ravel()
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], want[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(want[~nan]))
+
+
+def pin_decode_i8_exhaustive(lib):
+    X = np.arange(-128, 128, dtype=np.int64).astype(np.int8).reshape(1, -1)
+    got = oracle.decode("i8", X, lib=lib).ravel()
+    assert np.array_equal(got, np.arange(-128, 128, dtype=np.float64))
+
+
+# ------------------------------------------------- library-routine pins
+
+def pin_ip_equals_integer_matmul(lib):
+    """Inner-product join == threshold of numpy's exact int64 product P.Q^T."""
+    rng = np.random.default_rng(11)
+    for dtype in DT:
+        for (n_p, n_q, d, lo, hi) in ((37, 53, 1, -8, 8), (29, 41, 7, -8, 8), (40, 33, 33, -4, 4),
+                                      (23, 31, 130, -3, 5)):
+            P = rand_int(rng, n_p, d, lo, hi, dtype)
+            Q = rand_int(rng, n_q, d, lo, hi, dtype)
+            S = values(dtype, P).astype(np.int64) @ values(dtype, Q).astype(np.int64).T
+            for s in np.unique(np.quantile(S, [0.0, 0.3, 0.9, 0.99, 1.0]).round()):
+                got = oracle.join("ip", dtype, P, Q, float(s), lib=lib)
+                want = mask_to_pairs(S >= s)
+                assert got.total == want.shape[0], (dtype, n_p, n_q, d, s)
+                assert np.array_equal(got.pairs.astype(np.int64), want), (dtype, d, s)
+
+
+def pin_l2_equals_norm_expansion(lib):
+    """Squared-L2 join == threshold of N_x + N_y - 2 P.Q^T (numpy int64)."""
+    rng = np.random.default_rng(12)
+    for dtype in DT:
+        for (n_p, n_q, d, lo, hi) in ((31, 45, 1, -15, 15), (26, 38, 9, -15, 15),
+                                      (33, 21, 64, -6, 6)):
+            P = rand_int(rng, n_p, d, lo, hi, dtype)
+            Q = rand_int(rng, n_q, d, lo, hi, dtype)
+            Pv = values(dtype, P).astype(np.int64)
+            Qv = values(dtype, Q).astype(np.int64)
+            D = (Pv * Pv).sum(1)[:, None] + (Qv * Qv).sum(1)[None, :] - 2 * (Pv @ Qv.T)
+            for r2 in np.unique(np.quantile(D, [0.0, 0.01, 0.2, 0.7, 1.0]).round()):
+                got = oracle.join("l2", dtype, P, Q, float(r2), lib=lib)
+                want = mask_to_pairs(D <= r2)
+                assert np.array_equal(got.pairs.astype(np.int64), want), (dtype, d, r2)
+
+
+def pin_l2_equals_paper_fg(lib):
+    """Section 4's squared-L2 ip-distance: f(x) = (x_k^2, 1, -2 x_k)_k and
+    g(y) = (1, y_k^2, y_k)_k (the last triple of g read as (1, y^2, y), see
+    the readings in the design notes) give f(x).g(y) = ||x - y||^2 for every
+    pair; checked exactly against the oracle's scores with numpy int64."""
+    rng = np.random.default_rng(13)
+    for dtype in DT:
+        P = rand_int(rng, 17, 11, -15, 15, dtype)
+        Q = rand_int(rng, 19, 11, -15, 15, dtype)
+        x = values(dtype, P).astype(np.int64)
+        y = values(dtype, Q).astype(np.int64)
+        F = np.stack([x * x, np.ones_like(x), -2 * x], axis=2).reshape(x.shape[0], -1)
+        G = np.stack([np.ones_like(y), y * y, y], axis=2).reshape(y.shape[0], -1)
+        D = F @ G.T
+        pr = np.array([(i, j) for i in range(17) for j in range(19)])
+        got = oracle.scores("l2", dtype, P, Q, pr, lib=lib)
+        assert np.array_equal(got, D.ravel().astype(np.float64)), dtype
+
+
+def pin_hamming_closed_form(lib):
+    """On {0,1}^d the squared distance is the Hamming distance, which Section
+    4's Hamming ip-distance f(x) = (x_k, 1 - x_k)_k, g(y) = (1 - y_k, y_k)_k
+    also computes; both checked against popcount(x xor y)."""
+    rng = np.random.default_rng(14)
+    d = 23
+    bp = rng.integers(0, 2, size=(21, d))
+    bq = rng.integers(0, 2, size=(18, d))
+    pr = np.array([(i, j) for i in range(21) for j in range(18)])
+    ham = np.array([bin(int("".join(map(str, bp[i])), 2) ^ int("".join(map(str, bq[j])), 2))
+                    .count("1") for i, j in pr], dtype=np.float64)
+    F = np.stack([bp, 1 - bp], 2).reshape(21, -1)
+    G = np.stack([1 - bq, bq], 2).reshape(18, -1)
+    assert np.array_equal((F @ G.T).ravel().astype(np.float64), ham)
+    for dtype in DT:
+        got = oracle.scores("l2", dtype, encode(bp, dtype), encode(bq, dtype), pr, lib=lib)
+        assert np.array_equal(got, ham), dtype
+
+
+# ------------------------------------------------------- closed forms
+
+def pin_hypercube_ip_counts(lib):
+    """P = Q = all of {-1,+1}^d: <x, y> = d - 2 Ham(x, y) and each x has
+    C(d, h) partners at Hamming distance h, so the join has
+    2^d * sum_{h : d - 2h >= s} C(d, h) pairs (ties included)."""
+    for d in (1, 6, 9):
+        cube = np.array([[1 if (v >> k) & 1 else -1 for k in range(d)] for v in range(1 << d)])
+        for dtype in DT:
+            X = encode(cube, dtype)
+            for s in (-d - 1, -d, -1, 0, 1, 2, d - 2, d - 1, d, d + 1, 0.5, -0.5):
+                want = (1 << d) * sum(math.comb(d, h) for h in range(d + 1) if d - 2 * h >= s)
+                got = oracle.count("ip", dtype, X, X.copy(), float(s), lib=lib)
+                assert got == want, (d, dtype, s, got, want)
+
+
+def pin_binary_l2_counts(lib):
+    """P = Q = all of {0,1}^d: ||x - y||^2 = Ham(x, y), so the join at radius
+    r2 has 2^d * sum_{h <= r2} C(d, h) pairs."""
+    for d in (1, 5, 8):
+        cube = np.array([[(v >> k) & 1 for k in range(d)] for v in range(1 << d)])
+        for dtype in DT:
+            X = encode(cube, dtype)
+            for r2 in (-1, 0, 0.5, 1, 2, d - 1, d, d + 3):
+                want = (1 << d) * sum(math.comb(d, h) for h in range(d + 1) if h <= r2)
+                got = oracle.count("l2", dtype, X, X.copy(), float(r2), lib=lib)
+                assert got == want, (d, dtype, r2, got, want)
+
+
+def pin_identical_rows(lib):
+    """n_p copies of x joined with n_q copies of x: all n_p * n_q pairs when
+    s <= ||x||^2, none above; for L2 all pairs at any r2 >= 0."""
+    rng = np.random.default_rng(15)
+    for dtype in DT:
+        x = rng.integers(-7, 8, size=13)
+        nx = int((x * x).sum())
+        P = encode(np.tile(x, (9, 1)), dtype)
+        Q = encode(np.tile(x, (14, 1)), dtype)
+        assert oracle.count("ip", dtype, P, Q, float(nx), lib=lib) == 126
+        assert oracle.count("ip", dtype, P, Q, nx + 0.5, lib=lib) == 0
+        assert oracle.count("ip", dtype, P, Q, float(nx + 1), lib=lib) == 0
+        assert oracle.count("l2", dtype, P, Q, 0.0, lib=lib) == 126
+        assert oracle.count("l2", dtype, P, Q, -0.5, lib=lib) == 0
+
+
+def pin_one_hot_counts(lib):
+    """Rows c * e_k: <x, y> = c^2 when the hot coordinates agree and 0
+    otherwise, so for 0 < s <= c^2 the join has sum_k |P_k| |Q_k| pairs and for
+    s <= 0 all of them; squared distance is 0 or 2 c^2."""
+    rng = np.random.default_rng(16)
+    d, c = 10, 3
+    kp = rng.integers(0, d, size=40)
+    kq = rng.integers(0, d, size=35)
+    Pv = np.zeros((40, d), np.int64)
+    Qv = np.zeros((35, d), np.int64)
+    Pv[np.arange(40), kp] = c
+    Qv[np.arange(35), kq] = c
+    same = sum(int((kp == k).sum()) * int((kq == k).sum()) for k in range(d))
+    for dtype in DT:
+        P, Q = encode(Pv, dtype), encode(Qv, dtype)
+        assert oracle.count("ip", dtype, P, Q, float(c * c), lib=lib) == same
+        assert oracle.count("ip", dtype, P, Q, 1.0, lib=lib) == same
+        assert oracle.count("ip", dtype, P, Q, 0.0, lib=lib) == 40 * 35
+        assert oracle.count("ip", dtype, P, Q, c * c + 1.0, lib=lib) == 0
+        assert oracle.count("l2", dtype, P, Q, 0.0, lib=lib) == same
+        assert oracle.count("l2", dtype, P, Q, 2.0 * c * c - 1, lib=lib) == same
+        assert oracle.count("l2", dtype, P, Q, 2.0 * c * c, lib=lib) == 40 * 35
+        got = oracle.join("ip", dtype, P, Q, 1.0, lib=lib).pairs.astype(np.int64)
+        want = mask_to_pairs(kp[:, None] == kq[None, :])
+        assert np.array_equal(got, want)
+
+
+def pin_orthogonal_clusters(lib):
+    """Rows with positive entries on disjoint coordinate blocks (one block per
+    cluster): <x, y> > 0 exactly within a cluster, so at s = 1 the join is the
+    union of the cluster products."""
+    rng = np.random.default_rng(17)
+    nc, bw = 5, 4
+    lp = rng.integers(0, nc, size=30)
+    lq = rng.integers(0, nc, size=27)
+    Pv = np.zeros((30, nc * bw), np.int64)
+    Qv = np.zeros((27, nc * bw), np.int64)
+    for i, a in enumerate(lp):
+        Pv[i, a * bw:(a + 1) * bw] = rng.integers(1, 4, size=bw)
+    for j, a in enumerate(lq):
+        Qv[j, a * bw:(a + 1) * bw] = rng.integers(1, 4, size=bw)
+    want = mask_to_pairs(lp[:, None] == lq[None, :])
+    for dtype in DT:
+        got = oracle.join("ip", dtype, encode(Pv, dtype), encode(Qv, dtype), 1.0, lib=lib)
+        assert np.array_equal(got.pairs.astype(np.int64), want), dtype
+
+
+# --------------------------------------------- exact rational arithmetic
+
+def pin_real_scores_within_summation_bound(lib):
+    """Real-valued fp16/bf16 rows: every product of two decoded elements is
+    exact in binary64 (at most 11 x 11 significand bits), so the oracle's only
+    error is the recursive summation, bounded by gamma_{d} * sum_k |x_k y_k|
+    with gamma_d = d u / (1 - d u), u = 2^-53.  Exact values come from Python
+    Fractions."""
+    rng = np.random.default_rng(18)
+    u = 2.0 ** -53
+    for dtype in ("f16", "bf16"):
+        for d in (3, 64, 256):
+            P = encode(rng.standard_normal((6, d)) / math.sqrt(d), dtype)
+            Q = encode(rng.standard_normal((7, d)) / math.sqrt(d), dtype)
+            x, y = values(dtype, P), values(dtype, Q)
+            pr = np.array([(i, j) for i in range(6) for j in range(7)])
+            for metric in ("ip", "l2"):
+                got = oracle.scores(metric, dtype, P, Q, pr, lib=lib)
+                g = d * u / (1 - d * u)
+                for t, (i, j) in enumerate(pr):
+                    if metric == "ip":
+                        terms = [Fraction(a) * Fraction(b) for a, b in zip(x[i], y[j])]
+                    else:
+                        terms = [(Fraction(a) - Fraction(b)) ** 2 for a, b in zip(x[i], y[j])]
+                    exact = sum(terms, Fraction(0))
+                    mag = float(sum(abs(v) for v in terms))
+                    # the l2 terms also round the difference and the square
+                    bound = g * mag + (4 * u * mag if metric == "l2" else 0.0)
+                    assert abs(Fraction(got[t]) - exact) <= Fraction(bound), (dtype, d, metric)
+
+
+# ----------------------------------------------------------- invariants
+
+def pin_self_join_symmetry(lib):
+    """P joined with itself: (i, j) matches iff (j, i) does, for both metrics."""
+    rng = np.random.default_rng(19)
+    for dtype in DT:
+        X = rand_int(rng, 60, 12, -6, 6, dtype)
+        for metric, thr in (("ip", 20.0), ("l2", 200.0)):
+            got = pairset(oracle.join(metric, dtype, X, X, thr, lib=lib).pairs)
+            assert got, (dtype, metric)
+            assert got == {(j, i) for (i, j) in got}, (dtype, metric)
+
+
+def pin_monotone_in_threshold(lib):
+    """Raising s shrinks the inner-product join; raising r2 grows the L2 join
+    (as sets, not just counts)."""
+    rng = np.random.default_rng(20)
+    for dtype in DT:
+        P = rand_int(rng, 40, 16, -5, 5, dtype)
+        Q = rand_int(rng, 45, 16, -5, 5, dtype)
+        prev = None
+        for s in (-50.0, 0.0, 10.0, 25.0, 40.0, 80.0):
+            cur = pairset(oracle.join("ip", dtype, P, Q, s, lib=lib).pairs)
+            if prev is not None:
+                assert cur <= prev
+            prev = cur
+        prev = None
+        for r2 in (0.0, 200.0, 300.0, 400.0, 900.0):
+            cur = pairset(oracle.join("l2", dtype, P, Q, r2, lib=lib).pairs)
+            if prev is not None:
+                assert prev <= cur
+            prev = cur
+
+
+def pin_permutation_equivariance(lib):
+    """Permuting the rows of P and Q permutes the join's index pairs."""
+    rng = np.random.default_rng(21)
+    for dtype in DT:
+        P = rand_int(rng, 33, 10, -6, 6, dtype)
+        Q = rand_int(rng, 28, 10, -6, 6, dtype)
+        pp, pq = rng.permutation(33), rng.permutation(28)
+        for metric, thr in (("ip", 15.0), ("l2", 150.0)):
+            base = pairset(oracle.join(metric, dtype, P, Q, thr, lib=lib).pairs)
+            perm = pairset(oracle.join(metric, dtype, np.ascontiguousarray(P[pp]),
+                                       np.ascontiguousarray(Q[pq]), thr, lib=lib).pairs)
+            inv_p, inv_q = np.argsort(pp), np.argsort(pq)
+            assert perm == {(int(inv_p[i]), int(inv_q[j])) for (i, j) in base}
+
+
+def pin_zero_padding(lib):
+    """Appending zero coordinates to every point changes neither metric."""
+    rng = np.random.default_rng(22)
+    for dtype in DT:
+        Pv = rng.integers(-6, 7, size=(25, 9))
+        Qv = rng.integers(-6, 7, size=(31, 9))
+        pad = lambda X: np.concatenate([X, np.zeros((X.shape[0], 23), np.int64)], 1)  # noqa
+        for metric, thr in (("ip", 12.0), ("l2", 120.0)):
+            a = oracle.join(metric, dtype, encode(Pv, dtype), encode(Qv, dtype), thr, lib=lib)
+            b = oracle.join(metric, dtype, encode(pad(Pv), dtype), encode(pad(Qv), dtype), thr,
+                            lib=lib)
+            assert np.array_equal(a.pairs, b.pairs)
+
+
+def pin_translation_invariance_l2(lib):
+    """Adding one vector t to every point leaves squared distances unchanged."""
+    rng = np.random.default_rng(23)
+    for dtype in DT:
+        Pv = rng.integers(-9, 10, size=(27, 14))
+        Qv = rng.integers(-9, 10, size=(26, 14))
+        t = rng.integers(-9, 10, size=14)
+        a = oracle.join("l2", dtype, encode(Pv, dtype), encode(Qv, dtype), 300.0, lib=lib)
+        b = oracle.join("l2", dtype, encode(Pv + t, dtype), encode(Qv + t, dtype), 300.0, lib=lib)
+        assert a.total > 0 and np.array_equal(a.pairs, b.pairs)
+
+
+def pin_scaling(lib):
+    """Doubling P doubles every inner product: join(2P, Q, 2s) = join(P, Q, s).
+    Doubling both sets quadruples squared distances."""
+    rng = np.random.default_rng(24)
+    for dtype in DT:
+        Pv = rng.integers(-7, 8, size=(30, 12))
+        Qv = rng.integers(-7, 8, size=(29, 12))
+        a = oracle.join("ip", dtype, encode(Pv, dtype), encode(Qv, dtype), 30.0, lib=lib)
+        b = oracle.join("ip", dtype, encode(2 * Pv, dtype), encode(Qv, dtype), 60.0, lib=lib)
+        assert a.total > 0 and np.array_equal(a.pairs, b.pairs)
+        a = oracle.join("l2", dtype, encode(Pv, dtype), encode(Qv, dtype), 400.0, lib=lib)
+        b = oracle.join("l2", dtype, encode(2 * Pv, dtype), encode(2 * Qv, dtype), 1600.0, lib=lib)
+        assert a.total > 0 and np.array_equal(a.pairs, b.pairs)
+
+
+def pin_block_decomposition(lib):
+    """The join of P and Q is the union of the joins of their row blocks,
+    with the blocks' index offsets added back."""
+    rng = np.random.default_rng(25)
+    for dtype in DT:
+        P = rand_int(rng, 37, 8, -6, 6, dtype)
+        Q = rand_int(rng, 41, 8, -6, 6, dtype)
+        for metric, thr in (("ip", 10.0), ("l2", 100.0)):
+            full = pairset(oracle.join(metric, dtype, P, Q, thr, lib=lib).pairs)
+            parts = set()
+            for a0, a1 in ((0, 15), (15, 37)):
+                for b0, b1 in ((0, 20), (20, 41)):
+                    r = oracle.join(metric, dtype, np.ascontiguousarray(P[a0:a1]),
+                                    np.ascontiguousarray(Q[b0:b1]), thr, lib=lib)
+                    parts |= {(i + a0, j + b0) for (i, j) in pairset(r.pairs)}
+            assert full == parts
+
+
+def pin_row_subset_and_order(lib):
+    """Joining only some rows of P gives those rows' pairs; output pairs are in
+    lexicographic (i, j) order and carry no duplicates."""
+    rng = np.random.default_rng(26)
+    for dtype in DT:
+        P = rand_int(rng, 50, 6, -5, 5, dtype)
+        Q = rand_int(rng, 47, 6, -5, 5, dtype)
+        full = oracle.join("ip", dtype, P, Q, 8.0, lib=lib)
+        pr = full.pairs.astype(np.int64)
+        key = pr[:, 0] * (1 << 32) + pr[:, 1]
+        assert np.all(np.diff(key) > 0)
+        rows = np.array([3, 7, 20, 21, 49])
+        sub = oracle.join("ip", dtype, P, Q, 8.0, rows=rows, lib=lib)
+        assert pairset(sub.pairs) == {p for p in pairset(pr) if p[0] in set(rows.tolist())}
+        cnt, per = oracle.count("ip", dtype, P, Q, 8.0, rows=rows, per_row=True, lib=lib)
+        assert cnt == sub.total
+        assert per.tolist() == [int((pr[:, 0] == r).sum()) for r in rows]
+
+
+def pin_band_report(lib):
+    """Boundary-band pairs are exactly the pairs whose score is within the
+    band of the threshold, with the right match flag."""
+    rng = np.random.default_rng(27)
+    P = rand_int(rng, 30, 10, -5, 5, "i8")
+    Q = rand_int(rng, 35, 10, -5, 5, "i8")
+    x, y = P.astype(np.int64), Q.astype(np.int64)
+    S = x @ y.T
+    r = oracle.join("ip", "i8", P, Q, 12.0, band=2.0, lib=lib)
+    want = mask_to_pairs(np.abs(S - 12) <= 2)
+    assert np.array_equal(r.band_pairs.astype(np.int64), want)
+    assert np.array_equal(r.band_match, S[want[:, 0], want[:, 1]] >= 12)
+
+
+PINS = {name[4:]: fn for name, fn in sorted(globals().items()) if name.startswith("pin_")}
