@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X similarity join (one GPU).
+
+A step is one whole join call -- sj_join_ip / sj_join_l2 on one batch of
+synthetic input already resident in HBM: (row norms for L2), the fused MFMA
+product + threshold + compaction kernel, and the hand-back of the match count
+(two passes plus the scan for workloads that need count-then-emit).  The
+default workload is the 65536 x 65536, d = 128, bf16 inner-product join; the
+others (--workload c0..c4) are available for measurements but are not the
+headline line.
+
+Prints ONE JSON line on stdout:
+  metric/value/unit: pair-evaluations per second of the whole step
+  roofline: the join kernel's algorithmic FLOP (2 d per pair) / its average
+            duration measured with HIP events on the stream it runs on, against
+            the MI355X dense MFMA peak for its dtype
+  cpu_baseline: the oracle (plain C loops) on a bounded sample of the same
+            workload on this host's cores
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# dense MFMA peaks of MI355X (TFLOP/s or TOP/s)
+PEAK = {"f16": 2500.0, "bf16": 2500.0, "i8": 5000.0}
+WORKLOADS = {"c0": 0, "c1": 1, "c2": 2, "c3": 3, "c4": 4}
+TWO_PASS = {4}          # high-output workload runs count-then-emit
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2006_12608_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".h", ".hip", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(workload: str, launches_bytes_alg: float):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources; otherwise None."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p)).get(workload)
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("kernel_sha") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, target_s: float = 12.0):
+    import numpy as np
+    import oracle
+    threads = oracle.max_threads()
+    rng = np.random.default_rng(4242)
+    per_row_work = w.n_q * max(w.d, 1)
+    r0 = max(1, min(w.n_p, int(2e8 // per_row_work) or 1))
+    rows = np.sort(rng.choice(w.n_p, size=r0, replace=False))
+    t = time.perf_counter()
+    oracle.join(w.metric, w.dtype, w.P, w.Q, w.threshold, rows=rows, threads=threads)
+    t0 = time.perf_counter() - t
+    n_rows = int(max(1, min(w.n_p, round(r0 * target_s / max(t0, 1e-3)))))
+    rows = np.sort(rng.choice(w.n_p, size=n_rows, replace=False))
+    t = time.perf_counter()
+    r = oracle.join(w.metric, w.dtype, w.P, w.Q, w.threshold, rows=rows, threads=threads)
+    el = time.perf_counter() - t
+    return {"value": n_rows * w.n_q / el, "unit": "pair-evaluations/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_rows} random rows of P against all {w.n_q} rows of Q "
+                      f"({n_rows * w.n_q:.3g} pair evaluations, {el:.1f} s, {r.total} matches)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c1", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the join shards "
+              "by rows of P across GPUs, which this build does not run", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2006_12608_amd as sj
+    import workloads
+    to_device = workloads.to_torch
+
+    k = WORKLOADS[args.workload]
+    log(f"generating workload {args.workload} ...")
+    w = workloads.make_config(k)
+    torch.cuda.set_device(0)
+    Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ctx = sj.context(0, stream)
+    dt = {"f16": sj.SJ_F16, "bf16": sj.SJ_BF16, "i8": sj.SJ_I8}[w.dtype]
+    two_pass = k in TWO_PASS
+    flags = sj.SJ_FLAG_TIMING | (sj.SJ_FLAG_TWO_PASS if two_pass else 0)
+    fn = sj.sj_join_ip if w.metric == "ip" else sj.sj_join_l2
+
+    total = sj.count(Pd, Qd, w.threshold, w.metric, ctx=ctx)
+    out = torch.empty((max(total, 1), 2), dtype=torch.int32, device="cuda")
+    log(f"{w.name}: {total} matches; warmup {args.warmup}, steps {args.steps}")
+
+    def step():
+        st, n = fn(ctx, dt, Pd.data_ptr(), w.n_p, Qd.data_ptr(), w.n_q, w.d, w.threshold,
+                   out.data_ptr(), total, flags)
+        if st != sj.SJ_OK:
+            raise sj.SjError(st, sj.sj_last_error(), n)
+        return n
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kern_ms, emit_ms, count_ms, scan_ms, norm_ms = [], [], [], [], []
+    t0 = time.perf_counter()
+    n_out = 0
+    for _ in range(args.steps):
+        n_out = step()
+        s = sj.sj_get_stats(ctx)
+        kern_ms.append(s.ms_join if not two_pass else s.ms_count)
+        emit_ms.append(s.ms_emit)
+        count_ms.append(s.ms_count)
+        scan_ms.append(s.ms_scan)
+        norm_ms.append(s.ms_norms)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ms_step = el / args.steps * 1e3
+    pair_evals = w.n_p * w.n_q
+    value = pair_evals / (ms_step / 1e3)
+    kms = float(np.mean(kern_ms))
+    flop = 2.0 * pair_evals * max(w.d, 1)
+    achieved = flop / (kms / 1e3) / 1e12
+    peak = PEAK[w.dtype]
+    traffic = traffic_for(args.workload, flop)
+    line = {
+        "metric": "pair-evaluations/sec",
+        "value": value,
+        "unit": "pair-evaluations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded generator, inputs resident in HBM)",
+        "config": {"workload": w.name, "metric": w.metric, "n_p": w.n_p, "n_q": w.n_q, "d": w.d,
+                   "threshold": w.threshold, "mode": "two-pass" if two_pass else "single-pass",
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak,
+                     "unit": "TOP/s" if w.dtype == "i8" else "TFLOP/s", "frac": achieved / peak,
+                     "traffic": traffic,
+                     "kernel": "join_resident" if w.d * (1 if w.dtype == "i8" else 2) <= 512
+                     else "join_streamed",
+                     "kernel_ms": kms},
+        "effective_tflops_step": flop / (ms_step / 1e3) / 1e12,
+        "pct_peak_step": flop / (ms_step / 1e3) / 1e12 / peak,
+        "n_out": int(n_out),
+        "pairs_emitted_per_s": n_out / (float(np.mean(emit_ms)) / 1e3) if two_pass
+        else n_out / (ms_step / 1e3),
+        "phases_ms": {"norms": float(np.mean(norm_ms)), "join_or_count": kms,
+                      "scan": float(np.mean(scan_ms)), "emit": float(np.mean(emit_ms))},
+        "kernel_sha": kernel_source_hash(),
+    }
+    if two_pass:
+        line["emit_hbm_gbps_algorithmic"] = n_out * 8 / (float(np.mean(emit_ms)) / 1e3) / 1e9
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a sample ...")
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

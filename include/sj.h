@@ -1,0 +1,142 @@
+/*
+ * sj.h -- C-ABI of the MI355X (gfx950) similarity-join library (libsj.so).
+ *
+ * The operation is the similarity join of Ahle & Silvestri, "Similarity Search
+ * with Tensor Core Units", Section 4: given point sets P and Q in R^d, report
+ * every pair (x, y), x in P, y in Q, whose distance is within a threshold.  The
+ * distances are the paper's ip-distances (Section 4): inner product / cosine
+ * similarity (cosine is the inner product of rows the caller has normalised,
+ * f = g = x / ||x||) and the squared Euclidean distance.  The library computes
+ * it the way Section 4's brute-force method does: one blocked dense product of
+ * P and Q^T on the matrix cores (Theorem 1's blocked multiplication), with the
+ * threshold test and the pair compaction fused into the product's epilogue, so
+ * no score matrix is ever stored.
+ *
+ * Conventions shared by every entry point
+ *   - P is n_p x d and Q is n_q x d, row-major and contiguous (row stride d
+ *     elements), resident in device memory of the context's GPU and owned by
+ *     the caller.  Elements are IEEE binary16 (SJ_F16), bfloat16 (SJ_BF16) or
+ *     int8 (SJ_I8); inputs must be finite.  P and Q may be the same pointer
+ *     (self-join: every ordered pair, (i, i) included).
+ *   - Results are ordered index pairs (i, j), i indexing P and j indexing Q,
+ *     both 0-based uint32, stored as interleaved {i, j} (8 bytes per pair) in
+ *     the caller's device buffer `pairs` of `cap` pairs (8-byte aligned).
+ *     Duplicate rows are distinct points.
+ *   - Tests are inclusive: <P_i, Q_j> >= s, ||P_i - Q_j||^2 <= r2.
+ *   - Arithmetic: fp16/bf16 products accumulate in fp32 on the matrix cores,
+ *     int8 products accumulate exactly in int32.  Thresholds are converted once
+ *     with directed rounding so that the fp32 comparison equals the comparison
+ *     with the double threshold: s -> the smallest float >= s, r2 -> the largest
+ *     float <= r2; for int8, s -> ceil(s) and r2 -> floor(r2).  The squared
+ *     distance is evaluated as N_x + N_y - 2 <x, y> with the squared row norms
+ *     N (int32 for int8, fp32 otherwise).  Integer-valued fp16/bf16 inputs whose
+ *     partial sums stay below 2^24 in magnitude are therefore joined exactly.
+ *   - Calls are ordered on the context's stream and return once the result
+ *     count is known (they synchronise that stream).  Inputs must be ready on
+ *     that stream.  A context is not thread-safe: use one per host thread.
+ *   - Errors: every call returns a status (SJ_OK = 0 or a negative code) and
+ *     never aborts or throws; sj_last_error() describes the last failure of the
+ *     calling thread.
+ *
+ * Sizes: n_p, n_q < 2^32; 0 <= d <= 65536 for fp16/bf16 and d <= 32768 for
+ * int8 (larger d could overflow the int32 accumulators); n_p, n_q or d equal
+ * to 0 are valid (d = 0 makes every score 0).
+ */
+#ifndef SJ_H
+#define SJ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sj_ctx sj_ctx;
+
+/* Element types of P and Q. */
+enum sj_dtype { SJ_F16 = 1, SJ_BF16 = 2, SJ_I8 = 3 };
+
+/* Metrics: inner product (>= s) and squared Euclidean distance (<= r2). */
+enum sj_metric { SJ_IP = 0, SJ_L2 = 1 };
+
+/* Status codes. */
+enum sj_status {
+    SJ_OK = 0,
+    SJ_E_INVAL = -1,       /* bad argument: NULL or non-device pointer, buffer
+                              smaller than its shape, NaN threshold, bad enum */
+    SJ_E_OVERFLOW = -2,    /* more matches than `cap`: *n_out holds the exact
+                              total and the contents of `pairs` are not a valid
+                              answer */
+    SJ_E_NOMEM = -3,       /* device scratch could not be allocated */
+    SJ_E_HIP = -4,         /* a HIP runtime call failed */
+    SJ_E_UNSUPPORTED = -5  /* valid but unsupported: d too large, not gfx950 */
+};
+
+/* Flags of sj_join_ip / sj_join_l2. */
+enum sj_flags {
+    /* Count-then-emit: a first pass counts the matches of every output block,
+     * an exclusive scan turns the counts into offsets, and a second pass
+     * recomputes the product and writes each block's pairs at its offset.
+     * Costs a second product but never writes beyond `cap`, and the output
+     * order is deterministic (block-major).  Without the flag a single pass
+     * appends pairs through one atomic counter (order unspecified). */
+    SJ_FLAG_TWO_PASS = 1u,
+    /* Record GPU timestamps around every phase of the call (see sj_stats). */
+    SJ_FLAG_TIMING = 2u
+};
+
+/* Diagnostics of the last sj_join_ip / sj_join_l2 / sj_count call. */
+typedef struct sj_stats {
+    uint64_t total;        /* matches found */
+    double ms_norms;       /* GPU time of the row-norm kernel (L2 only)        */
+    double ms_join;        /* single pass: the fused product/filter/compaction */
+    double ms_count;       /* two-pass / count: the counting pass              */
+    double ms_scan;        /* two-pass / count: the scan of the block counts   */
+    double ms_emit;        /* two-pass: the emitting pass                      */
+    uint32_t kernel;       /* 1 = P rows resident in registers, 2 = K-streamed */
+    uint32_t timed;        /* 1 when the ms_* fields were measured             */
+} sj_stats;
+
+/* Create a context on `device` (a gfx950 GPU), bound to `stream` (a
+ * hipStream_t; NULL = the null stream).  The context owns only its device
+ * scratch (match counter, block counts and offsets, row norms), which grows on
+ * demand and is freed by sj_destroy.  Returns SJ_E_UNSUPPORTED on a GPU that
+ * is not gfx950. */
+int sj_create(sj_ctx **ctx, int device, void *stream);
+
+/* Inner-product join (Section 4; cosine when the caller's rows are unit):
+ * every (i, j) with <P_i, Q_j> >= s.  The first min(total, cap) pairs are
+ * written to `pairs` (device; may be NULL when cap == 0) and the total is
+ * stored in *n_out (host).  Returns SJ_E_OVERFLOW when total > cap. */
+int sj_join_ip(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+               uint32_t d, double s, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+               unsigned flags);
+
+/* Squared-Euclidean join (Section 4's squared L2 ip-distance): every (i, j)
+ * with ||P_i - Q_j||^2 <= r2 (r2 is the squared radius).  Outputs and errors
+ * as sj_join_ip. */
+int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+               uint32_t d, double r2, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+               unsigned flags);
+
+/* Number of matches of the join with metric `metric` (SJ_IP: threshold s,
+ * SJ_L2: threshold r2), stored in *count (host); writes no pairs.  Runs the
+ * counting pass and the scan of the count-then-emit protocol. */
+int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
+             uint32_t n_q, uint32_t d, double threshold, uint64_t *count);
+
+/* Free the context and its scratch; NULL is a no-op. */
+void sj_destroy(sj_ctx *ctx);
+
+/* Copy the diagnostics of the context's last call into *out. */
+int sj_get_stats(const sj_ctx *ctx, sj_stats *out);
+
+/* Message describing the last failed call made by this thread ("" if none).
+ * The string is owned by the library and valid until the thread's next call. */
+const char *sj_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SJ_H */

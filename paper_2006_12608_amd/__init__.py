@@ -1,0 +1,200 @@
+"""MI355X-native similarity join (Ahle & Silvestri, "Similarity Search with
+Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
+
+The raw C-ABI entry points are exposed under their C names (sj_create,
+sj_join_ip, sj_join_l2, sj_count, sj_destroy, sj_get_stats, sj_last_error)
+with plain integer pointers; `join_ip`, `join_l2` and `count` are
+conveniences over PyTorch device tensors.  This module only marshals
+arguments: every step of the join runs in the library's HIP kernels.  Import
+fails when libsj.so has not been built (python -m paper_2006_12608_amd.build).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsj.so")
+
+SJ_F16, SJ_BF16, SJ_I8 = 1, 2, 3
+SJ_IP, SJ_L2 = 0, 1
+SJ_OK, SJ_E_INVAL, SJ_E_OVERFLOW, SJ_E_NOMEM, SJ_E_HIP, SJ_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING = 1, 2
+
+STATUS_NAMES = {0: "SJ_OK", -1: "SJ_E_INVAL", -2: "SJ_E_OVERFLOW", -3: "SJ_E_NOMEM",
+                -4: "SJ_E_HIP", -5: "SJ_E_UNSUPPORTED"}
+
+
+class SjError(RuntimeError):
+    def __init__(self, status: int, message: str, n_out: int | None = None):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.n_out = n_out
+
+
+class sj_stats(ctypes.Structure):
+    _fields_ = [("total", ctypes.c_uint64), ("ms_norms", ctypes.c_double),
+                ("ms_join", ctypes.c_double), ("ms_count", ctypes.c_double),
+                ("ms_scan", ctypes.c_double), ("ms_emit", ctypes.c_double),
+                ("kernel", ctypes.c_uint32), ("timed", ctypes.c_uint32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2006_12608_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, u32, u64, dbl, i32 = (ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_double,
+                              ctypes.c_int)
+    lib.sj_create.argtypes = [ctypes.POINTER(vp), i32, vp]
+    lib.sj_create.restype = i32
+    join_args = [vp, i32, vp, u32, vp, u32, u32, dbl, vp, u64, ctypes.POINTER(u64), ctypes.c_uint]
+    lib.sj_join_ip.argtypes = join_args
+    lib.sj_join_ip.restype = i32
+    lib.sj_join_l2.argtypes = join_args
+    lib.sj_join_l2.restype = i32
+    lib.sj_count.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, ctypes.POINTER(u64)]
+    lib.sj_count.restype = i32
+    lib.sj_destroy.argtypes = [vp]
+    lib.sj_destroy.restype = None
+    lib.sj_get_stats.argtypes = [vp, ctypes.POINTER(sj_stats)]
+    lib.sj_get_stats.restype = i32
+    lib.sj_last_error.argtypes = []
+    lib.sj_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+# ------------------------------------------------------------ raw C-ABI names
+
+def sj_last_error() -> str:
+    return lib.sj_last_error().decode()
+
+
+def sj_create(device: int = 0, stream: int | None = None) -> int:
+    """Returns an opaque context handle (int)."""
+    h = ctypes.c_void_p()
+    st = lib.sj_create(ctypes.byref(h), device, stream or None)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return h.value
+
+
+def sj_destroy(ctx: int | None) -> None:
+    lib.sj_destroy(ctx)
+
+
+def _join_raw(fn, ctx, dtype, P, n_p, Q, n_q, d, thr, pairs, cap, flags):
+    n = ctypes.c_uint64(0)
+    st = fn(ctx, dtype, P, n_p, Q, n_q, d, float(thr), pairs, cap, ctypes.byref(n), flags)
+    return st, n.value
+
+
+def sj_join_ip(ctx, dtype, P, n_p, Q, n_q, d, s, pairs, cap, flags=0):
+    """Returns (status, n_out); pointers are integers (device addresses)."""
+    return _join_raw(lib.sj_join_ip, ctx, dtype, P, n_p, Q, n_q, d, s, pairs, cap, flags)
+
+
+def sj_join_l2(ctx, dtype, P, n_p, Q, n_q, d, r2, pairs, cap, flags=0):
+    """Returns (status, n_out); pointers are integers (device addresses)."""
+    return _join_raw(lib.sj_join_l2, ctx, dtype, P, n_p, Q, n_q, d, r2, pairs, cap, flags)
+
+
+def sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, threshold):
+    """Returns (status, count)."""
+    n = ctypes.c_uint64(0)
+    st = lib.sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, float(threshold), ctypes.byref(n))
+    return st, n.value
+
+
+def sj_get_stats(ctx) -> sj_stats:
+    out = sj_stats()
+    st = lib.sj_get_stats(ctx, ctypes.byref(out))
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return out
+
+
+# ------------------------------------------------------ torch conveniences
+
+_contexts: dict = {}
+
+
+def context(device: int | None = None, stream=None) -> int:
+    """A cached context bound to (device, stream); defaults to torch's
+    current device and stream."""
+    import torch
+    dev = torch.cuda.current_device() if device is None else int(device)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    handle = int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream or 0)
+    key = (dev, handle)
+    if key not in _contexts:
+        _contexts[key] = sj_create(dev, handle)
+    return _contexts[key]
+
+
+def dtype_code(t) -> int:
+    import torch
+    codes = {torch.float16: SJ_F16, torch.bfloat16: SJ_BF16, torch.int8: SJ_I8}
+    if t.dtype not in codes:
+        raise TypeError(f"unsupported dtype {t.dtype}; use float16, bfloat16 or int8")
+    return codes[t.dtype]
+
+
+def _check_pair(P, Q):
+    if P.dim() != 2 or Q.dim() != 2 or P.shape[1] != Q.shape[1]:
+        raise ValueError("P and Q must be 2-D with the same number of columns")
+    if P.dtype != Q.dtype:
+        raise ValueError("P and Q must have the same dtype")
+    if not (P.is_cuda and Q.is_cuda):
+        raise ValueError("P and Q must be device tensors")
+    if not (P.is_contiguous() and Q.is_contiguous()):
+        raise ValueError("P and Q must be contiguous")
+
+
+def count(P, Q, threshold: float, metric: str = "ip", ctx=None) -> int:
+    """Number of matching pairs (sj_count)."""
+    _check_pair(P, Q)
+    ctx = ctx or context(P.device.index)
+    m = SJ_IP if metric == "ip" else SJ_L2
+    st, n = sj_count(ctx, m, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0],
+                     P.shape[1], threshold)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return n
+
+
+def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out):
+    import torch
+    _check_pair(P, Q)
+    ctx = ctx or context(P.device.index)
+    flags = (SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
+    if cap is None and out is None:
+        cap = count(P, Q, thr, metric, ctx)
+    if out is None:
+        out = torch.empty((max(int(cap), 1), 2), dtype=torch.int32, device=P.device)
+        cap = int(cap)
+    else:
+        cap = out.shape[0] if cap is None else int(cap)
+    fn = sj_join_ip if metric == "ip" else sj_join_l2
+    st, n = fn(ctx, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0], P.shape[1],
+               thr, out.data_ptr() if cap else None, cap, flags)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error(), n)
+    return out[:n]
+
+
+def join_ip(P, Q, s: float, cap: int | None = None, two_pass: bool = False, timing: bool = False,
+            ctx=None, out=None):
+    """All (i, j) with <P_i, Q_j> >= s as an (n, 2) int32 tensor of uint32
+    indices.  With cap=None the exact size is counted first."""
+    return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out)
+
+
+def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool = False,
+            timing: bool = False, ctx=None, out=None):
+    """All (i, j) with ||P_i - Q_j||^2 <= r2 (see join_ip)."""
+    return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out)

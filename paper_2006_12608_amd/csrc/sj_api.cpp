@@ -1,0 +1,425 @@
+// sj_api.cpp -- host side of libsj.so: argument checking, threshold conversion,
+// scratch management and the single-pass / count-then-emit protocols around
+// the gfx950 kernels.  Public contract: include/sj.h.
+#include "sj.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cfloat>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "sj_internal.h"
+
+struct sj_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    int num_cus = 256;
+    unsigned long long *d_small = nullptr;  // [0] match counter, [1] scan total
+    unsigned long long *h_small = nullptr;  // pinned host copy of d_small
+    void *scratch = nullptr;
+    size_t scratch_bytes = 0;
+    hipEvent_t ev[6] = {};
+    sj_stats stats = {};
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(SJ_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define SJ_HIP(call)                                \
+    do {                                            \
+        hipError_t e_ = (call);                     \
+        if (e_ != hipSuccess)                       \
+            return hip_fail(e_, #call);             \
+    } while (0)
+
+size_t esize(int dtype) { return dtype == SJ_I8 ? 1 : 2; }
+
+// `p` must be device memory of the context's GPU holding at least `bytes`
+// bytes from p on (checked against its allocation's range).
+int check_device_ptr(const sj_ctx *c, const void *p, size_t bytes, const char *name)
+{
+    if (bytes == 0)
+        return SJ_OK;
+    if (!p)
+        return fail(SJ_E_INVAL, "%s is NULL", name);
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SJ_E_INVAL, "%s is not a pointer known to HIP", name);
+    }
+    if (a.type != hipMemoryTypeDevice && a.type != hipMemoryTypeManaged)
+        return fail(SJ_E_INVAL, "%s is not device memory", name);
+    if (a.device != c->device)
+        return fail(SJ_E_INVAL, "%s lives on device %d, the context on %d", name, a.device,
+                    c->device);
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p) == hipSuccess && base) {
+        const uintptr_t b = (uintptr_t)base, q = (uintptr_t)p;
+        if (q < b || q - b > size || size - (q - b) < bytes)
+            return fail(SJ_E_INVAL, "%s: %zu bytes needed but its allocation holds %zu from there",
+                        name, bytes, (size_t)(size - (q - b)));
+    } else {
+        (void)hipGetLastError();
+    }
+    return SJ_OK;
+}
+
+// Smallest float >= s (so acc >= s32 <=> acc >= s for every float acc).
+float float_at_or_above(double s)
+{
+    if (std::isinf(s))
+        return (float)s;
+    if (s > (double)FLT_MAX)
+        return INFINITY;
+    float f = (float)s;
+    if ((double)f < s)
+        f = std::nextafter(f, INFINITY);
+    return f;
+}
+
+// Largest float <= r (so x <= r32 <=> x <= r for every float x).
+float float_at_or_below(double r)
+{
+    if (std::isinf(r))
+        return (float)r;
+    if (r < -(double)FLT_MAX)
+        return -INFINITY;
+    float f = (float)r;
+    if ((double)f > r)
+        f = std::nextafter(f, -INFINITY);
+    return f;
+}
+
+int grow_scratch(sj_ctx *c, size_t bytes)
+{
+    if (bytes <= c->scratch_bytes)
+        return SJ_OK;
+    if (c->scratch) {
+        (void)hipStreamSynchronize(c->stream);
+        (void)hipFree(c->scratch);
+        c->scratch = nullptr;
+        c->scratch_bytes = 0;
+    }
+    size_t want = bytes + bytes / 4;
+    if (hipMalloc(&c->scratch, want) != hipSuccess) {
+        (void)hipGetLastError();
+        c->scratch = nullptr;
+        if (hipMalloc(&c->scratch, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            c->scratch = nullptr;
+            return fail(SJ_E_NOMEM, "cannot allocate %zu bytes of device scratch", bytes);
+        }
+        want = bytes;
+    }
+    c->scratch_bytes = want;
+    return SJ_OK;
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+double elapsed_ms(hipEvent_t a, hipEvent_t b)
+{
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0.0;
+    }
+    return ms;
+}
+
+struct Request {
+    int metric, dtype;
+    const void *P, *Q;
+    uint32_t n_p, n_q, d;
+    double thr;
+    uint32_t *pairs;
+    uint64_t cap;
+    bool two_pass, count_only, timing;
+};
+
+int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
+{
+    if (!c)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (!n_out)
+        return fail(SJ_E_INVAL, "result pointer is NULL");
+    *n_out = 0;
+    if (rq.dtype != SJ_F16 && rq.dtype != SJ_BF16 && rq.dtype != SJ_I8)
+        return fail(SJ_E_INVAL, "unknown dtype %d", rq.dtype);
+    if (rq.metric != SJ_IP && rq.metric != SJ_L2)
+        return fail(SJ_E_INVAL, "unknown metric %d", rq.metric);
+    if (std::isnan(rq.thr))
+        return fail(SJ_E_INVAL, "threshold is NaN");
+    if (rq.d > (rq.dtype == SJ_I8 ? 32768u : 65536u))
+        return fail(SJ_E_UNSUPPORTED, "d = %u is above the limit for this dtype", rq.d);
+    const size_t row_bytes = (size_t)rq.d * esize(rq.dtype);
+    const size_t bytes_p = (size_t)rq.n_p * row_bytes, bytes_q = (size_t)rq.n_q * row_bytes;
+    int st;
+    if ((st = check_device_ptr(c, rq.P, bytes_p, "P")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(c, rq.Q, bytes_q, "Q")) != SJ_OK)
+        return st;
+    if (!rq.count_only && rq.cap > 0) {
+        if (rq.cap > (uint64_t)SIZE_MAX / 8)
+            return fail(SJ_E_INVAL, "cap too large");
+        if ((st = check_device_ptr(c, rq.pairs, (size_t)rq.cap * 8, "pairs")) != SJ_OK)
+            return st;
+        if ((uintptr_t)rq.pairs % 8 != 0)
+            return fail(SJ_E_INVAL, "pairs must be 8-byte aligned");
+    }
+    c->stats = sj_stats{};
+    if (rq.n_p == 0 || rq.n_q == 0)
+        return SJ_OK;
+
+    sjk::Plan plan;
+    if (!sjk::plan_join(rq.dtype, rq.metric, rq.n_p, rq.n_q, (uint32_t)row_bytes, c->num_cus,
+                        &plan))
+        return fail(SJ_E_UNSUPPORTED, "shape %u x %u x %u is too large for one launch", rq.n_p,
+                    rq.n_q, rq.d);
+    const bool aligned = row_bytes % 16 == 0 && ((uintptr_t)rq.P % 16) == 0 &&
+                         ((uintptr_t)rq.Q % 16) == 0;
+    const bool self = rq.P == rq.Q && rq.n_p == rq.n_q;
+    const bool l2 = rq.metric == SJ_L2;
+    const bool blocks = rq.two_pass || rq.count_only;
+
+    // scratch layout: [norms P][norms Q][block counts][block offsets][scan partials]
+    size_t off_np = 0, off_nq = 0, off_cnt = 0, off_offs = 0, off_part = 0, need = 0;
+    if (l2) {
+        off_np = need;
+        need = align_up(need + (size_t)rq.n_p * 4);
+        off_nq = self ? off_np : need;
+        if (!self)
+            need = align_up(need + (size_t)rq.n_q * 4);
+    }
+    if (blocks) {
+        off_cnt = need;
+        need = align_up(need + plan.n_blocks * 4);
+        off_offs = need;
+        need = align_up(need + plan.n_blocks * 8);
+        off_part = need;
+        need = align_up(need + sjk::scan_partials_size(plan.n_blocks) * 8);
+    }
+    if ((st = grow_scratch(c, need)) != SJ_OK)
+        return st;
+    uint8_t *scr = (uint8_t *)c->scratch;
+
+    sjk::JoinArgs g = {};
+    g.P = (const uint8_t *)rq.P;
+    g.Q = (const uint8_t *)rq.Q;
+    g.n_p = rq.n_p;
+    g.n_q = rq.n_q;
+    g.row_bytes = (uint32_t)row_bytes;
+    if (rq.dtype == SJ_I8) {
+        if (!l2) {
+            const double s = std::ceil(rq.thr);
+            g.thr_i = s < -1073741824.0 ? -1073741824 : s > 1073741824.0 ? 1073741824 : (int32_t)s;
+        } else {
+            const double r = std::floor(rq.thr);
+            g.thr_i = r < -1.0 ? -1 : r > 2147483647.0 ? 2147483647 : (int32_t)r;
+        }
+    } else {
+        g.thr_f = l2 ? float_at_or_below(rq.thr) : float_at_or_above(rq.thr);
+    }
+    g.norm_p = scr + off_np;
+    g.norm_q = scr + off_nq;
+    g.pairs = rq.count_only ? nullptr : rq.pairs;
+    g.cap = rq.count_only ? 0 : rq.cap;
+    g.counter = c->d_small;
+    g.block_counts = (uint32_t *)(scr + off_cnt);
+    g.block_offsets = (const unsigned long long *)(scr + off_offs);
+    g.qsplit = plan.qsplit;
+
+    hipStream_t s = c->stream;
+    SJ_HIP(hipSetDevice(c->device));
+    if (!blocks)
+        SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
+    if (rq.timing)
+        SJ_HIP(hipEventRecord(c->ev[0], s));
+    if (l2) {
+        SJ_HIP(sjk::launch_norms(rq.dtype, g.P, rq.n_p, g.row_bytes, aligned, scr + off_np, s));
+        if (!self)
+            SJ_HIP(sjk::launch_norms(rq.dtype, g.Q, rq.n_q, g.row_bytes, aligned, scr + off_nq, s));
+    }
+    if (rq.timing)
+        SJ_HIP(hipEventRecord(c->ev[1], s));
+
+    uint64_t total = 0;
+    if (!blocks) {
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_SINGLE, aligned, g, s));
+        if (rq.timing)
+            SJ_HIP(hipEventRecord(c->ev[2], s));
+        SJ_HIP(hipMemcpyAsync(c->h_small, c->d_small, sizeof(unsigned long long),
+                              hipMemcpyDeviceToHost, s));
+        SJ_HIP(hipStreamSynchronize(s));
+        total = c->h_small[0];
+        if (rq.timing) {
+            c->stats.ms_norms = l2 ? elapsed_ms(c->ev[0], c->ev[1]) : 0.0;
+            c->stats.ms_join = elapsed_ms(c->ev[1], c->ev[2]);
+        }
+    } else {
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_COUNT, aligned, g, s));
+        if (rq.timing)
+            SJ_HIP(hipEventRecord(c->ev[2], s));
+        SJ_HIP(sjk::launch_scan(g.block_counts, plan.n_blocks,
+                                (unsigned long long *)(scr + off_offs),
+                                (unsigned long long *)(scr + off_part), c->d_small + 1, s));
+        if (rq.timing)
+            SJ_HIP(hipEventRecord(c->ev[3], s));
+        SJ_HIP(hipMemcpyAsync(c->h_small + 1, c->d_small + 1, sizeof(unsigned long long),
+                              hipMemcpyDeviceToHost, s));
+        SJ_HIP(hipStreamSynchronize(s));
+        total = c->h_small[1];
+        if (rq.timing) {
+            c->stats.ms_norms = l2 ? elapsed_ms(c->ev[0], c->ev[1]) : 0.0;
+            c->stats.ms_count = elapsed_ms(c->ev[1], c->ev[2]);
+            c->stats.ms_scan = elapsed_ms(c->ev[2], c->ev[3]);
+        }
+        if (!rq.count_only && total <= rq.cap && total > 0) {
+            if (rq.timing)
+                SJ_HIP(hipEventRecord(c->ev[4], s));
+            SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, aligned, g, s));
+            if (rq.timing)
+                SJ_HIP(hipEventRecord(c->ev[5], s));
+            SJ_HIP(hipStreamSynchronize(s));
+            if (rq.timing)
+                c->stats.ms_emit = elapsed_ms(c->ev[4], c->ev[5]);
+        }
+    }
+    c->stats.total = total;
+    c->stats.kernel = (uint32_t)plan.family;
+    c->stats.timed = rq.timing ? 1u : 0u;
+    *n_out = total;
+    if (!rq.count_only && total > rq.cap)
+        return fail(SJ_E_OVERFLOW, "%llu matches exceed the capacity of %llu pairs",
+                    (unsigned long long)total, (unsigned long long)rq.cap);
+    return SJ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sj_create(sj_ctx **out, int device, void *stream)
+{
+    g_err.clear();
+    if (!out)
+        return fail(SJ_E_INVAL, "ctx pointer is NULL");
+    *out = nullptr;
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return hip_fail(e, "hipGetDeviceCount");
+    }
+    if (device < 0 || device >= n)
+        return fail(SJ_E_INVAL, "device %d does not exist (%d visible)", device, n);
+    hipDeviceProp_t prop;
+    SJ_HIP(hipGetDeviceProperties(&prop, device));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(SJ_E_UNSUPPORTED, "device %d is %s; this library is built for gfx950", device,
+                    prop.gcnArchName);
+    SJ_HIP(hipSetDevice(device));
+    sj_ctx *c = new (std::nothrow) sj_ctx();
+    if (!c)
+        return fail(SJ_E_NOMEM, "out of host memory");
+    c->device = device;
+    c->stream = (hipStream_t)stream;
+    c->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+    if (hipMalloc(&c->d_small, 2 * sizeof(unsigned long long)) != hipSuccess ||
+        hipHostMalloc(&c->h_small, 2 * sizeof(unsigned long long), hipHostMallocDefault) !=
+            hipSuccess) {
+        (void)hipGetLastError();
+        sj_destroy(c);
+        return fail(SJ_E_NOMEM, "cannot allocate the match counter");
+    }
+    for (auto &ev : c->ev)
+        if (hipEventCreate(&ev) != hipSuccess) {
+            (void)hipGetLastError();
+            ev = nullptr;
+            sj_destroy(c);
+            return fail(SJ_E_HIP, "hipEventCreate failed");
+        }
+    *out = c;
+    return SJ_OK;
+}
+
+int sj_join_ip(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+               uint32_t d, double s, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+               unsigned flags)
+{
+    g_err.clear();
+    Request rq{SJ_IP, dtype, P, Q, n_p, n_q, d, s, pairs, cap,
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0};
+    return run(ctx, rq, n_out);
+}
+
+int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+               uint32_t d, double r2, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+               unsigned flags)
+{
+    g_err.clear();
+    Request rq{SJ_L2, dtype, P, Q, n_p, n_q, d, r2, pairs, cap,
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0};
+    return run(ctx, rq, n_out);
+}
+
+int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
+             uint32_t n_q, uint32_t d, double threshold, uint64_t *count)
+{
+    g_err.clear();
+    Request rq{metric, dtype, P, Q, n_p, n_q, d, threshold, nullptr, 0, true, true, false};
+    return run(ctx, rq, count);
+}
+
+void sj_destroy(sj_ctx *c)
+{
+    if (!c)
+        return;
+    (void)hipSetDevice(c->device);
+    if (c->stream || c->d_small)
+        (void)hipStreamSynchronize(c->stream);
+    for (auto &ev : c->ev)
+        if (ev)
+            (void)hipEventDestroy(ev);
+    if (c->scratch)
+        (void)hipFree(c->scratch);
+    if (c->d_small)
+        (void)hipFree(c->d_small);
+    if (c->h_small)
+        (void)hipHostFree(c->h_small);
+    delete c;
+}
+
+int sj_get_stats(const sj_ctx *ctx, sj_stats *out)
+{
+    if (!ctx || !out)
+        return fail(SJ_E_INVAL, "NULL argument");
+    *out = ctx->stats;
+    return SJ_OK;
+}
+
+const char *sj_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,282 @@
+// sj_aux.hip -- kernel planning and dispatch, the squared-row-norm kernel and
+// the exclusive scan of the count-then-emit protocol (gfx950).
+#include "sj_internal.h"
+
+#include <type_traits>
+
+namespace sjk {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------------ planning
+// Resident-P limits: 32-byte k-steps of the largest variant (16 for 2-byte
+// elements, 8 for int8, i.e. d <= 256 either way); workgroup of 4 waves over
+// 32 * WMB rows each; Q tiles of 64 rows.  Must agree with sj_join_kernels.h.
+static const int kResKS16[4] = {2, 4, 8, 16};
+static const int kResKS8[4] = {1, 2, 4, 8};
+static const uint32_t kResNW = 4, kResBN = 64;
+static const uint32_t kStBM = 128, kStBN = 128, kStG = 8;
+
+bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
+               Plan *plan)
+{
+    (void)metric;
+    const uint32_t ks_needed = row_bytes == 0 ? 1u : (row_bytes + 31) / 32;
+    const int *tab = dtype == DT_I8 ? kResKS8 : kResKS16;
+    int variant = -1;
+    for (int v = 0; v < 4; ++v)
+        if ((uint32_t)tab[v] >= ks_needed) {
+            variant = v;
+            break;
+        }
+    if (variant >= 0) {
+        const int ks = tab[variant];
+        const uint32_t wmb = (dtype == DT_I8 && ks <= 2) ? 4 : 2;
+        const uint32_t bm = kResNW * 32 * wmb;
+        const uint64_t n_pb = (n_p + (uint64_t)bm - 1) / bm;
+        const uint64_t n_qt = (n_q + (uint64_t)kResBN - 1) / kResBN;
+        // Enough workgroups for two per CU; splits of Q are powers of two so
+        // that, with workgroups dealt round-robin to the 8 XCDs, each XCD's
+        // workgroups sweep the same Q range (shared in that XCD's L2).
+        uint64_t qsplit = 1;
+        while (n_pb * qsplit < 2ull * (uint64_t)num_cus && qsplit * 2 <= n_qt && qsplit < 64)
+            qsplit *= 2;
+        plan->family = FAM_RESIDENT;
+        plan->variant = variant;
+        plan->qsplit = (uint32_t)qsplit;
+        plan->block = kResNW * 64;
+        const uint64_t grid = n_pb * qsplit;
+        if (grid > 0x7fffffffull)
+            return false;
+        plan->grid = (uint32_t)grid;
+        plan->n_blocks = n_pb * kResNW * n_qt;
+        return true;
+    }
+    const uint64_t n_pt = (n_p + (uint64_t)kStBM - 1) / kStBM;
+    const uint64_t n_qt = (n_q + (uint64_t)kStBN - 1) / kStBN;
+    const uint64_t groups = ((n_pt + kStG - 1) / kStG) * ((n_qt + kStG - 1) / kStG);
+    const uint64_t grid = groups * kStG * kStG;
+    if (grid > 0x7fffffffull)
+        return false;
+    plan->family = FAM_STREAMED;
+    plan->variant = 0;
+    plan->qsplit = 1;
+    plan->block = 256;
+    plan->grid = (uint32_t)grid;
+    plan->n_blocks = n_pt * n_qt * 4;
+    return true;
+}
+
+hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, bool aligned,
+                       const JoinArgs &args, hipStream_t stream)
+{
+    switch (dtype) {
+    case DT_F16: return launch_join_f16(plan, metric, mode, aligned, args, stream);
+    case DT_BF16: return launch_join_bf16(plan, metric, mode, aligned, args, stream);
+    case DT_I8: return launch_join_i8(plan, metric, mode, aligned, args, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ----------------------------------------------------------------- row norms
+// One team of TEAM lanes per row; each lane sums the squares of its 16-byte
+// chunks, the team reduces with cross-lane shuffles.  int8 sums are exact in
+// int32; fp16/bf16 sums are accumulated in fp32.
+template <int DT, int TEAM>
+__global__ void __launch_bounds__(256) row_norms(const uint8_t *X, uint32_t n, uint32_t row_bytes,
+                                                 uint32_t aligned, void *out)
+{
+    const uint64_t gt = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    const uint64_t row = gt / TEAM;
+    const uint32_t sub = (uint32_t)(gt % TEAM);
+    typedef typename std::conditional<DT == DT_I8, int, float>::type V;
+    V acc = V(0);
+    if (row < n) {
+        const uint8_t *p = X + (size_t)row * row_bytes;
+        for (uint32_t off = 16 * sub; off < row_bytes; off += 16 * TEAM) {
+            i32x4 v = {0, 0, 0, 0};
+            if (aligned) {
+                v = *(const i32x4 *)(p + off);
+            } else {
+                uint32_t w[4] = {0, 0, 0, 0};
+                for (uint32_t b = 0; b < 16 && off + b < row_bytes; ++b)
+                    w[b >> 2] |= (uint32_t)p[off + b] << (8 * (b & 3));
+                v = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+            }
+            if constexpr (DT == DT_I8) {
+#pragma unroll
+                for (int w = 0; w < 4; ++w)
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        const int x = (int)(int8_t)((uint32_t)v[w] >> (8 * b));
+                        acc += x * x;
+                    }
+            } else if constexpr (DT == DT_F16) {
+                const f16x8 h = __builtin_bit_cast(f16x8, v);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float x = (float)h[e];
+                    acc = __builtin_fmaf(x, x, acc);
+                }
+            } else {
+                const bf16x8 h = __builtin_bit_cast(bf16x8, v);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float x = (float)h[e];
+                    acc = __builtin_fmaf(x, x, acc);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int m = TEAM / 2; m > 0; m >>= 1)
+        acc += __shfl_xor(acc, m, TEAM);
+    if (row < n && sub == 0)
+        ((V *)out)[row] = acc;
+}
+
+template <int DT>
+static hipError_t norms_dt(const uint8_t *X, uint32_t n, uint32_t row_bytes, uint32_t al, void *out,
+                           hipStream_t st)
+{
+    if (row_bytes <= 128) {
+        const uint64_t threads = (uint64_t)n * 4;
+        hipLaunchKernelGGL((row_norms<DT, 4>), dim3((uint32_t)((threads + 255) / 256)), dim3(256), 0,
+                           st, X, n, row_bytes, al, out);
+    } else {
+        const uint64_t threads = (uint64_t)n * 32;
+        hipLaunchKernelGGL((row_norms<DT, 32>), dim3((uint32_t)((threads + 255) / 256)), dim3(256),
+                           0, st, X, n, row_bytes, al, out);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, bool aligned,
+                        void *out, hipStream_t stream)
+{
+    if (n == 0)
+        return hipSuccess;
+    const uint32_t al = aligned ? 1u : 0u;
+    switch (dtype) {
+    case DT_F16: return norms_dt<DT_F16>(X, n, row_bytes, al, out, stream);
+    case DT_BF16: return norms_dt<DT_BF16>(X, n, row_bytes, al, out, stream);
+    case DT_I8: return norms_dt<DT_I8>(X, n, row_bytes, al, out, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------- scan
+// Exclusive scan of uint32 block counts into uint64 offsets, in three kernels:
+// per-chunk sums, a scan of the chunk sums by one workgroup (which also writes
+// the total), and a rescan of every chunk from its offset.
+static const uint32_t kScanT = 256, kScanE = 16, kScanChunk = kScanT * kScanE;
+
+uint64_t scan_partials_size(uint64_t n) { return (n + kScanChunk - 1) / kScanChunk + 1; }
+
+__device__ __forceinline__ unsigned long long wave_incl_scan(unsigned long long v, int lane)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long u = __shfl_up(v, o, 64);
+        if (lane >= o)
+            v += u;
+    }
+    return v;
+}
+
+// Exclusive scan over the 256 threads of a workgroup; returns the workgroup sum.
+__device__ __forceinline__ unsigned long long block_excl_scan(unsigned long long v,
+                                                              unsigned long long &excl)
+{
+    __shared__ unsigned long long s_w[kScanT / 64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const unsigned long long inc = wave_incl_scan(v, lane);
+    if (lane == 63)
+        s_w[w] = inc;
+    __syncthreads();
+    unsigned long long before = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < (int)(kScanT / 64); ++k) {
+        if (k < w)
+            before += s_w[k];
+        total += s_w[k];
+    }
+    excl = before + inc - v;
+    __syncthreads();
+    return total;
+}
+
+__global__ void __launch_bounds__(256) scan_reduce(const uint32_t *c, uint64_t n,
+                                                   unsigned long long *partials)
+{
+    const uint64_t base = (uint64_t)blockIdx.x * kScanChunk + (uint64_t)threadIdx.x * kScanE;
+    unsigned long long s = 0;
+#pragma unroll
+    for (uint32_t e = 0; e < kScanE; ++e)
+        if (base + e < n)
+            s += c[base + e];
+    unsigned long long excl;
+    const unsigned long long tot = block_excl_scan(s, excl);
+    if (threadIdx.x == 0)
+        partials[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(256) scan_top(unsigned long long *partials, uint64_t np,
+                                                unsigned long long *total)
+{
+    unsigned long long carry = 0;
+    for (uint64_t b = 0; b < np; b += kScanT) {
+        const uint64_t k = b + threadIdx.x;
+        const unsigned long long v = k < np ? partials[k] : 0ull;
+        unsigned long long excl;
+        const unsigned long long tot = block_excl_scan(v, excl);
+        if (k < np)
+            partials[k] = carry + excl;
+        carry += tot;
+    }
+    if (threadIdx.x == 0)
+        *total = carry;
+}
+
+__global__ void __launch_bounds__(256) scan_apply(const uint32_t *c, uint64_t n,
+                                                  const unsigned long long *partials,
+                                                  unsigned long long *offsets)
+{
+    const uint64_t base = (uint64_t)blockIdx.x * kScanChunk + (uint64_t)threadIdx.x * kScanE;
+    uint32_t v[kScanE];
+    unsigned long long s = 0;
+#pragma unroll
+    for (uint32_t e = 0; e < kScanE; ++e) {
+        v[e] = base + e < n ? c[base + e] : 0u;
+        s += v[e];
+    }
+    unsigned long long excl;
+    block_excl_scan(s, excl);
+    unsigned long long run = partials[blockIdx.x] + excl;
+#pragma unroll
+    for (uint32_t e = 0; e < kScanE; ++e)
+        if (base + e < n) {
+            offsets[base + e] = run;
+            run += v[e];
+        }
+}
+
+hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *offsets,
+                       unsigned long long *partials, unsigned long long *total, hipStream_t stream)
+{
+    const uint64_t np = (n + kScanChunk - 1) / kScanChunk;
+    if (np > 0x7fffffffull)
+        return hipErrorInvalidValue;
+    if (np)
+        hipLaunchKernelGGL(scan_reduce, dim3((uint32_t)np), dim3(kScanT), 0, stream, counts, n,
+                           partials);
+    hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanT), 0, stream, partials, np, total);
+    if (np)
+        hipLaunchKernelGGL(scan_apply, dim3((uint32_t)np), dim3(kScanT), 0, stream, counts, n,
+                           partials, offsets);
+    return hipGetLastError();
+}
+
+}  // namespace sjk

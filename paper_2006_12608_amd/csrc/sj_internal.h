@@ -1,0 +1,80 @@
+// sj_internal.h -- interface between the host API (sj_api.cpp) and the gfx950
+// kernels (sj_kernels_*.hip).  Not part of the public C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sjk {
+
+enum { DT_F16 = 1, DT_BF16 = 2, DT_I8 = 3 };
+enum { MET_IP = 0, MET_L2 = 1 };
+
+// What the fused epilogue does with the matches it finds.
+enum Mode {
+    MODE_SINGLE = 0,  // append through one atomic counter per wave (single pass)
+    MODE_COUNT = 1,   // count the matches of every output block, write no pairs
+    MODE_EMIT = 2     // write each block's matches at its precomputed offset
+};
+
+// Kernel families.
+enum Family {
+    FAM_RESIDENT = 1,  // P rows held in VGPRs for the whole of d; Q tiles streamed via LDS
+    FAM_STREAMED = 2   // both operands streamed through LDS in K chunks (large d)
+};
+
+struct JoinArgs {
+    const uint8_t *P;            // n_p rows of row_bytes bytes
+    const uint8_t *Q;            // n_q rows of row_bytes bytes
+    uint32_t n_p, n_q;
+    uint32_t row_bytes;          // d * element size
+    float thr_f;                 // fp16/bf16: IP s32 (acc >= thr_f); L2 r2_32
+    int32_t thr_i;               // int8: IP ceil(s) (acc >= thr_i); L2 floor(r2)
+    const void *norm_p;          // L2: squared norms of P rows (int32 for int8, float otherwise)
+    const void *norm_q;          // L2: squared norms of Q rows
+    uint32_t *pairs;             // cap x {i, j}
+    uint64_t cap;
+    unsigned long long *counter; // MODE_SINGLE: running match count
+    uint32_t *block_counts;      // MODE_COUNT: one count per output block
+    const unsigned long long *block_offsets;  // MODE_EMIT: exclusive prefix of block_counts
+    uint32_t qsplit;             // FAM_RESIDENT: Q ranges per P block
+};
+
+// A launch decided by plan_join; the count and emit passes of one call use the
+// same plan so that their output blocks coincide.
+struct Plan {
+    int family;
+    int variant;                 // index into the family's instantiation table
+    uint32_t grid, block;
+    uint32_t qsplit;
+    uint64_t n_blocks;           // number of output blocks (entries of block_counts)
+};
+
+// Chooses the kernel for (dtype, metric, shape) on a GPU with `num_cus` CUs.
+// Returns false when the shape is unsupported.
+bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes,
+               int num_cus, Plan *plan);
+
+hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, bool aligned,
+                       const JoinArgs &args, hipStream_t stream);
+
+// Squared row norms: out[i] = sum_k X[i][k]^2 (int32 for int8, fp32 otherwise).
+hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, bool aligned,
+                        void *out, hipStream_t stream);
+
+// Exclusive scan of n uint32 counts into n uint64 offsets; *total receives the
+// sum.  `partials` needs scan_partials_size(n) elements of scratch.
+uint64_t scan_partials_size(uint64_t n);
+hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *offsets,
+                       unsigned long long *partials, unsigned long long *total,
+                       hipStream_t stream);
+
+// Per-dtype launchers (one translation unit per element type).
+hipError_t launch_join_f16(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
+                           hipStream_t);
+hipError_t launch_join_bf16(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
+                            hipStream_t);
+hipError_t launch_join_i8(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
+                          hipStream_t);
+
+}  // namespace sjk

@@ -1,0 +1,13 @@
+// sj_join_bf16.hip -- instantiates the fused join kernels for BF16 inputs
+// (kept in its own translation unit so the element types compile in parallel).
+#include "sj_join_kernels.h"
+
+namespace sjk {
+
+hipError_t launch_join_bf16(const Plan &p, int metric, int mode, bool aligned, const JoinArgs &g,
+                          hipStream_t st)
+{
+    return launch_dtype<DT_BF16>(p, metric, mode, aligned, g, st);
+}
+
+}  // namespace sjk

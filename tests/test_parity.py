@@ -1,0 +1,245 @@
+"""GPU library vs the oracle, element by element (pair sets), on seeded inputs.
+
+Integer-valued inputs must give identical pair sets; real-valued inputs must
+agree outside the boundary band 1e-3 * |threshold| (those pairs are excluded
+and counted).  Cases cover every kernel variant (d picks the k-step variant;
+d > 256 takes the K-streamed kernel), ragged n against the tile sizes,
+unaligned rows, both metrics, both modes, edge cases, and the full-size
+workloads on sampled rows.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_util import compare, gpu_join, sorted_pairs, to_device
+from pins import values
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2006_12608_amd  # noqa: F401  (fails loudly when libsj.so is missing)
+    yield
+    torch.cuda.synchronize()
+
+
+def run_case(w, thr=None, two_pass=False, rows=None):
+    thr = w.threshold if thr is None else thr
+    Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
+    if w.self_join:
+        Qd = Pd
+    say(w.name, w.metric, w.dtype, w.n_p, w.n_q, w.d, thr, "two_pass" if two_pass else "single")
+    g = sorted_pairs(gpu_join(w.metric, Pd, Qd, thr, two_pass=two_pass))
+    band = 1e-3 * abs(thr) if w.real_valued else 0.0
+    ref = oracle.join(w.metric, w.dtype, w.P, w.Q, thr, band=band, rows=rows)
+    if rows is not None:
+        g = g[np.isin(g[:, 0], np.asarray(rows))]
+    return compare(g, ref, w.real_valued), g, ref
+
+
+# ------------------------------------------------------- the five workloads
+
+@pytest.mark.parametrize("k,n", [(0, None), (1, 2048), (2, 2048), (3, 4096), (4, 1024)])
+@pytest.mark.parametrize("two_pass", [False, True])
+def test_workload_reduced(k, n, two_pass):
+    w = workloads.make_config(k, n=n)
+    info, g, ref = run_case(w, two_pass=two_pass)
+    if w.planted.size:
+        assert set(map(tuple, w.planted.tolist())) <= set(map(tuple, g.astype(np.int64).tolist()))
+    if w.real_valued:
+        say("band", info)
+
+
+def test_c0_true_self_join():
+    w = workloads.make_config(0, self_join=True)
+    _, g, _ = run_case(w)
+    s = set(map(tuple, g.tolist()))
+    assert s == {(j, i) for (i, j) in s}
+
+
+# ------------------------------------------------------ random shapes
+
+DIMS = [1, 7, 16, 33, 64, 65, 100, 128, 200, 256, 257, 600, 1024]
+SHAPES = [(300, 517), (70, 1), (1030, 129), (513, 64)]
+
+
+def _case(seed, dtype, d, shape, metric):
+    n_p, n_q = shape
+    lo, hi = (-8, 8) if dtype != "i8" else (-128, 127)
+    if dtype != "i8" and metric == "l2":
+        lo, hi = -20, 20
+    w = workloads.random_case(seed, n_p, n_q, d, dtype, lo=lo, hi=hi, metric=metric)
+    x = values(dtype, w.P).astype(np.int64)
+    y = values(dtype, w.Q).astype(np.int64)
+    if metric == "ip":
+        S = x @ y.T
+        q = 0.5 if seed % 3 == 0 else 0.99
+        w.threshold = float(np.quantile(S, q, method="nearest"))
+    else:
+        D = (x * x).sum(1)[:, None] + (y * y).sum(1)[None, :] - 2 * (x @ y.T)
+        q = 0.5 if seed % 3 == 0 else 0.01
+        w.threshold = float(np.quantile(D, q, method="nearest"))
+    return w
+
+
+@pytest.mark.parametrize("metric", ["ip", "l2"])
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+@pytest.mark.parametrize("d", DIMS)
+def test_random_shapes(d, dtype, metric):
+    seed = 100 + DIMS.index(d) * 7 + ["f16", "bf16", "i8"].index(dtype) * 3 + (metric == "l2")
+    shape = SHAPES[seed % len(SHAPES)]
+    w = _case(seed, dtype, d, shape, metric)
+    run_case(w, two_pass=(seed % 2 == 1))
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("metric", ["ip", "l2"])
+def test_real_valued_band(dtype, metric):
+    w = workloads.random_case(7, 700, 900, 96, dtype, real=True, metric=metric)
+    x, y = values(dtype, w.P), values(dtype, w.Q)
+    if metric == "ip":
+        thr = float(np.quantile(x @ y.T, 0.995))
+    else:
+        D = (x * x).sum(1)[:, None] + (y * y).sum(1)[None, :] - 2 * (x @ y.T)
+        thr = float(np.quantile(D, 0.01))
+    info, _, _ = run_case(w, thr=thr)
+    say("band", info)
+
+
+# ------------------------------------------------------- protocol / edges
+
+def test_two_pass_is_deterministic_and_equals_single():
+    import torch
+    w = workloads.make_config(4, n=1024)
+    Pd, Qd = to_device(w.P, "bf16"), to_device(w.Q, "bf16")
+    say("two-pass determinism c4@1024")
+    a = gpu_join("ip", Pd, Qd, w.threshold, two_pass=True)
+    b = gpu_join("ip", Pd, Qd, w.threshold, two_pass=True)
+    assert torch.equal(a, b)            # same order, not only the same set
+    c = gpu_join("ip", Pd, Qd, w.threshold, two_pass=False)
+    assert np.array_equal(sorted_pairs(a), sorted_pairs(c))
+
+
+def test_overflow_reports_exact_total():
+    import torch
+    import paper_2006_12608_amd as sj
+    w = workloads.make_config(0)
+    Pd, Qd = to_device(w.P, "f16"), to_device(w.Q, "f16")
+    total = oracle.count("ip", "f16", w.P, w.Q, w.threshold)
+    say("overflow", total)
+    assert sj.count(Pd, Qd, w.threshold) == total
+    for two_pass in (False, True):
+        for cap in (0, total - 1):
+            out = torch.empty((max(cap, 1), 2), dtype=torch.int32, device="cuda")
+            with pytest.raises(sj.SjError) as e:
+                sj.join_ip(Pd, Qd, w.threshold, cap=cap, out=out, two_pass=two_pass)
+            assert e.value.status == sj.SJ_E_OVERFLOW and e.value.n_out == total
+        out = torch.empty((total, 2), dtype=torch.int32, device="cuda")
+        r = sj.join_ip(Pd, Qd, w.threshold, cap=total, out=out, two_pass=two_pass)
+        assert r.shape[0] == total
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "i8"])
+def test_extreme_thresholds(dtype):
+    import paper_2006_12608_amd as sj
+    w = workloads.random_case(3, 130, 70, 40, dtype)
+    Pd, Qd = to_device(w.P, dtype), to_device(w.Q, dtype)
+    say("extreme thresholds", dtype)
+    for metric in ("ip", "l2"):
+        f = sj.join_ip if metric == "ip" else sj.join_l2
+        all_thr, none_thr = (-np.inf, np.inf) if metric == "ip" else (np.inf, -np.inf)
+        assert f(Pd, Qd, all_thr).shape[0] == 130 * 70
+        assert f(Pd, Qd, none_thr).shape[0] == 0
+        big = 1e30 if metric == "ip" else -1.0
+        assert f(Pd, Qd, big).shape[0] == 0
+        huge = -1e30 if metric == "ip" else 1e30
+        assert sj.count(Pd, Qd, huge, metric) == 130 * 70
+
+
+def test_ties_are_inclusive():
+    """Rows with known exact scores at the threshold are reported; one above is not."""
+    rng = np.random.default_rng(5)
+    for dtype in ("f16", "bf16", "i8"):
+        x = rng.integers(-5, 6, size=(40, 24))
+        w = workloads.Workload("ties", "ip", dtype, workloads.encode(x, dtype),
+                               workloads.encode(x, dtype), 0.0, np.zeros((0, 2), np.int64))
+        S = x @ x.T
+        for s in (float(S[3, 7]), float(S[3, 7]) + 1):
+            run_case(w, thr=s)
+
+
+def test_empty_and_zero_dim():
+    import torch
+    import paper_2006_12608_amd as sj
+    say("empty inputs")
+    P = torch.zeros((0, 16), dtype=torch.float16, device="cuda")
+    Q = torch.ones((5, 16), dtype=torch.float16, device="cuda")
+    assert sj.join_ip(P, Q, 0.0).shape[0] == 0
+    assert sj.join_l2(Q, P, 0.0).shape[0] == 0
+    assert sj.count(P, Q, -1.0) == 0
+    # d = 0: every score is 0, so everything matches s <= 0 and nothing s > 0
+    P0 = torch.zeros((7, 0), dtype=torch.int8, device="cuda")
+    Q0 = torch.zeros((9, 0), dtype=torch.int8, device="cuda")
+    assert sj.join_ip(P0, Q0, 0.0).shape[0] == 63
+    assert sj.join_ip(P0, Q0, 0.5).shape[0] == 0
+    assert sj.join_l2(P0, Q0, 0.0).shape[0] == 63
+
+
+def test_self_join_same_pointer_all_variants():
+    for dtype, d in (("f16", 64), ("bf16", 300), ("i8", 64), ("i8", 500)):
+        w = workloads.random_case(11, 333, 333, d, dtype, lo=-3, hi=3)
+        w.Q = w.P
+        w.self_join = True
+        x = values(dtype, w.P).astype(np.int64)
+        w.threshold = float(np.quantile(x @ x.T, 0.98, method="nearest"))
+        _, g, _ = run_case(w)
+        s = set(map(tuple, g.tolist()))
+        assert s == {(j, i) for (i, j) in s}
+
+
+# ------------------------------------------------ full-size, sampled rows
+
+def _sample_rows(n, k, seed):
+    rng = np.random.default_rng(seed)
+    return np.sort(rng.choice(n, size=k, replace=False))
+
+
+@pytest.mark.parametrize("k,n_rows,two_pass", [(1, 48, False), (2, 12, False), (3, 12, False),
+                                                (4, 8, True)])
+def test_full_size_sampled_rows(k, n_rows, two_pass):
+    """The full workload on the GPU in the launch configuration the benchmark
+    uses; the oracle recomputes a sample of P's rows against all of Q."""
+    import torch
+    import paper_2006_12608_amd as sj
+    w = workloads.make_config(k)
+    Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
+    rows = _sample_rows(w.n_p, n_rows, 77 + k)
+    if w.planted.size:   # include some planted rows
+        rows = np.unique(np.concatenate([rows, w.planted[:4, 0]]))
+    say("full size", w.name, "rows", rows.size, "two_pass", two_pass)
+    total = sj.count(Pd, Qd, w.threshold, w.metric)
+    out = torch.empty((total, 2), dtype=torch.int32, device="cuda")
+    f = sj.join_ip if w.metric == "ip" else sj.join_l2
+    pairs = f(Pd, Qd, w.threshold, cap=total, out=out, two_pass=two_pass)
+    assert pairs.shape[0] == total
+    sel = torch.isin(pairs[:, 0], torch.from_numpy(rows.astype(np.int32)).cuda())
+    g = sorted_pairs(pairs[sel])
+    band = 1e-3 * abs(w.threshold) if w.real_valued else 0.0
+    ref = oracle.join(w.metric, w.dtype, w.P, w.Q, w.threshold, rows=rows, band=band)
+    info = compare(g, ref, w.real_valued)
+    say("total", total, "sampled", ref.total, info)
+    if w.planted.size:
+        pl = w.planted[np.isin(w.planted[:, 0], rows)]
+        assert set(map(tuple, pl.tolist())) <= set(map(tuple, g.astype(np.int64).tolist()))

@@ -14,4 +14,5 @@ from .gen import (  # noqa: F401
     bf16_bits_from_f32,
     DTYPES,
     ESIZE,
+    to_torch,
 )

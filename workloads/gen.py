@@ -266,3 +266,19 @@ def random_case(seed: int, n_p: int, n_q: int, d: int, dtype: str, lo: int = -4,
         Qv = rng.integers(lo, hi + 1, size=(n_q, d))
     return Workload(f"rand{seed}_{n_p}x{n_q}x{d}_{dtype}", metric, dtype, encode(Pv, dtype),
                     encode(Qv, dtype), threshold, np.zeros((0, 2), np.int64), real_valued=real)
+
+
+def to_torch(X: np.ndarray, dtype: str, device="cuda"):
+    """The storage array as a torch tensor of the matching element type
+    (float16, bfloat16 or int8) on `device`."""
+    import torch
+    X = np.ascontiguousarray(X)
+    if dtype == "f16":
+        t = torch.from_numpy(X)
+    elif dtype == "bf16":
+        t = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16)
+    elif dtype == "i8":
+        t = torch.from_numpy(X)
+    else:
+        raise ValueError(dtype)
+    return t.to(device)
