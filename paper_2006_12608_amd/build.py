@@ -19,8 +19,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["sj_api.cpp", "sj_aux.hip", "sj_join_f16.hip", "sj_join_bf16.hip", "sj_join_i8.hip"]
 # Packed-fp32 instructions are kept out of the generated code (they are not
 # needed here and some of their forms are unreliable on this hardware).
+# MFMA results stay in arch VGPRs so the fused epilogue reads them directly.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 

@@ -194,18 +194,33 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         return SJ_OK;
 
     sjk::Plan plan;
-    if (!sjk::plan_join(rq.dtype, rq.metric, rq.n_p, rq.n_q, (uint32_t)row_bytes, c->num_cus,
-                        &plan))
+    if (!sjk::plan_join(rq.dtype, rq.metric, rq.n_p, rq.n_q,
+                        (uint32_t)(row_bytes == 0 ? 16 : (row_bytes + 15) & ~(size_t)15),
+                        c->num_cus, &plan))
         return fail(SJ_E_UNSUPPORTED, "shape %u x %u x %u is too large for one launch", rq.n_p,
                     rq.n_q, rq.d);
-    const bool aligned = row_bytes % 16 == 0 && ((uintptr_t)rq.P % 16) == 0 &&
+    // The kernels read rows as 16-byte chunks: inputs whose rows are not
+    // 16-byte aligned are first repacked into zero-padded rows (zero columns
+    // change neither inner products nor squared distances).
+    // d = 0 takes the same path: one zero chunk per row (every score is 0).
+    const bool aligned = row_bytes > 0 && row_bytes % 16 == 0 && ((uintptr_t)rq.P % 16) == 0 &&
                          ((uintptr_t)rq.Q % 16) == 0;
+    const size_t krow = row_bytes == 0 ? 16 : (row_bytes + 15) & ~(size_t)15;
     const bool self = rq.P == rq.Q && rq.n_p == rq.n_q;
     const bool l2 = rq.metric == SJ_L2;
     const bool blocks = rq.two_pass || rq.count_only;
 
-    // scratch layout: [norms P][norms Q][block counts][block offsets][scan partials]
+    // scratch layout: [repacked P][repacked Q][norms P][norms Q][block counts]
+    //                 [block offsets][scan partials]
+    size_t off_rp = 0, off_rq = 0;
     size_t off_np = 0, off_nq = 0, off_cnt = 0, off_offs = 0, off_part = 0, need = 0;
+    if (!aligned) {
+        off_rp = need;
+        need = align_up(need + (size_t)rq.n_p * krow);
+        off_rq = self ? off_rp : need;
+        if (!self)
+            need = align_up(need + (size_t)rq.n_q * krow);
+    }
     if (l2) {
         off_np = need;
         need = align_up(need + (size_t)rq.n_p * 4);
@@ -226,11 +241,11 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     uint8_t *scr = (uint8_t *)c->scratch;
 
     sjk::JoinArgs g = {};
-    g.P = (const uint8_t *)rq.P;
-    g.Q = (const uint8_t *)rq.Q;
+    g.P = aligned ? (const uint8_t *)rq.P : scr + off_rp;
+    g.Q = aligned ? (const uint8_t *)rq.Q : scr + off_rq;
     g.n_p = rq.n_p;
     g.n_q = rq.n_q;
-    g.row_bytes = (uint32_t)row_bytes;
+    g.row_bytes = (uint32_t)krow;
     if (rq.dtype == SJ_I8) {
         if (!l2) {
             const double s = std::ceil(rq.thr);
@@ -257,17 +272,24 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
     if (rq.timing)
         SJ_HIP(hipEventRecord(c->ev[0], s));
-    if (l2) {
-        SJ_HIP(sjk::launch_norms(rq.dtype, g.P, rq.n_p, g.row_bytes, aligned, scr + off_np, s));
+    if (!aligned) {
+        SJ_HIP(sjk::launch_repack((const uint8_t *)rq.P, rq.n_p, (uint32_t)row_bytes,
+                                  scr + off_rp, (uint32_t)krow, s));
         if (!self)
-            SJ_HIP(sjk::launch_norms(rq.dtype, g.Q, rq.n_q, g.row_bytes, aligned, scr + off_nq, s));
+            SJ_HIP(sjk::launch_repack((const uint8_t *)rq.Q, rq.n_q, (uint32_t)row_bytes,
+                                      scr + off_rq, (uint32_t)krow, s));
+    }
+    if (l2) {
+        SJ_HIP(sjk::launch_norms(rq.dtype, g.P, rq.n_p, g.row_bytes, scr + off_np, s));
+        if (!self)
+            SJ_HIP(sjk::launch_norms(rq.dtype, g.Q, rq.n_q, g.row_bytes, scr + off_nq, s));
     }
     if (rq.timing)
         SJ_HIP(hipEventRecord(c->ev[1], s));
 
     uint64_t total = 0;
     if (!blocks) {
-        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_SINGLE, aligned, g, s));
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_SINGLE, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(hipMemcpyAsync(c->h_small, c->d_small, sizeof(unsigned long long),
@@ -279,7 +301,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
             c->stats.ms_join = elapsed_ms(c->ev[1], c->ev[2]);
         }
     } else {
-        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_COUNT, aligned, g, s));
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_COUNT, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(sjk::launch_scan(g.block_counts, plan.n_blocks,
@@ -299,7 +321,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         if (!rq.count_only && total <= rq.cap && total > 0) {
             if (rq.timing)
                 SJ_HIP(hipEventRecord(c->ev[4], s));
-            SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, aligned, g, s));
+            SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, g, s));
             if (rq.timing)
                 SJ_HIP(hipEventRecord(c->ev[5], s));
             SJ_HIP(hipStreamSynchronize(s));

@@ -13,10 +13,12 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 // ------------------------------------------------------------------ planning
 // Resident-P limits: 32-byte k-steps of the largest variant (16 for 2-byte
 // elements, 8 for int8, i.e. d <= 256 either way); workgroup of 4 waves over
-// 32 * WMB rows each; Q tiles of 64 rows.  Must agree with sj_join_kernels.h.
+// 32 * WMB rows each; Q tiles of 128 rows (64 for the longest rows).  Must
+// agree with sj_join_kernels.h.
 static const int kResKS16[4] = {2, 4, 8, 16};
 static const int kResKS8[4] = {1, 2, 4, 8};
-static const uint32_t kResNW = 4, kResBN = 64;
+static const uint32_t kResNW = 4;
+static uint32_t res_bn(int ks) { return ks <= 8 ? 128 : 64; }
 static const uint32_t kStBM = 128, kStBN = 128, kStG = 8;
 
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
@@ -36,7 +38,8 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
         const uint32_t wmb = (dtype == DT_I8 && ks <= 2) ? 4 : 2;
         const uint32_t bm = kResNW * 32 * wmb;
         const uint64_t n_pb = (n_p + (uint64_t)bm - 1) / bm;
-        const uint64_t n_qt = (n_q + (uint64_t)kResBN - 1) / kResBN;
+        const uint64_t bn = res_bn(ks);
+        const uint64_t n_qt = (n_q + bn - 1) / bn;
         // Enough workgroups for two per CU; splits of Q are powers of two so
         // that, with workgroups dealt round-robin to the 8 XCDs, each XCD's
         // workgroups sweep the same Q range (shared in that XCD's L2).
@@ -69,13 +72,13 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
     return true;
 }
 
-hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, bool aligned,
-                       const JoinArgs &args, hipStream_t stream)
+hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, const JoinArgs &args,
+                       hipStream_t stream)
 {
     switch (dtype) {
-    case DT_F16: return launch_join_f16(plan, metric, mode, aligned, args, stream);
-    case DT_BF16: return launch_join_bf16(plan, metric, mode, aligned, args, stream);
-    case DT_I8: return launch_join_i8(plan, metric, mode, aligned, args, stream);
+    case DT_F16: return launch_join_f16(plan, metric, mode, args, stream);
+    case DT_BF16: return launch_join_bf16(plan, metric, mode, args, stream);
+    case DT_I8: return launch_join_i8(plan, metric, mode, args, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -86,7 +89,7 @@ hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, bool a
 // int32; fp16/bf16 sums are accumulated in fp32.
 template <int DT, int TEAM>
 __global__ void __launch_bounds__(256) row_norms(const uint8_t *X, uint32_t n, uint32_t row_bytes,
-                                                 uint32_t aligned, void *out)
+                                                 void *out)
 {
     const uint64_t gt = (uint64_t)blockIdx.x * 256 + threadIdx.x;
     const uint64_t row = gt / TEAM;
@@ -96,15 +99,7 @@ __global__ void __launch_bounds__(256) row_norms(const uint8_t *X, uint32_t n, u
     if (row < n) {
         const uint8_t *p = X + (size_t)row * row_bytes;
         for (uint32_t off = 16 * sub; off < row_bytes; off += 16 * TEAM) {
-            i32x4 v = {0, 0, 0, 0};
-            if (aligned) {
-                v = *(const i32x4 *)(p + off);
-            } else {
-                uint32_t w[4] = {0, 0, 0, 0};
-                for (uint32_t b = 0; b < 16 && off + b < row_bytes; ++b)
-                    w[b >> 2] |= (uint32_t)p[off + b] << (8 * (b & 3));
-                v = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-            }
+            const i32x4 v = *(const i32x4 *)(p + off);
             if constexpr (DT == DT_I8) {
 #pragma unroll
                 for (int w = 0; w < 4; ++w)
@@ -138,33 +133,66 @@ __global__ void __launch_bounds__(256) row_norms(const uint8_t *X, uint32_t n, u
 }
 
 template <int DT>
-static hipError_t norms_dt(const uint8_t *X, uint32_t n, uint32_t row_bytes, uint32_t al, void *out,
+static hipError_t norms_dt(const uint8_t *X, uint32_t n, uint32_t row_bytes, void *out,
                            hipStream_t st)
 {
     if (row_bytes <= 128) {
         const uint64_t threads = (uint64_t)n * 4;
         hipLaunchKernelGGL((row_norms<DT, 4>), dim3((uint32_t)((threads + 255) / 256)), dim3(256), 0,
-                           st, X, n, row_bytes, al, out);
+                           st, X, n, row_bytes, out);
     } else {
         const uint64_t threads = (uint64_t)n * 32;
         hipLaunchKernelGGL((row_norms<DT, 32>), dim3((uint32_t)((threads + 255) / 256)), dim3(256),
-                           0, st, X, n, row_bytes, al, out);
+                           0, st, X, n, row_bytes, out);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, bool aligned,
-                        void *out, hipStream_t stream)
+hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, void *out,
+                        hipStream_t stream)
 {
     if (n == 0)
         return hipSuccess;
-    const uint32_t al = aligned ? 1u : 0u;
     switch (dtype) {
-    case DT_F16: return norms_dt<DT_F16>(X, n, row_bytes, al, out, stream);
-    case DT_BF16: return norms_dt<DT_BF16>(X, n, row_bytes, al, out, stream);
-    case DT_I8: return norms_dt<DT_I8>(X, n, row_bytes, al, out, stream);
+    case DT_F16: return norms_dt<DT_F16>(X, n, row_bytes, out, stream);
+    case DT_BF16: return norms_dt<DT_BF16>(X, n, row_bytes, out, stream);
+    case DT_I8: return norms_dt<DT_I8>(X, n, row_bytes, out, stream);
     }
     return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------------- repack
+// One thread per 4-byte word of the destination, gathered byte by byte (only
+// inputs whose rows are not 16-byte aligned take this path).
+__global__ void __launch_bounds__(256) repack_rows(const uint8_t *src, uint32_t n,
+                                                   uint32_t src_bytes, uint8_t *dst,
+                                                   uint32_t dst_bytes)
+{
+    const uint64_t words = (uint64_t)n * (dst_bytes / 4);
+    for (uint64_t w = (uint64_t)blockIdx.x * 256 + threadIdx.x; w < words;
+         w += (uint64_t)gridDim.x * 256) {
+        const uint64_t row = w / (dst_bytes / 4);
+        const uint32_t col = (uint32_t)(w % (dst_bytes / 4)) * 4;
+        uint32_t v = 0;
+#pragma unroll
+        for (uint32_t b = 0; b < 4; ++b)
+            if (col + b < src_bytes)
+                v |= (uint32_t)src[row * src_bytes + col + b] << (8 * b);
+        *(uint32_t *)(dst + row * dst_bytes + col) = v;
+    }
+}
+
+hipError_t launch_repack(const uint8_t *src, uint32_t n, uint32_t src_bytes, uint8_t *dst,
+                         uint32_t dst_bytes, hipStream_t stream)
+{
+    if (n == 0)
+        return hipSuccess;
+    const uint64_t words = (uint64_t)n * (dst_bytes / 4);
+    const uint64_t blocks = (words + 255) / 256;
+    const uint32_t grid = (uint32_t)(blocks < 65536 ? blocks : 65536);
+    hipLaunchKernelGGL(repack_rows, dim3(grid), dim3(256), 0, stream, src, n, src_bytes, dst,
+                       dst_bytes);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------- scan

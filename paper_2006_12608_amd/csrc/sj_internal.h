@@ -27,7 +27,7 @@ struct JoinArgs {
     const uint8_t *P;            // n_p rows of row_bytes bytes
     const uint8_t *Q;            // n_q rows of row_bytes bytes
     uint32_t n_p, n_q;
-    uint32_t row_bytes;          // d * element size
+    uint32_t row_bytes;          // bytes per row: a multiple of 16, rows 16-byte aligned
     float thr_f;                 // fp16/bf16: IP s32 (acc >= thr_f); L2 r2_32
     int32_t thr_i;               // int8: IP ceil(s) (acc >= thr_i); L2 floor(r2)
     const void *norm_p;          // L2: squared norms of P rows (int32 for int8, float otherwise)
@@ -55,12 +55,18 @@ struct Plan {
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes,
                int num_cus, Plan *plan);
 
-hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, bool aligned,
-                       const JoinArgs &args, hipStream_t stream);
+hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, const JoinArgs &args,
+                       hipStream_t stream);
 
 // Squared row norms: out[i] = sum_k X[i][k]^2 (int32 for int8, fp32 otherwise).
-hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, bool aligned,
-                        void *out, hipStream_t stream);
+// Rows as in JoinArgs (16-byte aligned, row_bytes a multiple of 16).
+hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_bytes, void *out,
+                        hipStream_t stream);
+
+// Copies n rows of src_bytes bytes (any alignment) into rows of dst_bytes
+// bytes (dst_bytes >= src_bytes, a multiple of 16), zero-filling the tail.
+hipError_t launch_repack(const uint8_t *src, uint32_t n, uint32_t src_bytes, uint8_t *dst,
+                         uint32_t dst_bytes, hipStream_t stream);
 
 // Exclusive scan of n uint32 counts into n uint64 offsets; *total receives the
 // sum.  `partials` needs scan_partials_size(n) elements of scratch.
@@ -70,11 +76,8 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
                        hipStream_t stream);
 
 // Per-dtype launchers (one translation unit per element type).
-hipError_t launch_join_f16(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
-                           hipStream_t);
-hipError_t launch_join_bf16(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
-                            hipStream_t);
-hipError_t launch_join_i8(const Plan &, int metric, int mode, bool aligned, const JoinArgs &,
-                          hipStream_t);
+hipError_t launch_join_f16(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
+hipError_t launch_join_bf16(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
+hipError_t launch_join_i8(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
 
 }  // namespace sjk

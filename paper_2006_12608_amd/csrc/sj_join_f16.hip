@@ -4,10 +4,10 @@
 
 namespace sjk {
 
-hipError_t launch_join_f16(const Plan &p, int metric, int mode, bool aligned, const JoinArgs &g,
+hipError_t launch_join_f16(const Plan &p, int metric, int mode, const JoinArgs &g,
                           hipStream_t st)
 {
-    return launch_dtype<DT_F16>(p, metric, mode, aligned, g, st);
+    return launch_dtype<DT_F16>(p, metric, mode, g, st);
 }
 
 }  // namespace sjk

@@ -74,27 +74,15 @@ __device__ __forceinline__ float big_val<float>() { return __builtin_inff(); }
 template <>
 __device__ __forceinline__ int big_val<int>() { return 0x3fffffff; }
 
-// 16 bytes at byte `off` of row `row`, zero outside the row or past n_rows.
-// `aligned` (uniform): row_bytes % 16 == 0 and the base is 16-byte aligned, so a
-// chunk is either wholly inside the row or wholly outside it.
+// 16 bytes at byte `off` of row `row`, zero past the row or past n_rows.
+// Rows are 16-byte aligned and row_bytes is a multiple of 16 (the host repacks
+// inputs that are not), so a chunk is either wholly inside a row or outside.
 __device__ __forceinline__ i32x4 load_chunk(const uint8_t *base, uint32_t row, uint32_t n_rows,
-                                            uint32_t row_bytes, uint32_t off, bool aligned)
+                                            uint32_t row_bytes, uint32_t off)
 {
     i32x4 v = {0, 0, 0, 0};
-    if (row < n_rows && off < row_bytes) {
-        const uint8_t *p = base + (size_t)row * row_bytes + off;
-        if (aligned) {
-            v = *(const i32x4 *)p;
-        } else {
-            uint32_t w[4] = {0, 0, 0, 0};
-            const uint32_t lim = row_bytes - off;
-#pragma unroll
-            for (int b = 0; b < 16; ++b)
-                if ((uint32_t)b < lim)
-                    w[b >> 2] |= (uint32_t)p[b] << (8 * (b & 3));
-            v = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-        }
-    }
+    if (row < n_rows && off < row_bytes)
+        v = *(const i32x4 *)(base + (size_t)row * row_bytes + off);
     return v;
 }
 
@@ -109,6 +97,24 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
 {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// LDS tile layout: rows of CPR 16-byte chunks, unpadded; chunk c of row r is
+// stored at position c ^ swz(r).  With 32 banks of 4 bytes a 128-bit access
+// serves 8 lanes per cycle; swz makes both access patterns conflict-free:
+// B-fragment reads (8 consecutive rows, same chunk) and tile stores (8
+// consecutive chunks of one row, or two rows when CPR = 4, four when CPR = 2).
+template <int CPR>
+__device__ __forceinline__ int swz(int r)
+{
+    if constexpr (CPR >= 8)
+        return r & 7;
+    else if constexpr (CPR == 4)
+        return (r >> 1) & 3;
+    else if constexpr (CPR == 2)
+        return (r >> 2) & 1;
+    else
+        return 0;
 }
 
 // Exact test of one pair.  IP: acc >= thr.  L2: 2 acc >= (N_x + N_y) - r2,
@@ -132,20 +138,19 @@ __device__ __forceinline__ bool pair_matches(typename Mma<DT>::val_t acc,
     }
 }
 
-// Epilogue of one wave over a (32*WMB) x 32 block of results:
-// accumulators acc[a] hold rows prow0 + 32a + (8(r/4) + 4 half + r%4), column j.
-//  1. Cheap necessary condition per lane (one max over all its results against
-//     a per-lane bound); a wave whose lanes all fail is done.
-//  2. Otherwise every result is tested exactly; ballots give each wave's match
-//     count; MODE_SINGLE reserves space with one atomicAdd per wave, MODE_EMIT
-//     takes the block's running offset; matches are stored so that each store
-//     instruction writes consecutive slots.
-template <int DT, int MET, int MODE, int WMB>
-__device__ __forceinline__ void epilogue(const typename Mma<DT>::acc_t (&acc)[WMB], uint32_t prow0,
-                                         uint32_t j, int half, int lane,
-                                         typename Mma<DT>::val_t nmin,
-                                         typename Mma<DT>::val_t ny, const JoinArgs &g,
-                                         uint64_t &blk_run)
+// Epilogue of one wave over a (32*WMB) x 32 block of results, in two parts.
+// Accumulator acc[a] register r of lane l holds the pair
+//   (i, j) = (ibase + 32 a + 8 (r / 4) + r % 4,  j)  with ibase = prow0 + 4 (l / 32).
+//
+// lane_may_match: a necessary condition per lane, from one max over the lane's
+// 16 * WMB results.  IP: max acc >= thr.  L2: 2 max acc >= (nmin + N_y) - r2,
+// where nmin is the smallest squared norm among the lane's rows; since the
+// fp32 rounding of (N_x + N_y) - r2 is monotone in N_x, a lane whose bound
+// fails holds no match.  Lanes of columns past n_q never match.
+template <int DT, int MET, int WMB>
+__device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&acc)[WMB],
+                                               uint32_t j, typename Mma<DT>::val_t nmin,
+                                               typename Mma<DT>::val_t ny, const JoinArgs &g)
 {
     typedef typename Mma<DT>::val_t V;
     V m = acc[0][0];
@@ -156,37 +161,119 @@ __device__ __forceinline__ void epilogue(const typename Mma<DT>::acc_t (&acc)[WM
             if (a | r)
                 m = vmax(m, acc[a][r]);
     bool pass;
-    if constexpr (MET == MET_IP) {
+    if constexpr (MET == MET_IP)
         pass = pair_matches<DT, MET>(m, V(0), V(0), g);
-    } else {
+    else
         pass = pair_matches<DT, MET>(m, nmin, ny, g);
-    }
-    pass = pass && (j < g.n_q);
-    if (__ballot(pass) == 0)
-        return;
+    return pass && (j < g.n_q);
+}
 
-    const V *np = (const V *)g.norm_p;
+// Per-wave output staging for the single-pass mode: a wave appends its
+// matches to its own LDS buffer (no atomics) and moves them to the global pair
+// buffer in bulk, reserving the global slots with one atomicAdd per flush.
+struct WaveOut {
+    uint2 *buf;      // this wave's LDS buffer of `cap` pairs
+    uint32_t cap;
+    uint32_t fill;   // wave-uniform
+};
+
+__device__ __forceinline__ void flush_wave_out(WaveOut &wo, int lane, const JoinArgs &g)
+{
+    if (wo.fill == 0)
+        return;
+    unsigned long long b = 0;
+    if (lane == 0)
+        b = atomicAdd(g.counter, (unsigned long long)wo.fill);
+    const uint64_t base = first_lane_u64(b);
+    for (uint32_t k = lane; k < wo.fill; k += 64)
+        if (base + k < g.cap)
+            *(uint2 *)(g.pairs + 2 * (base + k)) = wo.buf[k];
+    wo.fill = 0;
+}
+
+// Final flush of every wave's staging buffer with one atomicAdd per workgroup
+// (all waves must call it; it contains barriers).
+template <int NW>
+__device__ __forceinline__ void flush_workgroup_out(WaveOut &wo, int wave, int lane,
+                                                    const JoinArgs &g)
+{
+    __shared__ uint32_t s_fill[NW];
+    __shared__ unsigned long long s_base;
+    if (lane == 0)
+        s_fill[wave] = wo.fill;
+    __syncthreads();
+    if (wave == 0) {
+        uint32_t tot = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            tot += s_fill[w];
+        if (lane == 0)
+            s_base = tot ? atomicAdd(g.counter, (unsigned long long)tot) : 0ull;
+    }
+    __syncthreads();
+    uint64_t base = s_base;
+    for (int w = 0; w < wave; ++w)
+        base += s_fill[w];
+    for (uint32_t k = lane; k < wo.fill; k += 64)
+        if (base + k < g.cap)
+            *(uint2 *)(g.pairs + 2 * (base + k)) = wo.buf[k];
+    wo.fill = 0;
+}
+
+// exact_block: every result of one 32x32 block (accumulator `acc`, rows
+// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly; ballots give
+// the wave's match count; MODE_SINGLE appends the matches to the wave's LDS
+// staging buffer, MODE_EMIT writes them at the output block's running offset,
+// MODE_COUNT only counts.  Matches are stored so that each store instruction
+// fills consecutive slots.  L2 row norms come from `nrow` (LDS: this lane's rows of the block).
+template <int DT, int MET, int MODE>
+__device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, uint32_t ib,
+                                            uint32_t j, int lane, typename Mma<DT>::val_t ny,
+                                            const typename Mma<DT>::val_t *nrow,
+                                            const JoinArgs &g, uint64_t &blk_run, WaveOut &wo)
+{
+    typedef typename Mma<DT>::val_t V;
+    // Opaque to the optimiser: keeps the per-result row indices from being
+    // hoisted into (and occupying registers of) the caller's main loop.
+    asm volatile("" : "+v"(ib));
+    const bool jok = j < g.n_q;
+    auto test = [&](int r) -> bool {
+        const uint32_t i = ib + 8 * (r >> 2) + (r & 3);
+        if constexpr (MET == MET_L2)
+            return jok && i < g.n_p &&
+                   pair_matches<DT, MET>(acc[r], nrow[8 * (r >> 2) + (r & 3)], ny, g);
+        else
+            return jok && i < g.n_p && pair_matches<DT, MET>(acc[r], V(0), V(0), g);
+    };
     uint32_t tot = 0;
 #pragma unroll
-    for (int a = 0; a < WMB; ++a)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const uint32_t i = prow0 + 32 * a + 8 * (r >> 2) + 4 * half + (r & 3);
-            bool p = false;
-            if (i < g.n_p && j < g.n_q) {
-                V nx = V(0);
-                if constexpr (MET == MET_L2)
-                    nx = np[i];
-                p = pair_matches<DT, MET>(acc[a][r], nx, ny, g);
-            }
-            tot += (uint32_t)__popcll(__ballot(p));
-        }
+    for (int r = 0; r < 16; ++r)
+        tot += (uint32_t)__popcll(__ballot(test(r)));
     if constexpr (MODE == MODE_COUNT) {
         blk_run += tot;
         return;
     }
     if (tot == 0)
         return;
+    if constexpr (MODE == MODE_SINGLE) {
+        if (wo.fill + tot > wo.cap)
+            flush_wave_out(wo, lane, g);
+        if (tot <= wo.cap) {
+            uint32_t base = wo.fill;
+            wo.fill += tot;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const bool p = test(r);
+                const uint64_t mk = __ballot(p);
+                if (p)
+                    wo.buf[base + lanes_below(mk)] = make_uint2(ib + 8 * (r >> 2) + (r & 3), j);
+                base += (uint32_t)__popcll(mk);
+            }
+            return;
+        }
+    }
+    // Emit pass (block offset) or a block with more matches than the staging
+    // buffer holds (one atomic reserves its slots).
     uint64_t base;
     if constexpr (MODE == MODE_SINGLE) {
         unsigned long long b = 0;
@@ -198,25 +285,61 @@ __device__ __forceinline__ void epilogue(const typename Mma<DT>::acc_t (&acc)[WM
         blk_run += tot;
     }
 #pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const bool p = test(r);
+        const uint64_t mk = __ballot(p);
+        if (p) {
+            const uint64_t slot = base + lanes_below(mk);
+            if (slot < g.cap)
+                *(uint2 *)(g.pairs + 2 * slot) = make_uint2(ib + 8 * (r >> 2) + (r & 3), j);
+        }
+        base += (uint64_t)__popcll(mk);
+    }
+}
+
+// All WMB blocks of a wave's sub-tile that hold a possible match.
+template <int DT, int MET, int MODE, int WMB>
+__device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc)[WMB],
+                                             uint32_t ibase, uint32_t j, int lane,
+                                             typename Mma<DT>::val_t nmin,
+                                             typename Mma<DT>::val_t ny,
+                                             const typename Mma<DT>::val_t *nrows,
+                                             const JoinArgs &g, uint64_t &blk_run, WaveOut &wo)
+{
+#pragma unroll
+    for (int a = 0; a < WMB; ++a) {
+        typename Mma<DT>::acc_t one[1] = {acc[a]};
+        if (__ballot(lane_may_match<DT, MET, 1>(one, j, nmin, ny, g)) != 0)
+            exact_block<DT, MET, MODE>(acc[a], ibase + 32 * a, j, lane, ny, nrows + 32 * a, g,
+                                       blk_run, wo);
+    }
+}
+
+// Squared norms of a wave's 32 * WMB rows into LDS (rows past n_p get a large
+// placeholder and are excluded by the exact test); returns the smallest norm
+// among this lane's rows.
+template <int DT, int WMB>
+__device__ __forceinline__ typename Mma<DT>::val_t stage_row_norms(uint32_t prow0, int lane,
+                                                                   typename Mma<DT>::val_t *s_n,
+                                                                   const JoinArgs &g)
+{
+    typedef typename Mma<DT>::val_t V;
+    const V *np = (const V *)g.norm_p;
+#pragma unroll
+    for (int k = 0; k < WMB / 2; ++k) {
+        const uint32_t i = prow0 + 64 * k + lane;
+        s_n[64 * k + lane] = i < g.n_p ? np[i] : big_val<V>();
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int half = lane >> 5;
+    V nmin = big_val<V>();
+#pragma unroll
     for (int a = 0; a < WMB; ++a)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const uint32_t i = prow0 + 32 * a + 8 * (r >> 2) + 4 * half + (r & 3);
-            bool p = false;
-            if (i < g.n_p && j < g.n_q) {
-                V nx = V(0);
-                if constexpr (MET == MET_L2)
-                    nx = np[i];
-                p = pair_matches<DT, MET>(acc[a][r], nx, ny, g);
-            }
-            const uint64_t mk = __ballot(p);
-            if (p) {
-                const uint64_t slot = base + lanes_below(mk);
-                if (slot < g.cap)
-                    *(uint2 *)(g.pairs + 2 * slot) = make_uint2(i, j);
-            }
-            base += (uint64_t)__popcll(mk);
-        }
+        for (int r = 0; r < 16; ++r)
+            nmin = vmin(nmin, s_n[32 * a + 4 * half + 8 * (r >> 2) + (r & 3)]);
+    return nmin;
 }
 
 // ---------------------------------------------------------------------------
@@ -225,38 +348,48 @@ __device__ __forceinline__ void epilogue(const typename Mma<DT>::acc_t (&acc)[WM
 // A workgroup of NW waves owns BM = NW * 32 * WMB consecutive rows of P; each
 // wave keeps its 32*WMB rows, all KS k-steps, as MFMA A-fragments in VGPRs for
 // the whole kernel.  The workgroup sweeps its range of Q in tiles of BN rows,
-// double-buffered in LDS (row stride padded by 16 bytes so that the 32 rows a
-// B-fragment read touches fall in different banks).  Per tile and per 32-row
-// sub-tile each wave issues KS * WMB MFMAs and runs the epilogue.
-// Output block (for the count/emit passes) = one wave's rows x one Q tile;
+// double-buffered in LDS (XOR-swizzled chunks, see swz); the next tile's
+// direct global-to-LDS loads are issued before the current tile's MFMAs.  Inside a tile the 32-row
+// sub-tiles are software-pipelined: the MFMAs of sub-tile s are issued in the
+// same instruction block as the epilogue bound of sub-tile s - 1 (two
+// accumulator sets), so the VALU work of the epilogue overlaps the matrix
+// cores.  Output block (count/emit passes) = one wave's rows x one Q tile;
 // block index = (global wave row-block) * n_qtiles + tile.
 template <int DT, int MET, int MODE, int KS, int WMB, int NW, int BN>
-__global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g, uint32_t aligned)
+__global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
 {
     typedef Mma<DT> M;
     typedef typename M::acc_t acc_t;
     typedef typename M::val_t V;
-    constexpr int LS = KS * 32 + 16;        // LDS row stride in bytes
+    constexpr int LS = KS * 32;             // LDS row stride in bytes
     constexpr int NT = NW * 64;
     constexpr int CPR = KS * 2;             // 16-byte chunks per row
     constexpr int TCH = BN * CPR;           // chunks per Q tile
-    constexpr int CPT = (TCH + NT - 1) / NT;
     constexpr int SUBS = BN / 32;
     constexpr int BM = NW * 32 * WMB;
     constexpr bool NEED_NORMS = (MET == MET_L2);
 
-    __shared__ __attribute__((aligned(16))) uint8_t s_q[2][BN * LS];
-    __shared__ V s_nq[NEED_NORMS ? 2 : 1][NEED_NORMS ? BN : 1];
+    // Two distinct LDS buffers (not one array indexed at run time): the tile
+    // loop is unrolled by two so every access names its buffer statically, which
+    // lets the compiler see that the direct loads into one buffer never alias
+    // the reads of the other (and not wait for them).
+    __shared__ __attribute__((aligned(16))) uint8_t s_q0[BN * LS];
+    __shared__ __attribute__((aligned(16))) uint8_t s_q1[BN * LS];
+    __shared__ V s_nq0[NEED_NORMS ? BN : 1];
+    __shared__ V s_nq1[NEED_NORMS ? BN : 1];
+    __shared__ V s_np[NEED_NORMS ? NW : 1][NEED_NORMS ? 32 * WMB : 1];
+    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 256 : 1;
+    __shared__ uint2 s_out[NW][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
-    const bool al = aligned != 0;
     const uint32_t qsplit = g.qsplit;
     const uint32_t pb = blockIdx.x / qsplit, qs = blockIdx.x - pb * qsplit;
     const uint32_t n_qt = (g.n_q + BN - 1) / BN;
     const uint32_t t0 = (uint32_t)((uint64_t)qs * n_qt / qsplit);
     const uint32_t t1 = (uint32_t)((uint64_t)(qs + 1) * n_qt / qsplit);
     const uint32_t prow0 = pb * BM + wave * 32 * WMB;
+    const uint32_t ibase = prow0 + 4 * half;
 
     i32x4 A[WMB][KS];
 #pragma unroll
@@ -264,28 +397,42 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g, uint32_t al
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
             A[a][ks] = load_chunk(g.P, prow0 + 32 * a + c32, g.n_p, g.row_bytes,
-                                  32 * ks + 16 * half, al);
+                                  32 * ks + 16 * half);
 
     V nmin = big_val<V>();
+    const V *nrows = nullptr;
     if constexpr (NEED_NORMS) {
-        const V *np = (const V *)g.norm_p;
-#pragma unroll
-        for (int a = 0; a < WMB; ++a)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const uint32_t i = prow0 + 32 * a + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (i < g.n_p)
-                    nmin = vmin(nmin, np[i]);
-            }
+        nmin = stage_row_norms<DT, WMB>(prow0, lane, s_np[wave], g);
+        nrows = &s_np[wave][4 * half];
     }
+    // Drain the resident-row loads here: otherwise the wait inserted for their
+    // first use inside the tile loop also waits for the next tile's prefetch.
+    __builtin_amdgcn_s_waitcnt(0);
 
-    auto stage_load = [&](uint32_t t, i32x4(&st)[CPT], V &stn) {
+    // Q tiles go straight from global memory into LDS (no staging registers):
+    // each wave instruction fills 64 consecutive 16-byte LDS positions, and the
+    // lane at position p = r * CPR + c' loads chunk c = c' ^ swz(r) of tile row
+    // r, which stores the tile swizzled.  Rows past n_q read the last row
+    // instead (their columns are never reported); chunks past row_bytes read
+    // the row's last chunk (they meet the zero padding of the resident rows).
+    static_assert(TCH % (64 * NW) == 0, "tile must split evenly over the waves");
+    constexpr int TPW = TCH / (64 * NW);     // direct-load instructions per wave
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    auto stage_issue = [&](uint32_t t, uint8_t *dst) {
 #pragma unroll
-        for (int k = 0; k < CPT; ++k) {
-            const int c = tid + k * NT;
-            if (TCH % NT == 0 || c < TCH)
-                st[k] = load_chunk(g.Q, t * BN + c / CPR, g.n_q, g.row_bytes, 16 * (c % CPR), al);
+        for (int kk = 0; kk < TPW; ++kk) {
+            const int k = kk * NW + wv;
+            const int pos = 64 * k + lane;
+            const int r = pos / CPR;
+            const int c = (pos % CPR) ^ swz<CPR>(r);
+            const uint32_t row = min(t * BN + r, g.n_q - 1);
+            const uint32_t off = min((uint32_t)(16 * c), g.row_bytes - 16);
+            __builtin_amdgcn_global_load_lds(
+                (const void *)(g.Q + (size_t)row * g.row_bytes + off),
+                (__attribute__((address_space(3))) void *)(dst + 1024 * k), 16, 0, 0);
         }
+    };
+    auto norm_load = [&](uint32_t t, V &stn) {
         if constexpr (NEED_NORMS) {
             if (tid < BN) {
                 const uint32_t jq = t * BN + tid;
@@ -293,69 +440,94 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g, uint32_t al
             }
         }
     };
-    auto stage_store = [&](int buf, const i32x4(&st)[CPT], V stn) {
-#pragma unroll
-        for (int k = 0; k < CPT; ++k) {
-            const int c = tid + k * NT;
-            if (TCH % NT == 0 || c < TCH)
-                *(i32x4 *)&s_q[buf][(c / CPR) * LS + 16 * (c % CPR)] = st[k];
-        }
+    auto norm_store = [&](V *dst, V stn) {
         if constexpr (NEED_NORMS) {
             if (tid < BN)
-                s_nq[buf][tid] = stn;
+                dst[tid] = stn;
+        }
+    };
+    // MFMAs of one 32-row sub-tile of Q against the wave's resident rows;
+    // bp is this lane's row of the sub-tile (swizzle depends on c32 only,
+    // since sub-tiles start at multiples of 32 rows).
+    // Chunk 2 ks + half sits at (2 ks + half) ^ swz = (2 ks) ^ h with h below;
+    // the XOR only touches the low three bits, so k-steps four apart differ by
+    // a constant 128 bytes and four lane offsets cover every k-step.
+    const int h = half ^ swz<CPR>(c32);
+    int o4[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        o4[k] = 16 * ((2 * k) ^ h);
+    auto mma_sub = [&](acc_t(&acc)[WMB], const uint8_t *bp) {
+        const i32x4 b0 = *(const i32x4 *)(bp + o4[0]);
+#pragma unroll
+        for (int a = 0; a < WMB; ++a)
+            acc[a] = M::mma(A[a][0], b0, acc_t{});
+#pragma unroll
+        for (int ks = 1; ks < KS; ++ks) {
+            const i32x4 b = *(const i32x4 *)(bp + o4[ks & 3] + 128 * (ks >> 2));
+#pragma unroll
+            for (int a = 0; a < WMB; ++a)
+                acc[a] = M::mma(A[a][ks], b, acc[a]);
         }
     };
 
     if (t0 < t1) {
-        i32x4 st[CPT];
         V stn = V(0);
-        stage_load(t0, st, stn);
-        stage_store(0, st, stn);
+        stage_issue(t0, s_q0);
+        norm_load(t0, stn);
+        norm_store(s_nq0, stn);
     }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
+    WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
-    for (uint32_t t = t0; t < t1; ++t) {
-        const int buf = (t - t0) & 1;
+    // One Q tile: prefetch tile t+1 into `nxt`, compute tile t from `cur`.
+    auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt) {
         const bool more = t + 1 < t1;
-        i32x4 st[CPT];
         V stn = V(0);
-        if (more)
-            stage_load(t + 1, st, stn);
-
+        if (more) {
+            stage_issue(t + 1, nxt);
+            norm_load(t + 1, stn);
+        }
         const uint64_t blk = wave_row_block * n_qt + t;
         uint64_t blk_run = 0;
         if constexpr (MODE == MODE_EMIT)
             blk_run = g.block_offsets[blk];
 
+        const uint8_t *bq = cur + c32 * LS;
+        acc_t acc[2][WMB];
+        mma_sub(acc[0], bq);
 #pragma unroll
-        for (int s = 0; s < SUBS; ++s) {
-            acc_t acc[WMB];
-#pragma unroll
-            for (int a = 0; a < WMB; ++a)
-                acc[a] = acc_t{};
-            const uint8_t *bp = &s_q[buf][(32 * s + c32) * LS + 16 * half];
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const i32x4 b = *(const i32x4 *)(bp + 32 * ks);
-#pragma unroll
-                for (int a = 0; a < WMB; ++a)
-                    acc[a] = M::mma(A[a][ks], b, acc[a]);
-            }
-            V ny = V(0);
+        for (int s = 1; s <= SUBS; ++s) {
+            const int curi = s & 1, prv = curi ^ 1;
+            if (s < SUBS)
+                mma_sub(acc[curi], bq + 32 * s * LS);
+            const uint32_t jp = t * BN + 32 * (s - 1) + c32;
+            V nyp = V(0);
             if constexpr (NEED_NORMS)
-                ny = s_nq[buf][32 * s + c32];
-            epilogue<DT, MET, MODE, WMB>(acc, prow0, t * BN + 32 * s + c32, half, lane, nmin, ny,
-                                         g, blk_run);
+                nyp = ncur[32 * (s - 1) + c32];
+            const bool may = lane_may_match<DT, MET, WMB>(acc[prv], jp, nmin, nyp, g);
+            if (__builtin_expect(__ballot(may) != 0, 0))
+                exact_blocks<DT, MET, MODE, WMB>(acc[prv], ibase, jp, lane, nmin, nyp, nrows, g,
+                                                 blk_run, wo);
         }
         if constexpr (MODE == MODE_COUNT) {
             if (lane == 0)
                 g.block_counts[blk] = (uint32_t)blk_run;
         }
         if (more)
-            stage_store(buf ^ 1, st, stn);
+            norm_store(nnxt, stn);
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's direct loads of tile t+1 landed
         __syncthreads();
+    };
+    for (uint32_t t = t0; t < t1; t += 2) {
+        tile(t, s_q0, s_q1, s_nq0, s_nq1);
+        if (t + 1 < t1)
+            tile(t + 1, s_q1, s_q0, s_nq1, s_nq0);
     }
+    if constexpr (MODE == MODE_SINGLE)
+        flush_workgroup_out<NW>(wo, wave, lane, g);
 }
 
 // ---------------------------------------------------------------------------
@@ -371,12 +543,12 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g, uint32_t al
 constexpr int ST_BM = 128, ST_BN = 128, ST_KC = 128;
 
 template <int DT, int MET, int MODE>
-__global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligned)
+__global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
 {
     typedef Mma<DT> M;
     typedef typename M::acc_t acc_t;
     typedef typename M::val_t V;
-    constexpr int LS = ST_KC + 16;
+    constexpr int LS = ST_KC;
     constexpr int CPR = ST_KC / 16;                   // 8 chunks per row per K chunk
     constexpr int TCH = (ST_BM + ST_BN) * CPR;        // 2048 chunks
     constexpr int CPT = TCH / 256;                    // 8 per thread
@@ -384,11 +556,13 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligne
     constexpr bool NEED_NORMS = (MET == MET_L2);
 
     __shared__ __attribute__((aligned(16))) uint8_t s_op[2][(ST_BM + ST_BN) * LS];
+    __shared__ V s_np[NEED_NORMS ? 4 : 1][NEED_NORMS ? 64 : 1];
+    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 128 : 1;
+    __shared__ uint2 s_out[4][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
     const int wr = wave >> 1, wc = wave & 1;
-    const bool al = aligned != 0;
 
     // tile order: groups of 8 x 8 tiles, row-major inside a group
     const uint32_t n_pt = (g.n_p + ST_BM - 1) / ST_BM, n_qt = (g.n_q + ST_BN - 1) / ST_BN;
@@ -411,15 +585,16 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligne
             const int c = tid + k * 256;
             const int r = c / CPR, cc = c % CPR;
             const uint32_t off = kc * ST_KC + 16 * cc;
-            st[k] = r < ST_BM ? load_chunk(g.P, p0 + r, g.n_p, g.row_bytes, off, al)
-                              : load_chunk(g.Q, q0 + r - ST_BM, g.n_q, g.row_bytes, off, al);
+            st[k] = r < ST_BM ? load_chunk(g.P, p0 + r, g.n_p, g.row_bytes, off)
+                              : load_chunk(g.Q, q0 + r - ST_BM, g.n_q, g.row_bytes, off);
         }
     };
     auto stage_store = [&](int buf, const i32x4(&st)[CPT]) {
 #pragma unroll
         for (int k = 0; k < CPT; ++k) {
             const int c = tid + k * 256;
-            *(i32x4 *)&s_op[buf][(c / CPR) * LS + 16 * (c % CPR)] = st[k];
+            const int r = c / CPR;
+            *(i32x4 *)&s_op[buf][r * LS + 16 * ((c % CPR) ^ swz<CPR>(r))] = st[k];
         }
     };
 
@@ -442,17 +617,20 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligne
         i32x4 st[CPT];
         if (more)
             stage_load(kc + 1, st);
-        const uint8_t *pa = &s_op[buf][(64 * wr + c32) * LS + 16 * half];
-        const uint8_t *pbq = &s_op[buf][(ST_BM + 64 * wc + c32) * LS + 16 * half];
+        // rows of A- and B-blocks start at multiples of 32: swizzle = swz(c32)
+        const uint8_t *pa = &s_op[buf][(64 * wr + c32) * LS];
+        const uint8_t *pbq = &s_op[buf][(ST_BM + 64 * wc + c32) * LS];
+        const int h = half ^ swz<CPR>(c32);
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks) {
             i32x4 fa[2], fb[2];
+            const int off = 16 * ((2 * ks) ^ h);
 #pragma unroll
             for (int a = 0; a < 2; ++a)
-                fa[a] = *(const i32x4 *)(pa + 32 * a * LS + 32 * ks);
+                fa[a] = *(const i32x4 *)(pa + 32 * a * LS + off);
 #pragma unroll
             for (int s = 0; s < 2; ++s)
-                fb[s] = *(const i32x4 *)(pbq + 32 * s * LS + 32 * ks);
+                fb[s] = *(const i32x4 *)(pbq + 32 * s * LS + off);
 #pragma unroll
             for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -465,18 +643,14 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligne
     }
 
     const uint32_t prow0 = p0 + 64 * wr;
+    const uint32_t ibase = prow0 + 4 * half;
     V nmin = big_val<V>();
+    const V *nrows = nullptr;
     if constexpr (NEED_NORMS) {
-        const V *np = (const V *)g.norm_p;
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const uint32_t i = prow0 + 32 * a + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (i < g.n_p)
-                    nmin = vmin(nmin, np[i]);
-            }
+        nmin = stage_row_norms<DT, 2>(prow0, lane, s_np[wave], g);
+        nrows = &s_np[wave][4 * half];
     }
+    WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t blk = (uint64_t)(pt * n_qt + qt) * 4 + wave;
     uint64_t blk_run = 0;
     if constexpr (MODE == MODE_EMIT)
@@ -488,8 +662,13 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g, uint32_t aligne
         if constexpr (NEED_NORMS)
             ny = j < g.n_q ? ((const V *)g.norm_q)[j] : big_val<V>();
         const acc_t blk_acc[2] = {acc[0][s], acc[1][s]};
-        epilogue<DT, MET, MODE, 2>(blk_acc, prow0, j, half, lane, nmin, ny, g, blk_run);
+        const bool may = lane_may_match<DT, MET, 2>(blk_acc, j, nmin, ny, g);
+        if (__ballot(may) != 0)
+            exact_blocks<DT, MET, MODE, 2>(blk_acc, ibase, j, lane, nmin, ny, nrows, g, blk_run,
+                                           wo);
     }
+    if constexpr (MODE == MODE_SINGLE)
+        flush_workgroup_out<4>(wo, wave, lane, g);
     if constexpr (MODE == MODE_COUNT) {
         if (lane == 0)
             g.block_counts[blk] = (uint32_t)blk_run;
@@ -515,55 +694,60 @@ struct ResidentCfg<DT_I8> {
 };
 
 constexpr int RES_NW = 4;
-constexpr int RES_BN = 64;
 template <int DT, int KS>
 constexpr int res_wmb()
 {
     return (DT == DT_I8 && KS <= 2) ? 4 : 2;
 }
+// Q tile rows: 128 (four sub-tiles per barrier) unless the rows are so long
+// that two double-buffered tiles per CU would not fit in LDS.
+template <int KS>
+constexpr int res_bn()
+{
+    return KS <= 8 ? 128 : 64;
+}
 
 template <int DT, int MET, int MODE, int V>
-hipError_t launch_resident_v(const Plan &p, const JoinArgs &g, uint32_t al, hipStream_t st)
+hipError_t launch_resident_v(const Plan &p, const JoinArgs &g, hipStream_t st)
 {
     constexpr int KS = ResidentCfg<DT>::KS[V];
     constexpr int WMB = res_wmb<DT, KS>();
-    hipLaunchKernelGGL((join_resident<DT, MET, MODE, KS, WMB, RES_NW, RES_BN>), dim3(p.grid),
-                       dim3(RES_NW * 64), 0, st, g, al);
+    constexpr int BN = res_bn<KS>();
+    hipLaunchKernelGGL((join_resident<DT, MET, MODE, KS, WMB, RES_NW, BN>), dim3(p.grid),
+                       dim3(RES_NW * 64), 0, st, g);
     return hipGetLastError();
 }
 
 template <int DT, int MET, int MODE>
-hipError_t launch_mode(const Plan &p, const JoinArgs &g, uint32_t al, hipStream_t st)
+hipError_t launch_mode(const Plan &p, const JoinArgs &g, hipStream_t st)
 {
     if (p.family == FAM_STREAMED) {
-        hipLaunchKernelGGL((join_streamed<DT, MET, MODE>), dim3(p.grid), dim3(256), 0, st, g, al);
+        hipLaunchKernelGGL((join_streamed<DT, MET, MODE>), dim3(p.grid), dim3(256), 0, st, g);
         return hipGetLastError();
     }
     switch (p.variant) {
-    case 0: return launch_resident_v<DT, MET, MODE, 0>(p, g, al, st);
-    case 1: return launch_resident_v<DT, MET, MODE, 1>(p, g, al, st);
-    case 2: return launch_resident_v<DT, MET, MODE, 2>(p, g, al, st);
-    case 3: return launch_resident_v<DT, MET, MODE, 3>(p, g, al, st);
+    case 0: return launch_resident_v<DT, MET, MODE, 0>(p, g, st);
+    case 1: return launch_resident_v<DT, MET, MODE, 1>(p, g, st);
+    case 2: return launch_resident_v<DT, MET, MODE, 2>(p, g, st);
+    case 3: return launch_resident_v<DT, MET, MODE, 3>(p, g, st);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <int DT>
-hipError_t launch_dtype(const Plan &p, int metric, int mode, bool aligned, const JoinArgs &g,
-                        hipStream_t st)
+hipError_t launch_dtype(const Plan &p, int metric, int mode, const JoinArgs &g, hipStream_t st)
 {
-    const uint32_t al = aligned ? 1u : 0u;
     if (metric == MET_IP) {
         switch (mode) {
-        case MODE_SINGLE: return launch_mode<DT, MET_IP, MODE_SINGLE>(p, g, al, st);
-        case MODE_COUNT: return launch_mode<DT, MET_IP, MODE_COUNT>(p, g, al, st);
-        case MODE_EMIT: return launch_mode<DT, MET_IP, MODE_EMIT>(p, g, al, st);
+        case MODE_SINGLE: return launch_mode<DT, MET_IP, MODE_SINGLE>(p, g, st);
+        case MODE_COUNT: return launch_mode<DT, MET_IP, MODE_COUNT>(p, g, st);
+        case MODE_EMIT: return launch_mode<DT, MET_IP, MODE_EMIT>(p, g, st);
         }
     } else if (metric == MET_L2) {
         switch (mode) {
-        case MODE_SINGLE: return launch_mode<DT, MET_L2, MODE_SINGLE>(p, g, al, st);
-        case MODE_COUNT: return launch_mode<DT, MET_L2, MODE_COUNT>(p, g, al, st);
-        case MODE_EMIT: return launch_mode<DT, MET_L2, MODE_EMIT>(p, g, al, st);
+        case MODE_SINGLE: return launch_mode<DT, MET_L2, MODE_SINGLE>(p, g, st);
+        case MODE_COUNT: return launch_mode<DT, MET_L2, MODE_COUNT>(p, g, st);
+        case MODE_EMIT: return launch_mode<DT, MET_L2, MODE_EMIT>(p, g, st);
         }
     }
     return hipErrorInvalidValue;
