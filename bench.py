@@ -6,7 +6,7 @@ synthetic input already resident in HBM: (row norms for L2), the fused MFMA
 product + threshold + compaction kernel, and the hand-back of the match count
 (two passes plus the scan for workloads that need count-then-emit).  The
 default workload is the 65536 x 65536, d = 128, bf16 inner-product join; the
-others (--workload c0..c4) are available for measurements but are not the
+others (--workload NAME, see workloads.NAMES) are available for measurements but are not the
 headline line.
 
 Prints ONE JSON line on stdout:
@@ -31,8 +31,8 @@ sys.path.insert(0, ROOT)
 
 # dense MFMA peaks of MI355X (TFLOP/s or TOP/s)
 PEAK = {"f16": 2500.0, "bf16": 2500.0, "i8": 5000.0}
-WORKLOADS = {"c0": 0, "c1": 1, "c2": 2, "c3": 3, "c4": 4}
-TWO_PASS = {4}          # high-output workload runs count-then-emit
+DEFAULT_WORKLOAD = "ip_bf16_65536x128"
+TWO_PASS = {"ip_bf16_clustered_131072x1024"}   # high-output workload: count-then-emit
 
 
 def log(*a):
@@ -91,7 +91,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c1", choices=sorted(WORKLOADS))
+    import workloads
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.NAMES)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -105,8 +106,8 @@ def main():
     import workloads
     to_device = workloads.to_torch
 
-    k = WORKLOADS[args.workload]
-    log(f"generating workload {args.workload} ...")
+    k = args.workload
+    log(f"generating workload {k} ...")
     w = workloads.make_config(k)
     torch.cuda.set_device(0)
     Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)

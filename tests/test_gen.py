@@ -8,9 +8,9 @@ from pins import values
 
 
 def test_deterministic_per_seed():
-    a = workloads.make_config(0)
-    b = workloads.make_config(0)
-    c = workloads.make_config(0, seed=7)
+    a = workloads.make_config("ip_f16_2048x64")
+    b = workloads.make_config("ip_f16_2048x64")
+    c = workloads.make_config("ip_f16_2048x64", seed=7)
     assert np.array_equal(a.P, b.P) and np.array_equal(a.Q, b.Q)
     assert np.array_equal(a.planted, b.planted)
     assert not np.array_equal(a.P, c.P)
@@ -19,8 +19,10 @@ def test_deterministic_per_seed():
     assert np.array_equal(r1.P, r2.P) and np.array_equal(r1.Q, r2.Q)
 
 
-@pytest.mark.parametrize("k,n,lo,hi", [(0, None, -8, 8), (1, 2048, -4, 4), (3, 4096, -15, 15),
-                                       (4, 1024, -2, 2)])
+@pytest.mark.parametrize("k,n,lo,hi", [("ip_f16_2048x64", None, -8, 8),
+                                       ("ip_bf16_65536x128", 2048, -4, 4),
+                                       ("l2_i8_1048576x64", 4096, -15, 15),
+                                       ("ip_bf16_clustered_131072x1024", 1024, -2, 2)])
 def test_value_ranges_integer(k, n, lo, hi):
     w = workloads.make_config(k, n=n)
     for X in (w.P, w.Q):
@@ -31,7 +33,7 @@ def test_value_ranges_integer(k, n, lo, hi):
 
 
 def test_shapes_full_size_small_configs():
-    for k in (0, 1):
+    for k in ("ip_f16_2048x64", "ip_bf16_65536x128"):
         w = workloads.make_config(k)
         cfg = workloads.CONFIGS[k]
         assert w.P.shape == (cfg["n"], cfg["d"]) and w.Q.shape == (cfg["n"], cfg["d"])
@@ -41,7 +43,7 @@ def test_shapes_full_size_small_configs():
 
 
 def test_cosine_rows_are_unit():
-    w = workloads.make_config(2, n=2048)
+    w = workloads.make_config("cos_f16_262144x256", n=2048)
     for X in (w.P, w.Q):
         nrm = (X.astype(np.float64) ** 2).sum(1)
         # fp16 rounding of each coordinate moves ||x||^2 by at most ~2 * 2^-11 relative
@@ -49,7 +51,8 @@ def test_cosine_rows_are_unit():
     assert w.real_valued
 
 
-@pytest.mark.parametrize("k,n", [(0, None), (1, 4096), (2, 4096), (3, 16384)])
+@pytest.mark.parametrize("k,n", [("ip_f16_2048x64", None), ("ip_bf16_65536x128", 4096),
+                                 ("cos_f16_262144x256", 4096), ("l2_i8_1048576x64", 16384)])
 def test_planted_pairs_match(k, n):
     w = workloads.make_config(k, n=n)
     sc = oracle.scores(w.metric, w.dtype, w.P, w.Q, w.planted)
@@ -62,8 +65,8 @@ def test_planted_pairs_match(k, n):
         assert np.all(sc <= w.threshold), sc.max()
 
 
-def test_c3_ties_and_decoys():
-    w = workloads.make_config(3, n=65536)
+def test_l2_ties_and_decoys():
+    w = workloads.make_config("l2_i8_1048576x64", n=65536)
     sc = oracle.scores("l2", "i8", w.P, w.Q, w.planted)
     n_ties = int((sc == 2000).sum())
     assert n_ties == w.decoys.shape[0] > 0
@@ -85,7 +88,7 @@ def _ip_pmf(a, d):
     return pmf, -d * a * a      # pmf[t] = P(<x, y> = t + offset)
 
 
-@pytest.mark.parametrize("k,n,a", [(0, None, 8), (1, 2048, 4)])
+@pytest.mark.parametrize("k,n,a", [("ip_f16_2048x64", None, 8), ("ip_bf16_65536x128", 2048, 4)])
 def test_background_count_matches_exact_pmf(k, n, a):
     """Background matches agree with n^2 * P(<x,y> >= s) from the exact PMF."""
     w = workloads.make_config(k, n=n)
@@ -100,8 +103,8 @@ def test_background_count_matches_exact_pmf(k, n, a):
     assert abs(got - expect) <= tol, (got, expect)
 
 
-def test_c4_cluster_structure():
-    w = workloads.make_config(4, n=1024)
+def test_clustered_structure():
+    w = workloads.make_config("ip_bf16_clustered_131072x1024", n=1024)
     S = values("bf16", w.P) @ values("bf16", w.Q).T
     same = w.labels_p[:, None] == w.labels_q[None, :]
     assert S[same].min() > 1000          # same-cluster pairs always match s = 125

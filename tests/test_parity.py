@@ -51,7 +51,9 @@ def run_case(w, thr=None, two_pass=False, rows=None):
 
 # ------------------------------------------------------- the five workloads
 
-@pytest.mark.parametrize("k,n", [(0, None), (1, 2048), (2, 2048), (3, 4096), (4, 1024)])
+@pytest.mark.parametrize("k,n", [("ip_f16_2048x64", None), ("ip_bf16_65536x128", 2048),
+                                 ("cos_f16_262144x256", 2048), ("l2_i8_1048576x64", 4096),
+                                 ("ip_bf16_clustered_131072x1024", 1024)])
 @pytest.mark.parametrize("two_pass", [False, True])
 def test_workload_reduced(k, n, two_pass):
     w = workloads.make_config(k, n=n)
@@ -62,8 +64,8 @@ def test_workload_reduced(k, n, two_pass):
         say("band", info)
 
 
-def test_c0_true_self_join():
-    w = workloads.make_config(0, self_join=True)
+def test_true_self_join():
+    w = workloads.make_config("ip_f16_2048x64", self_join=True)
     _, g, _ = run_case(w)
     s = set(map(tuple, g.tolist()))
     assert s == {(j, i) for (i, j) in s}
@@ -122,9 +124,9 @@ def test_real_valued_band(dtype, metric):
 
 def test_two_pass_is_deterministic_and_equals_single():
     import torch
-    w = workloads.make_config(4, n=1024)
+    w = workloads.make_config("ip_bf16_clustered_131072x1024", n=1024)
     Pd, Qd = to_device(w.P, "bf16"), to_device(w.Q, "bf16")
-    say("two-pass determinism c4@1024")
+    say("two-pass determinism", w.name)
     a = gpu_join("ip", Pd, Qd, w.threshold, two_pass=True)
     b = gpu_join("ip", Pd, Qd, w.threshold, two_pass=True)
     assert torch.equal(a, b)            # same order, not only the same set
@@ -135,7 +137,7 @@ def test_two_pass_is_deterministic_and_equals_single():
 def test_overflow_reports_exact_total():
     import torch
     import paper_2006_12608_amd as sj
-    w = workloads.make_config(0)
+    w = workloads.make_config("ip_f16_2048x64")
     Pd, Qd = to_device(w.P, "f16"), to_device(w.Q, "f16")
     total = oracle.count("ip", "f16", w.P, w.Q, w.threshold)
     say("overflow", total)
@@ -216,8 +218,10 @@ def _sample_rows(n, k, seed):
     return np.sort(rng.choice(n, size=k, replace=False))
 
 
-@pytest.mark.parametrize("k,n_rows,two_pass", [(1, 48, False), (2, 12, False), (3, 12, False),
-                                                (4, 8, True)])
+@pytest.mark.parametrize("k,n_rows,two_pass", [("ip_bf16_65536x128", 48, False),
+                                                ("cos_f16_262144x256", 12, False),
+                                                ("l2_i8_1048576x64", 12, False),
+                                                ("ip_bf16_clustered_131072x1024", 8, True)])
 def test_full_size_sampled_rows(k, n_rows, two_pass):
     """The full workload on the GPU in the launch configuration the benchmark
     uses; the oracle recomputes a sample of P's rows against all of Q."""
@@ -225,7 +229,7 @@ def test_full_size_sampled_rows(k, n_rows, two_pass):
     import paper_2006_12608_amd as sj
     w = workloads.make_config(k)
     Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
-    rows = _sample_rows(w.n_p, n_rows, 77 + k)
+    rows = _sample_rows(w.n_p, n_rows, 77 + workloads.NAMES.index(k))
     if w.planted.size:   # include some planted rows
         rows = np.unique(np.concatenate([rows, w.planted[:4, 0]]))
     say("full size", w.name, "rows", rows.size, "two_pass", two_pass)

@@ -8,6 +8,7 @@ the GPU library on the other, which share nothing but these inputs.
 from .gen import (  # noqa: F401
     Workload,
     CONFIGS,
+    NAMES,
     make_config,
     random_case,
     encode,

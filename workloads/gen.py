@@ -93,19 +93,21 @@ class Workload:
         return self.n_p * self.n_q
 
 
-# Full-size shapes of the five workloads (index = config number).
+# Full-size shapes of the five workloads, by name.  The default seed of a
+# workload is 1000 + its position in this table.
 CONFIGS = {
-    0: dict(name="ip_f16_2048x64", n=2048, d=64, dtype="f16", metric="ip", threshold=300.0,
-            planted=50),
-    1: dict(name="ip_bf16_65536x128", n=65536, d=128, dtype="bf16", metric="ip", threshold=308.0,
-            planted=10_000),
-    2: dict(name="cos_f16_262144x256", n=262144, d=256, dtype="f16", metric="ip", threshold=0.9,
-            planted=100_000),
-    3: dict(name="l2_i8_1048576x64", n=1048576, d=64, dtype="i8", metric="l2", threshold=2000.0,
-            planted=1_000_000),
-    4: dict(name="ip_bf16_clustered_131072x1024", n=131072, d=1024, dtype="bf16", metric="ip",
-            threshold=125.0, planted=0),
+    "ip_f16_2048x64": dict(n=2048, d=64, dtype="f16", metric="ip", threshold=300.0,
+                           planted=50),
+    "ip_bf16_65536x128": dict(n=65536, d=128, dtype="bf16", metric="ip", threshold=308.0,
+                              planted=10_000),
+    "cos_f16_262144x256": dict(n=262144, d=256, dtype="f16", metric="ip", threshold=0.9,
+                               planted=100_000),
+    "l2_i8_1048576x64": dict(n=1048576, d=64, dtype="i8", metric="l2", threshold=2000.0,
+                             planted=1_000_000),
+    "ip_bf16_clustered_131072x1024": dict(n=131072, d=1024, dtype="bf16", metric="ip",
+                                          threshold=125.0, planted=0),
 }
+NAMES = list(CONFIGS)
 
 
 def _pick_pairs(rng, n_p, n_q, m):
@@ -122,24 +124,24 @@ def _scaled(count, n, n_full, minimum=1):
     return max(minimum, int(round(count * n / n_full)))
 
 
-def make_config(k: int, n: int | None = None, seed: int | None = None,
+def make_config(name: str, n: int | None = None, seed: int | None = None,
                 self_join: bool = False) -> Workload:
-    """Build workload k (0..4).  `n` overrides |P| = |Q| (planted counts are
-    scaled with n) so the same distribution can be checked at small sizes.
-    The default seed is 1000 + k."""
-    cfg = CONFIGS[k]
+    """Build the named workload.  `n` overrides |P| = |Q| (planted counts are
+    scaled with n) so the same distribution can be checked at small sizes."""
+    cfg = CONFIGS[name]
+    pos = NAMES.index(name)
     n_full = cfg["n"]
     n = n_full if n is None else int(n)
-    seed = 1000 + k if seed is None else seed
+    seed = 1000 + pos if seed is None else seed
     rng = np.random.default_rng(seed)
     d = cfg["d"]
-    builder = {0: _c0, 1: _c1, 2: _c2, 3: _c3, 4: _c4}[k]
+    builder = (_ip_f16_small, _ip_bf16, _cos_f16, _l2_i8, _ip_bf16_clustered)[pos]
     w = builder(rng, n, d, _scaled(cfg["planted"], n, n_full), self_join)
-    w.name = cfg["name"] if n == n_full else f"{cfg['name']}@n={n}"
+    w.name = name if n == n_full else f"{name}@n={n}"
     return w
 
 
-def _c0(rng, n, d, planted, self_join):
+def _ip_f16_small(rng, n, d, planted, self_join):
     """fp16 integers uniform in [-8, 8]; Q rows overwritten by copies of P rows."""
     Pv = rng.integers(-8, 9, size=(n, d))
     if self_join:
@@ -154,7 +156,7 @@ def _c0(rng, n, d, planted, self_join):
                     description="fp16 integers U{-8..8}; planted y = x")
 
 
-def _c1(rng, n, d, planted, self_join):
+def _ip_bf16(rng, n, d, planted, self_join):
     """bf16 integers uniform in [-4, 4]; planted y = x with 6 of 128 coordinates
     (5 %) redrawn from the same distribution."""
     Pv = rng.integers(-4, 5, size=(n, d))
@@ -174,7 +176,7 @@ def _unit_rows(X):
     return X / np.linalg.norm(X, axis=1, keepdims=True)
 
 
-def _c2(rng, n, d, planted, self_join):
+def _cos_f16(rng, n, d, planted, self_join):
     """fp16 unit rows: Gaussian rows normalised in float64 then rounded to fp16;
     planted y = normalise(x + 0.3 g) with g ~ N(0, I/d)."""
     Px = _unit_rows(rng.standard_normal((n, d)))
@@ -187,7 +189,7 @@ def _c2(rng, n, d, planted, self_join):
                     description="fp16 unit Gaussian rows (cosine); planted normalise(x+0.3g)")
 
 
-def _c3(rng, n, d, planted, self_join):
+def _l2_i8(rng, n, d, planted, self_join):
     """int8 integers uniform in [-15, 15]; squared radius 2000.
 
     Planted pairs: y = clamp(x + delta, -15, 15) with delta uniform in [-5, 5];
@@ -228,7 +230,7 @@ def _c3(rng, n, d, planted, self_join):
                     description="int8 integers U{-15..15}; planted within r; exact ties at 2000")
 
 
-def _c4(rng, n, d, planted, self_join):
+def _ip_bf16_clustered(rng, n, d, planted, self_join):
     """bf16 integers in [-2, 2] around 256 seeded cluster centres; each
     coordinate is independently redrawn from U{-2..2} with probability 0.1.
     Cluster labels are uniform and rows are not sorted by cluster."""
