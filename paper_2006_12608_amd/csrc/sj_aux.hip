@@ -35,7 +35,7 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
         }
     if (variant >= 0) {
         const int ks = tab[variant];
-        const uint32_t wmb = (dtype == DT_I8 && ks <= 2) ? 4 : 2;
+        const uint32_t wmb = 2;
         const uint32_t bm = kResNW * 32 * wmb;
         const uint64_t n_pb = (n_p + (uint64_t)bm - 1) / bm;
         const uint64_t bn = res_bn(ks);

@@ -19,6 +19,8 @@
 
 #include "sj_internal.h"
 
+#include <type_traits>
+
 namespace sjk {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -99,23 +101,11 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// LDS tile layout: rows of CPR 16-byte chunks, unpadded; chunk c of row r is
-// stored at position c ^ swz(r).  With 32 banks of 4 bytes a 128-bit access
-// serves 8 lanes per cycle; swz makes both access patterns conflict-free:
-// B-fragment reads (8 consecutive rows, same chunk) and tile stores (8
-// consecutive chunks of one row, or two rows when CPR = 4, four when CPR = 2).
-template <int CPR>
-__device__ __forceinline__ int swz(int r)
-{
-    if constexpr (CPR >= 8)
-        return r & 7;
-    else if constexpr (CPR == 4)
-        return (r >> 1) & 3;
-    else if constexpr (CPR == 2)
-        return (r >> 2) & 1;
-    else
-        return 0;
-}
+// LDS tile layout: a row of CPR 16-byte chunks is stored with a stride of
+// CPR + 1 chunks.  The LDS has 64 banks of 4 bytes, so a 128-bit access serves
+// 16 lanes per cycle; a B-fragment read has 16 consecutive rows fetch the same
+// chunk c, and their bank groups ((CPR + 1) r + c) mod 16 are all distinct for
+// every CPR used here (2, 4, 8, 16, 32 and the streamed kernel's 8).
 
 // Exact test of one pair.  IP: acc >= thr.  L2: 2 acc >= (N_x + N_y) - r2,
 // i.e. N_x + N_y - 2 <x,y> <= r2 with the fp32 additions rounded in this order
@@ -144,12 +134,14 @@ __device__ __forceinline__ bool pair_matches(typename Mma<DT>::val_t acc,
 //
 // lane_may_match: a necessary condition per lane, from one max over the lane's
 // 16 * WMB results.  IP: max acc >= thr.  L2: 2 max acc >= (nmin + N_y) - r2,
-// where nmin is the smallest squared norm among the lane's rows; since the
-// fp32 rounding of (N_x + N_y) - r2 is monotone in N_x, a lane whose bound
-// fails holds no match.  Lanes of columns past n_q never match.
+// where nmin is the smallest squared norm among the lane's rows; `nb` carries
+// nmin - r2 for int8 (exact integers) and nmin itself for fp32, whose bound
+// keeps the rounding order of the exact test: since fl(fl(N_x + N_y) - r2) is
+// monotone in N_x, a lane whose bound fails holds no match.  Columns past n_q
+// are not excluded here (the exact test does that).
 template <int DT, int MET, int WMB>
 __device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&acc)[WMB],
-                                               uint32_t j, typename Mma<DT>::val_t nmin,
+                                               typename Mma<DT>::val_t nb,
                                                typename Mma<DT>::val_t ny, const JoinArgs &g)
 {
     typedef typename Mma<DT>::val_t V;
@@ -160,12 +152,23 @@ __device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&a
         for (int r = 0; r < 16; ++r)
             if (a | r)
                 m = vmax(m, acc[a][r]);
-    bool pass;
     if constexpr (MET == MET_IP)
-        pass = pair_matches<DT, MET>(m, V(0), V(0), g);
+        return pair_matches<DT, MET>(m, V(0), V(0), g);
+    else if constexpr (DT == DT_I8)
+        return 2 * m >= nb + ny;
     else
-        pass = pair_matches<DT, MET>(m, nmin, ny, g);
-    return pass && (j < g.n_q);
+        return 2.0f * m >= (nb + ny) - g.thr_f;
+}
+
+// The per-lane constant of the L2 bound (see lane_may_match).
+template <int DT, int MET>
+__device__ __forceinline__ typename Mma<DT>::val_t bound_base(typename Mma<DT>::val_t nmin,
+                                                              const JoinArgs &g)
+{
+    if constexpr (MET == MET_L2 && DT == DT_I8)
+        return nmin - g.thr_i;
+    else
+        return nmin;
 }
 
 // Per-wave output staging for the single-pass mode: a wave appends its
@@ -301,7 +304,7 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
 template <int DT, int MET, int MODE, int WMB>
 __device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc)[WMB],
                                              uint32_t ibase, uint32_t j, int lane,
-                                             typename Mma<DT>::val_t nmin,
+                                             typename Mma<DT>::val_t nb,
                                              typename Mma<DT>::val_t ny,
                                              const typename Mma<DT>::val_t *nrows,
                                              const JoinArgs &g, uint64_t &blk_run, WaveOut &wo)
@@ -309,7 +312,7 @@ __device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc
 #pragma unroll
     for (int a = 0; a < WMB; ++a) {
         typename Mma<DT>::acc_t one[1] = {acc[a]};
-        if (__ballot(lane_may_match<DT, MET, 1>(one, j, nmin, ny, g)) != 0)
+        if (__ballot(lane_may_match<DT, MET, 1>(one, nb, ny, g)) != 0)
             exact_block<DT, MET, MODE>(acc[a], ibase + 32 * a, j, lane, ny, nrows + 32 * a, g,
                                        blk_run, wo);
     }
@@ -342,13 +345,37 @@ __device__ __forceinline__ typename Mma<DT>::val_t stage_row_norms(uint32_t prow
     return nmin;
 }
 
+// Compile-time loop: f(std::integral_constant<int, I>) for I = B .. E-1 (a
+// guaranteed full unroll, unlike #pragma unroll on a large body).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f)
+{
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// Scheduling hint for one pipelined step: alternate each of the NM MFMAs with
+// a share of the NV VALU instructions of the previous sub-tile's epilogue
+// bound, so that the bound executes while the matrix core is busy.
+template <int NM, int NV>
+__device__ __forceinline__ void interleave_mfma_valu()
+{
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, (NV + NM - 1) / NM, 0); // VALU
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Family 1: P rows resident in registers.
 //
 // A workgroup of NW waves owns BM = NW * 32 * WMB consecutive rows of P; each
 // wave keeps its 32*WMB rows, all KS k-steps, as MFMA A-fragments in VGPRs for
 // the whole kernel.  The workgroup sweeps its range of Q in tiles of BN rows,
-// double-buffered in LDS (XOR-swizzled chunks, see swz); the next tile's
+// double-buffered in LDS (rows padded by one chunk); the next tile's
 // direct global-to-LDS loads are issued before the current tile's MFMAs.  Inside a tile the 32-row
 // sub-tiles are software-pipelined: the MFMAs of sub-tile s are issued in the
 // same instruction block as the epilogue bound of sub-tile s - 1 (two
@@ -361,13 +388,15 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     typedef Mma<DT> M;
     typedef typename M::acc_t acc_t;
     typedef typename M::val_t V;
-    constexpr int LS = KS * 32;             // LDS row stride in bytes
-    constexpr int NT = NW * 64;
     constexpr int CPR = KS * 2;             // 16-byte chunks per row
-    constexpr int TCH = BN * CPR;           // chunks per Q tile
+    constexpr int LS = (CPR + 1) * 16;      // padded LDS row stride in bytes
+    constexpr int TCH = BN * (CPR + 1);     // LDS positions per Q tile
     constexpr int SUBS = BN / 32;
     constexpr int BM = NW * 32 * WMB;
     constexpr bool NEED_NORMS = (MET == MET_L2);
+    // Sub-tile pipeline (two accumulator sets) for rows of up to 8 k-steps; at
+    // 16 k-steps the register file holds only one set at two waves per SIMD.
+    constexpr bool PIPE = KS <= 8;
 
     // Two distinct LDS buffers (not one array indexed at run time): the tile
     // loop is unrolled by two so every access names its buffer statically, which
@@ -405,31 +434,46 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         nmin = stage_row_norms<DT, WMB>(prow0, lane, s_np[wave], g);
         nrows = &s_np[wave][4 * half];
     }
+    const V nb = bound_base<DT, MET>(nmin, g);
     // Drain the resident-row loads here: otherwise the wait inserted for their
     // first use inside the tile loop also waits for the next tile's prefetch.
     __builtin_amdgcn_s_waitcnt(0);
 
     // Q tiles go straight from global memory into LDS (no staging registers):
-    // each wave instruction fills 64 consecutive 16-byte LDS positions, and the
-    // lane at position p = r * CPR + c' loads chunk c = c' ^ swz(r) of tile row
-    // r, which stores the tile swizzled.  Rows past n_q read the last row
+    // each wave instruction fills 64 consecutive 16-byte LDS positions; the
+    // lane at position p loads chunk p % (CPR + 1) of tile row p / (CPR + 1)
+    // (the pad position reloads chunk 0).  Rows past n_q read the last row
     // instead (their columns are never reported); chunks past row_bytes read
     // the row's last chunk (they meet the zero padding of the resident rows).
-    static_assert(TCH % (64 * NW) == 0, "tile must split evenly over the waves");
-    constexpr int TPW = TCH / (64 * NW);     // direct-load instructions per wave
+    constexpr int NCALL = (TCH + 64 * NW - 1) / (64 * NW);   // direct loads per wave
     const int wv = __builtin_amdgcn_readfirstlane(wave);
-    auto stage_issue = [&](uint32_t t, uint8_t *dst) {
+    // per load: this lane's tile row and its byte offset within a full tile
+    int lrow[NCALL];
+    uint32_t loff[NCALL];
 #pragma unroll
-        for (int kk = 0; kk < TPW; ++kk) {
+    for (int kk = 0; kk < NCALL; ++kk) {
+        const int pos = 64 * (kk * NW + wv) + lane;
+        const int cp = pos % (CPR + 1);
+        lrow[kk] = min(pos / (CPR + 1), BN - 1);
+        const uint32_t off = min((uint32_t)(16 * (cp == CPR ? 0 : cp)), g.row_bytes - 16);
+        loff[kk] = (uint32_t)lrow[kk] * g.row_bytes + off;
+    }
+    auto stage_issue = [&](uint32_t t, uint8_t *dst) {
+        const bool full = (t + 1) * BN <= g.n_q;          // uniform
+        const uint8_t *qt = g.Q + (size_t)t * BN * g.row_bytes;
+#pragma unroll
+        for (int kk = 0; kk < NCALL; ++kk) {
             const int k = kk * NW + wv;
-            const int pos = 64 * k + lane;
-            const int r = pos / CPR;
-            const int c = (pos % CPR) ^ swz<CPR>(r);
-            const uint32_t row = min(t * BN + r, g.n_q - 1);
-            const uint32_t off = min((uint32_t)(16 * c), g.row_bytes - 16);
+            if (TCH % (64 * NW) != 0 && 64 * k >= TCH)
+                break;
+            const uint8_t *src = qt + loff[kk];
+            if (!full) {
+                const uint32_t row = min(t * BN + lrow[kk], g.n_q - 1);
+                src = g.Q + (size_t)row * g.row_bytes + (loff[kk] - lrow[kk] * g.row_bytes);
+            }
             __builtin_amdgcn_global_load_lds(
-                (const void *)(g.Q + (size_t)row * g.row_bytes + off),
-                (__attribute__((address_space(3))) void *)(dst + 1024 * k), 16, 0, 0);
+                (const void *)src, (__attribute__((address_space(3))) void *)(dst + 1024 * k), 16,
+                0, 0);
         }
     };
     auto norm_load = [&](uint32_t t, V &stn) {
@@ -447,24 +491,15 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         }
     };
     // MFMAs of one 32-row sub-tile of Q against the wave's resident rows;
-    // bp is this lane's row of the sub-tile (swizzle depends on c32 only,
-    // since sub-tiles start at multiples of 32 rows).
-    // Chunk 2 ks + half sits at (2 ks + half) ^ swz = (2 ks) ^ h with h below;
-    // the XOR only touches the low three bits, so k-steps four apart differ by
-    // a constant 128 bytes and four lane offsets cover every k-step.
-    const int h = half ^ swz<CPR>(c32);
-    int o4[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-        o4[k] = 16 * ((2 * k) ^ h);
+    // bp points at this lane's row and half (chunk 2 ks + half is 32 ks on).
     auto mma_sub = [&](acc_t(&acc)[WMB], const uint8_t *bp) {
-        const i32x4 b0 = *(const i32x4 *)(bp + o4[0]);
+        const i32x4 b0 = *(const i32x4 *)bp;
 #pragma unroll
         for (int a = 0; a < WMB; ++a)
             acc[a] = M::mma(A[a][0], b0, acc_t{});
 #pragma unroll
         for (int ks = 1; ks < KS; ++ks) {
-            const i32x4 b = *(const i32x4 *)(bp + o4[ks & 3] + 128 * (ks >> 2));
+            const i32x4 b = *(const i32x4 *)(bp + 32 * ks);
 #pragma unroll
             for (int a = 0; a < WMB; ++a)
                 acc[a] = M::mma(A[a][ks], b, acc[a]);
@@ -482,8 +517,45 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
 
     WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
+    // Epilogue of one wave sub-tile (bound, then the exact path if any lane
+    // may match).
+    auto epilogue = [&](const acc_t(&a)[WMB], uint32_t jp, V nyp, uint64_t &run)
+                        __attribute__((always_inline)) {
+        const bool may = lane_may_match<DT, MET, WMB>(a, nb, nyp, g);
+        if (__builtin_expect(__ballot(may) != 0, 0))
+            exact_blocks<DT, MET, MODE, WMB>(a, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
+    };
+    auto load_b = [&](i32x4(&bf)[KS], const uint8_t *bp) __attribute__((always_inline)) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            bf[ks] = *(const i32x4 *)(bp + 32 * ks);
+    };
+    auto mma_b = [&](acc_t(&a)[WMB], const i32x4(&bf)[KS]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int ai = 0; ai < WMB; ++ai)
+            a[ai] = M::mma(A[ai][0], bf[0], acc_t{});
+#pragma unroll
+        for (int ks = 1; ks < KS; ++ks)
+#pragma unroll
+            for (int ai = 0; ai < WMB; ++ai)
+                a[ai] = M::mma(A[ai][ks], bf[ks], a[ai]);
+    };
+
+    // Sub-tile pipeline state, carried across Q tiles: the last sub-tile's
+    // epilogue of tile t runs at the start of tile t + 1, while the first
+    // B-fragments of tile t + 1 are in flight.  For rows of at most 4 k-steps
+    // the B-fragments of sub-tile s + 1 are also read during sub-tile s.
+    constexpr bool PREFETCH = KS <= 4;
+    static_assert(!PIPE || SUBS % 2 == 0, "the accumulator ping-pong needs an even sub-tile count");
+    acc_t acc[2][WMB];
+    bool have_prev = false;
+    uint32_t j_prev = 0;
+    V ny_prev = V(0);
+    uint64_t blk_prev = 0, run_prev = 0;
+
     // One Q tile: prefetch tile t+1 into `nxt`, compute tile t from `cur`.
-    auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt) {
+    auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt)
+                    __attribute__((always_inline)) {
         const bool more = t + 1 < t1;
         V stn = V(0);
         if (more) {
@@ -495,26 +567,65 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         if constexpr (MODE == MODE_EMIT)
             blk_run = g.block_offsets[blk];
 
-        const uint8_t *bq = cur + c32 * LS;
-        acc_t acc[2][WMB];
-        mma_sub(acc[0], bq);
+        const uint8_t *bq = cur + c32 * LS + 16 * half;
+        if constexpr (!PIPE) {
+            // long rows: one accumulator set; the other wave on the SIMD covers
+            // the epilogue
+            static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
+                constexpr int s = decltype(S)::value;
+                acc_t acc1[WMB];
+                mma_sub(acc1, bq + 32 * s * LS);
+                V nyp = V(0);
+                if constexpr (NEED_NORMS)
+                    nyp = ncur[32 * s + c32];
+                epilogue(acc1, t * BN + 32 * s + c32, nyp, blk_run);
+            });
+            if constexpr (MODE == MODE_COUNT) {
+                if (lane == 0)
+                    g.block_counts[blk] = (uint32_t)blk_run;
+            }
+        } else {
+            i32x4 bnext[KS];
+            load_b(bnext, bq);
+            if (have_prev) {
+                epilogue(acc[1], j_prev, ny_prev, run_prev);
+                if constexpr (MODE == MODE_COUNT) {
+                    if (lane == 0)
+                        g.block_counts[blk_prev] = (uint32_t)run_prev;
+                }
+            }
+            static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
+                constexpr int s = decltype(S)::value;
+                constexpr int ci = s & 1, pi = ci ^ 1;
+                if constexpr (s == 0 || PREFETCH) {
+                    i32x4 bcur[KS];
 #pragma unroll
-        for (int s = 1; s <= SUBS; ++s) {
-            const int curi = s & 1, prv = curi ^ 1;
-            if (s < SUBS)
-                mma_sub(acc[curi], bq + 32 * s * LS);
-            const uint32_t jp = t * BN + 32 * (s - 1) + c32;
-            V nyp = V(0);
+                    for (int ks = 0; ks < KS; ++ks)
+                        bcur[ks] = bnext[ks];
+                    if constexpr (PREFETCH && s + 1 < SUBS)
+                        load_b(bnext, bq + 32 * (s + 1) * LS);
+                    mma_b(acc[ci], bcur);
+                } else {
+                    mma_sub(acc[ci], bq + 32 * s * LS);
+                }
+                if constexpr (s >= 1) {
+                    V nyp = V(0);
+                    if constexpr (NEED_NORMS)
+                        nyp = ncur[32 * (s - 1) + c32];
+                    const bool may = lane_may_match<DT, MET, WMB>(acc[pi], nb, nyp, g);
+                    interleave_mfma_valu<KS * WMB, 8 * WMB + 2>();
+                    if (__builtin_expect(__ballot(may) != 0, 0))
+                        exact_blocks<DT, MET, MODE, WMB>(acc[pi], ibase,
+                                                         t * BN + 32 * (s - 1) + c32, lane, nb,
+                                                         nyp, nrows, g, blk_run, wo);
+                }
+            });
+            j_prev = t * BN + 32 * (SUBS - 1) + c32;
             if constexpr (NEED_NORMS)
-                nyp = ncur[32 * (s - 1) + c32];
-            const bool may = lane_may_match<DT, MET, WMB>(acc[prv], jp, nmin, nyp, g);
-            if (__builtin_expect(__ballot(may) != 0, 0))
-                exact_blocks<DT, MET, MODE, WMB>(acc[prv], ibase, jp, lane, nmin, nyp, nrows, g,
-                                                 blk_run, wo);
-        }
-        if constexpr (MODE == MODE_COUNT) {
-            if (lane == 0)
-                g.block_counts[blk] = (uint32_t)blk_run;
+                ny_prev = ncur[32 * (SUBS - 1) + c32];
+            blk_prev = blk;
+            run_prev = blk_run;
+            have_prev = true;
         }
         if (more)
             norm_store(nnxt, stn);
@@ -525,6 +636,15 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         tile(t, s_q0, s_q1, s_nq0, s_nq1);
         if (t + 1 < t1)
             tile(t + 1, s_q1, s_q0, s_nq1, s_nq0);
+    }
+    if constexpr (PIPE) {
+        if (have_prev) {
+            epilogue(acc[1], j_prev, ny_prev, run_prev);
+            if constexpr (MODE == MODE_COUNT) {
+                if (lane == 0)
+                    g.block_counts[blk_prev] = (uint32_t)run_prev;
+            }
+        }
     }
     if constexpr (MODE == MODE_SINGLE)
         flush_workgroup_out<NW>(wo, wave, lane, g);
@@ -548,8 +668,8 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     typedef Mma<DT> M;
     typedef typename M::acc_t acc_t;
     typedef typename M::val_t V;
-    constexpr int LS = ST_KC;
     constexpr int CPR = ST_KC / 16;                   // 8 chunks per row per K chunk
+    constexpr int LS = (CPR + 1) * 16;                // padded row stride
     constexpr int TCH = (ST_BM + ST_BN) * CPR;        // 2048 chunks
     constexpr int CPT = TCH / 256;                    // 8 per thread
     constexpr int KSC = ST_KC / 32;                   // 4 k-steps per chunk
@@ -593,8 +713,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
 #pragma unroll
         for (int k = 0; k < CPT; ++k) {
             const int c = tid + k * 256;
-            const int r = c / CPR;
-            *(i32x4 *)&s_op[buf][r * LS + 16 * ((c % CPR) ^ swz<CPR>(r))] = st[k];
+            *(i32x4 *)&s_op[buf][(c / CPR) * LS + 16 * (c % CPR)] = st[k];
         }
     };
 
@@ -617,14 +736,12 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         i32x4 st[CPT];
         if (more)
             stage_load(kc + 1, st);
-        // rows of A- and B-blocks start at multiples of 32: swizzle = swz(c32)
-        const uint8_t *pa = &s_op[buf][(64 * wr + c32) * LS];
-        const uint8_t *pbq = &s_op[buf][(ST_BM + 64 * wc + c32) * LS];
-        const int h = half ^ swz<CPR>(c32);
+        const uint8_t *pa = &s_op[buf][(64 * wr + c32) * LS + 16 * half];
+        const uint8_t *pbq = &s_op[buf][(ST_BM + 64 * wc + c32) * LS + 16 * half];
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks) {
             i32x4 fa[2], fb[2];
-            const int off = 16 * ((2 * ks) ^ h);
+            const int off = 32 * ks;
 #pragma unroll
             for (int a = 0; a < 2; ++a)
                 fa[a] = *(const i32x4 *)(pa + 32 * a * LS + off);
@@ -650,6 +767,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         nmin = stage_row_norms<DT, 2>(prow0, lane, s_np[wave], g);
         nrows = &s_np[wave][4 * half];
     }
+    const V nb = bound_base<DT, MET>(nmin, g);
     WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t blk = (uint64_t)(pt * n_qt + qt) * 4 + wave;
     uint64_t blk_run = 0;
@@ -662,9 +780,9 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         if constexpr (NEED_NORMS)
             ny = j < g.n_q ? ((const V *)g.norm_q)[j] : big_val<V>();
         const acc_t blk_acc[2] = {acc[0][s], acc[1][s]};
-        const bool may = lane_may_match<DT, MET, 2>(blk_acc, j, nmin, ny, g);
+        const bool may = lane_may_match<DT, MET, 2>(blk_acc, nb, ny, g);
         if (__ballot(may) != 0)
-            exact_blocks<DT, MET, MODE, 2>(blk_acc, ibase, j, lane, nmin, ny, nrows, g, blk_run,
+            exact_blocks<DT, MET, MODE, 2>(blk_acc, ibase, j, lane, nb, ny, nrows, g, blk_run,
                                            wo);
     }
     if constexpr (MODE == MODE_SINGLE)
@@ -694,10 +812,12 @@ struct ResidentCfg<DT_I8> {
 };
 
 constexpr int RES_NW = 4;
+// Two 32-row A-blocks per wave: with the two accumulator sets of the
+// sub-tile pipeline this keeps every variant within 256 VGPRs.
 template <int DT, int KS>
 constexpr int res_wmb()
 {
-    return (DT == DT_I8 && KS <= 2) ? 4 : 2;
+    return 2;
 }
 // Q tile rows: 128 (four sub-tiles per barrier) unless the rows are so long
 // that two double-buffered tiles per CU would not fit in LDS.
