@@ -6,7 +6,7 @@ sj_join_ip, sj_join_l2, sj_count, sj_destroy, sj_get_stats, sj_last_error)
 with plain integer pointers; `join_ip`, `join_l2` and `count` are
 conveniences over PyTorch device tensors.  This module only marshals
 arguments: every step of the join runs in the library's HIP kernels.  Import
-fails when libsj.so has not been built (python -m paper_2006_12608_amd.build).
+fails when libsj.so has not been built (python paper_2006_12608_amd/build.py).
 """
 from __future__ import annotations
 
@@ -42,7 +42,7 @@ class sj_stats(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
-                          "`python -m paper_2006_12608_amd.build` (hipcc, gfx950)")
+                          "`python paper_2006_12608_amd/build.py` (hipcc, gfx950)")
     lib = ctypes.CDLL(LIB_PATH)
     vp, u32, u64, dbl, i32 = (ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_double,
                               ctypes.c_int)

@@ -1,6 +1,9 @@
 """Build libsj.so for gfx950 with hipcc (in-tree, next to this file).
 
-    python -m paper_2006_12608_amd.build
+    python paper_2006_12608_amd/build.py
+
+Run as a script (or loaded by file path): importing the package itself loads
+the library, which must not be needed to rebuild it.
 """
 from __future__ import annotations
 

@@ -95,6 +95,38 @@ __device__ __forceinline__ uint64_t first_lane_u64(uint64_t v)
     return ((uint64_t)hi << 32) | lo;
 }
 
+// One 16-byte buffer load per lane straight into LDS: lane l's bytes land at
+// lds + 16 l (lds is wave-uniform).  The descriptor covers [base, base + n_bytes);
+// offsets at or past n_bytes read zeros.
+__device__ __forceinline__ void buffer_load_lds16(const uint8_t *base, uint32_t n_bytes,
+                                                  uint32_t voff, uint8_t *lds)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, n_bytes, 0x00020000);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)lds,
+                                             16, voff, 0, 0, 0);
+#endif
+}
+
+// Explicit address spaces for the pair stores: through a generic pointer the
+// compiler may emit flat stores, which count on the LDS counter out of order
+// and so force full waits on every LDS read in the loop that follows.
+// A pair travels as one 64-bit word: i in the low half, j in the high half
+// (the (i, j) uint32 layout of the output buffer).
+typedef __attribute__((address_space(1))) uint64_t global_pair;
+typedef __attribute__((address_space(3))) uint64_t lds_pair;
+
+__device__ __forceinline__ global_pair *pair_slot(const JoinArgs &g, uint64_t k)
+{
+    return (global_pair *)g.pairs + k;
+}
+
+__device__ __forceinline__ uint64_t pack_pair(uint32_t i, uint32_t j)
+{
+    return (uint64_t)i | ((uint64_t)j << 32);
+}
+
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
 {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -139,25 +171,41 @@ __device__ __forceinline__ bool pair_matches(typename Mma<DT>::val_t acc,
 // keeps the rounding order of the exact test: since fl(fl(N_x + N_y) - r2) is
 // monotone in N_x, a lane whose bound fails holds no match.  Columns past n_q
 // are not excluded here (the exact test does that).
-template <int DT, int MET, int WMB>
-__device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&acc)[WMB],
-                                               typename Mma<DT>::val_t nb,
-                                               typename Mma<DT>::val_t ny, const JoinArgs &g)
+template <int DT, int MET>
+__device__ __forceinline__ bool lane_bound(typename Mma<DT>::val_t m, typename Mma<DT>::val_t nb,
+                                           typename Mma<DT>::val_t ny, const JoinArgs &g)
 {
     typedef typename Mma<DT>::val_t V;
-    V m = acc[0][0];
-#pragma unroll
-    for (int a = 0; a < WMB; ++a)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            if (a | r)
-                m = vmax(m, acc[a][r]);
     if constexpr (MET == MET_IP)
         return pair_matches<DT, MET>(m, V(0), V(0), g);
     else if constexpr (DT == DT_I8)
         return 2 * m >= nb + ny;
     else
         return 2.0f * m >= (nb + ny) - g.thr_f;
+}
+
+// Running max over the flattened results v = 16 a + r, v in [LO, HI), of
+// acc[WMB]; LO == 0 starts the chain.
+template <int LO, int HI, int WMB, typename ACC, typename V>
+__device__ __forceinline__ void fold_max(const ACC (&acc)[WMB], V &m)
+{
+    if constexpr (LO < HI) {
+        if constexpr (LO == 0)
+            m = acc[0][0];
+        else
+            m = vmax(m, acc[LO / 16][LO % 16]);
+        fold_max<LO + 1, HI, WMB>(acc, m);
+    }
+}
+
+template <int DT, int MET, int WMB>
+__device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&acc)[WMB],
+                                               typename Mma<DT>::val_t nb,
+                                               typename Mma<DT>::val_t ny, const JoinArgs &g)
+{
+    typename Mma<DT>::val_t m;
+    fold_max<0, 16 * WMB, WMB>(acc, m);
+    return lane_bound<DT, MET>(m, nb, ny, g);
 }
 
 // The per-lane constant of the L2 bound (see lane_may_match).
@@ -175,7 +223,7 @@ __device__ __forceinline__ typename Mma<DT>::val_t bound_base(typename Mma<DT>::
 // matches to its own LDS buffer (no atomics) and moves them to the global pair
 // buffer in bulk, reserving the global slots with one atomicAdd per flush.
 struct WaveOut {
-    uint2 *buf;      // this wave's LDS buffer of `cap` pairs
+    lds_pair *buf;   // this wave's LDS buffer of `cap` pairs
     uint32_t cap;
     uint32_t fill;   // wave-uniform
 };
@@ -190,7 +238,7 @@ __device__ __forceinline__ void flush_wave_out(WaveOut &wo, int lane, const Join
     const uint64_t base = first_lane_u64(b);
     for (uint32_t k = lane; k < wo.fill; k += 64)
         if (base + k < g.cap)
-            *(uint2 *)(g.pairs + 2 * (base + k)) = wo.buf[k];
+            *pair_slot(g, base + k) = wo.buf[k];
     wo.fill = 0;
 }
 
@@ -219,16 +267,18 @@ __device__ __forceinline__ void flush_workgroup_out(WaveOut &wo, int wave, int l
         base += s_fill[w];
     for (uint32_t k = lane; k < wo.fill; k += 64)
         if (base + k < g.cap)
-            *(uint2 *)(g.pairs + 2 * (base + k)) = wo.buf[k];
+            *pair_slot(g, base + k) = wo.buf[k];
     wo.fill = 0;
 }
 
 // exact_block: every result of one 32x32 block (accumulator `acc`, rows
-// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly; ballots give
-// the wave's match count; MODE_SINGLE appends the matches to the wave's LDS
-// staging buffer, MODE_EMIT writes them at the output block's running offset,
-// MODE_COUNT only counts.  Matches are stored so that each store instruction
-// fills consecutive slots.  L2 row norms come from `nrow` (LDS: this lane's rows of the block).
+// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly; the ballot
+// of result r is the wave's match mask for that register, and only registers
+// with a nonzero mask are stored.  MODE_SINGLE appends the matches to the
+// wave's LDS staging buffer, MODE_EMIT writes them at the output block's
+// running offset, MODE_COUNT only counts.  Each store instruction fills
+// consecutive slots.  L2 row norms come from `nrow` (LDS: this lane's rows of
+// the block).
 template <int DT, int MET, int MODE>
 __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, uint32_t ib,
                                             uint32_t j, int lane, typename Mma<DT>::val_t ny,
@@ -248,30 +298,36 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
         else
             return jok && i < g.n_p && pair_matches<DT, MET>(acc[r], V(0), V(0), g);
     };
+    uint64_t mk[16];
     uint32_t tot = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-        tot += (uint32_t)__popcll(__ballot(test(r)));
+    for (int r = 0; r < 16; ++r) {
+        mk[r] = __ballot(test(r));
+        tot += (uint32_t)__popcll(mk[r]);
+    }
     if constexpr (MODE == MODE_COUNT) {
         blk_run += tot;
         return;
     }
     if (tot == 0)
         return;
+    auto store_all = [&](auto &&dst, uint64_t base) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            if (mk[r] != 0) {                      // uniform
+                if ((mk[r] >> lane) & 1)
+                    dst(base + lanes_below(mk[r]), pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
+                base += (uint64_t)__popcll(mk[r]);
+            }
+        }
+    };
     if constexpr (MODE == MODE_SINGLE) {
         if (wo.fill + tot > wo.cap)
             flush_wave_out(wo, lane, g);
         if (tot <= wo.cap) {
-            uint32_t base = wo.fill;
+            const uint32_t base = wo.fill;
             wo.fill += tot;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const bool p = test(r);
-                const uint64_t mk = __ballot(p);
-                if (p)
-                    wo.buf[base + lanes_below(mk)] = make_uint2(ib + 8 * (r >> 2) + (r & 3), j);
-                base += (uint32_t)__popcll(mk);
-            }
+            store_all([&](uint64_t k, uint64_t v) { wo.buf[k] = v; }, base);
             return;
         }
     }
@@ -287,17 +343,12 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
         base = blk_run;
         blk_run += tot;
     }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const bool p = test(r);
-        const uint64_t mk = __ballot(p);
-        if (p) {
-            const uint64_t slot = base + lanes_below(mk);
+    store_all(
+        [&](uint64_t slot, uint64_t v) {
             if (slot < g.cap)
-                *(uint2 *)(g.pairs + 2 * slot) = make_uint2(ib + 8 * (r >> 2) + (r & 3), j);
-        }
-        base += (uint64_t)__popcll(mk);
-    }
+                *pair_slot(g, slot) = v;
+        },
+        base);
 }
 
 // All WMB blocks of a wave's sub-tile that hold a possible match.
@@ -312,7 +363,8 @@ __device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc
 #pragma unroll
     for (int a = 0; a < WMB; ++a) {
         typename Mma<DT>::acc_t one[1] = {acc[a]};
-        if (__ballot(lane_may_match<DT, MET, 1>(one, nb, ny, g)) != 0)
+        // L2: the block's own bound first (the exact test reads row norms)
+        if (MET == MET_IP || __ballot(lane_may_match<DT, MET, 1>(one, nb, ny, g)) != 0)
             exact_block<DT, MET, MODE>(acc[a], ibase + 32 * a, j, lane, ny, nrows + 32 * a, g,
                                        blk_run, wo);
     }
@@ -356,19 +408,6 @@ __device__ __forceinline__ void static_for(F &&f)
     }
 }
 
-// Scheduling hint for one pipelined step: alternate each of the NM MFMAs with
-// a share of the NV VALU instructions of the previous sub-tile's epilogue
-// bound, so that the bound executes while the matrix core is busy.
-template <int NM, int NV>
-__device__ __forceinline__ void interleave_mfma_valu()
-{
-#pragma unroll
-    for (int i = 0; i < NM; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, (NV + NM - 1) / NM, 0); // VALU
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Family 1: P rows resident in registers.
 //
@@ -408,7 +447,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __shared__ V s_nq1[NEED_NORMS ? BN : 1];
     __shared__ V s_np[NEED_NORMS ? NW : 1][NEED_NORMS ? 32 * WMB : 1];
     constexpr int OUT_CAP = MODE == MODE_SINGLE ? 256 : 1;
-    __shared__ uint2 s_out[NW][OUT_CAP];
+    __shared__ uint64_t s_out[NW][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
@@ -439,41 +478,35 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     // first use inside the tile loop also waits for the next tile's prefetch.
     __builtin_amdgcn_s_waitcnt(0);
 
-    // Q tiles go straight from global memory into LDS (no staging registers):
-    // each wave instruction fills 64 consecutive 16-byte LDS positions; the
-    // lane at position p loads chunk p % (CPR + 1) of tile row p / (CPR + 1)
-    // (the pad position reloads chunk 0).  Rows past n_q read the last row
-    // instead (their columns are never reported); chunks past row_bytes read
-    // the row's last chunk (they meet the zero padding of the resident rows).
+    // Q tiles go straight from global memory into LDS (no staging registers)
+    // with buffer loads: each wave instruction fills 64 consecutive 16-byte
+    // LDS positions; the lane at position p loads chunk p % (CPR + 1) of tile
+    // row p / (CPR + 1) (the pad position reloads chunk 0).  The tile's buffer
+    // descriptor ends at row n_q, so rows past it read zeros (their columns
+    // are never reported); chunks past row_bytes read the row's last chunk
+    // (they meet the zero padding of the resident rows).  (A global_load_lds
+    // would do the same, but the compiler then treats every LDS read of the
+    // loop as unordered and drains them all at each use.)
     constexpr int NCALL = (TCH + 64 * NW - 1) / (64 * NW);   // direct loads per wave
     const int wv = __builtin_amdgcn_readfirstlane(wave);
-    // per load: this lane's tile row and its byte offset within a full tile
-    int lrow[NCALL];
-    uint32_t loff[NCALL];
+    uint32_t loff[NCALL];   // this lane's byte offset in the tile, per load
 #pragma unroll
     for (int kk = 0; kk < NCALL; ++kk) {
         const int pos = 64 * (kk * NW + wv) + lane;
         const int cp = pos % (CPR + 1);
-        lrow[kk] = min(pos / (CPR + 1), BN - 1);
-        const uint32_t off = min((uint32_t)(16 * (cp == CPR ? 0 : cp)), g.row_bytes - 16);
-        loff[kk] = (uint32_t)lrow[kk] * g.row_bytes + off;
+        const uint32_t row = min(pos / (CPR + 1), BN - 1);
+        loff[kk] = row * g.row_bytes + min((uint32_t)(16 * (cp == CPR ? 0 : cp)), g.row_bytes - 16);
     }
+    // waves whose last load would start past the tile skip it (uniform)
+    const bool last_call = TCH % (64 * NW) == 0 || 64 * ((NCALL - 1) * NW + wv) < TCH;
     auto stage_issue = [&](uint32_t t, uint8_t *dst) {
-        const bool full = (t + 1) * BN <= g.n_q;          // uniform
-        const uint8_t *qt = g.Q + (size_t)t * BN * g.row_bytes;
+        const uint32_t rows = min(g.n_q - t * BN, (uint32_t)BN);
+        const uint8_t *base = g.Q + (size_t)t * BN * g.row_bytes;
 #pragma unroll
         for (int kk = 0; kk < NCALL; ++kk) {
-            const int k = kk * NW + wv;
-            if (TCH % (64 * NW) != 0 && 64 * k >= TCH)
+            if (kk == NCALL - 1 && !last_call)
                 break;
-            const uint8_t *src = qt + loff[kk];
-            if (!full) {
-                const uint32_t row = min(t * BN + lrow[kk], g.n_q - 1);
-                src = g.Q + (size_t)row * g.row_bytes + (loff[kk] - lrow[kk] * g.row_bytes);
-            }
-            __builtin_amdgcn_global_load_lds(
-                (const void *)src, (__attribute__((address_space(3))) void *)(dst + 1024 * k), 16,
-                0, 0);
+            buffer_load_lds16(base, rows * g.row_bytes, loff[kk], dst + 1024 * (kk * NW + wv));
         }
     };
     auto norm_load = [&](uint32_t t, V &stn) {
@@ -490,22 +523,6 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
                 dst[tid] = stn;
         }
     };
-    // MFMAs of one 32-row sub-tile of Q against the wave's resident rows;
-    // bp points at this lane's row and half (chunk 2 ks + half is 32 ks on).
-    auto mma_sub = [&](acc_t(&acc)[WMB], const uint8_t *bp) {
-        const i32x4 b0 = *(const i32x4 *)bp;
-#pragma unroll
-        for (int a = 0; a < WMB; ++a)
-            acc[a] = M::mma(A[a][0], b0, acc_t{});
-#pragma unroll
-        for (int ks = 1; ks < KS; ++ks) {
-            const i32x4 b = *(const i32x4 *)(bp + 32 * ks);
-#pragma unroll
-            for (int a = 0; a < WMB; ++a)
-                acc[a] = M::mma(A[a][ks], b, acc[a]);
-        }
-    };
-
     if (t0 < t1) {
         V stn = V(0);
         stage_issue(t0, s_q0);
@@ -515,45 +532,42 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
+    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
-    // Epilogue of one wave sub-tile (bound, then the exact path if any lane
-    // may match).
-    auto epilogue = [&](const acc_t(&a)[WMB], uint32_t jp, V nyp, uint64_t &run)
-                        __attribute__((always_inline)) {
-        const bool may = lane_may_match<DT, MET, WMB>(a, nb, nyp, g);
+    // Bound of one wave sub-tile from its running max, then the exact path if
+    // any lane may match.
+    auto check = [&](const acc_t(&a)[WMB], V m, uint32_t jp, V nyp, uint64_t &run)
+                     __attribute__((always_inline)) {
+        const bool may = lane_bound<DT, MET>(m, nb, nyp, g);
         if (__builtin_expect(__ballot(may) != 0, 0))
             exact_blocks<DT, MET, MODE, WMB>(a, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
     };
-    auto load_b = [&](i32x4(&bf)[KS], const uint8_t *bp) __attribute__((always_inline)) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            bf[ks] = *(const i32x4 *)(bp + 32 * ks);
-    };
-    auto mma_b = [&](acc_t(&a)[WMB], const i32x4(&bf)[KS]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int ai = 0; ai < WMB; ++ai)
-            a[ai] = M::mma(A[ai][0], bf[0], acc_t{});
-#pragma unroll
-        for (int ks = 1; ks < KS; ++ks)
-#pragma unroll
-            for (int ai = 0; ai < WMB; ++ai)
-                a[ai] = M::mma(A[ai][ks], bf[ks], a[ai]);
-    };
 
-    // Sub-tile pipeline state, carried across Q tiles: the last sub-tile's
-    // epilogue of tile t runs at the start of tile t + 1, while the first
-    // B-fragments of tile t + 1 are in flight.  For rows of at most 4 k-steps
-    // the B-fragments of sub-tile s + 1 are also read during sub-tile s.
-    constexpr bool PREFETCH = KS <= 4;
-    static_assert(!PIPE || SUBS % 2 == 0, "the accumulator ping-pong needs an even sub-tile count");
-    acc_t acc[2][WMB];
+    // A tile is a stream of SUBS * KS k-steps (sub-tile s = step / KS).  Each
+    // step issues the LDS read of the B-fragment LOOK steps ahead (a ring of
+    // LOOK + 1 fragments, continued across sub-tiles) and the WMB MFMAs of its
+    // own fragment; with two accumulator sets it also folds 16 WMB / KS results
+    // of the previous sub-tile into that sub-tile's running max, so the
+    // epilogue's VALU work runs beside the matrix cores.  Scheduling barriers
+    // between steps keep this order (left alone, the compiler drains every
+    // read right before its MFMAs).
+    constexpr int NSTEP = SUBS * KS;
+    constexpr int LOOK = KS >= 16 ? 2 : 3;
+    constexpr int RING = LOOK + 1;
+    constexpr int NVAL = 16 * WMB;
+    constexpr int NACC = PIPE ? 2 : 1;
+    acc_t acc[NACC][WMB];
+#pragma unroll
+    for (int c = 0; c < NACC; ++c)
+#pragma unroll
+        for (int a = 0; a < WMB; ++a)
+            acc[c][a] = acc_t{};
+    // Previous sub-tile of the pipeline when it belongs to the previous tile.
     bool have_prev = false;
     uint32_t j_prev = 0;
     V ny_prev = V(0);
     uint64_t blk_prev = 0, run_prev = 0;
 
-    // One Q tile: prefetch tile t+1 into `nxt`, compute tile t from `cur`.
     auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt)
                     __attribute__((always_inline)) {
         const bool more = t + 1 < t1;
@@ -567,65 +581,62 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         if constexpr (MODE == MODE_EMIT)
             blk_run = g.block_offsets[blk];
 
+        // this lane's B-fragment of step q: row 32 (q / KS) + c32, chunk
+        // 2 (q % KS) + half
         const uint8_t *bq = cur + c32 * LS + 16 * half;
-        if constexpr (!PIPE) {
-            // long rows: one accumulator set; the other wave on the SIMD covers
-            // the epilogue
-            static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
-                constexpr int s = decltype(S)::value;
-                acc_t acc1[WMB];
-                mma_sub(acc1, bq + 32 * s * LS);
-                V nyp = V(0);
-                if constexpr (NEED_NORMS)
-                    nyp = ncur[32 * s + c32];
-                epilogue(acc1, t * BN + 32 * s + c32, nyp, blk_run);
-            });
-            if constexpr (MODE == MODE_COUNT) {
-                if (lane == 0)
-                    g.block_counts[blk] = (uint32_t)blk_run;
-            }
-        } else {
-            i32x4 bnext[KS];
-            load_b(bnext, bq);
-            if (have_prev) {
-                epilogue(acc[1], j_prev, ny_prev, run_prev);
-                if constexpr (MODE == MODE_COUNT) {
-                    if (lane == 0)
-                        g.block_counts[blk_prev] = (uint32_t)run_prev;
-                }
-            }
-            static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
-                constexpr int s = decltype(S)::value;
-                constexpr int ci = s & 1, pi = ci ^ 1;
-                if constexpr (s == 0 || PREFETCH) {
-                    i32x4 bcur[KS];
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks)
-                        bcur[ks] = bnext[ks];
-                    if constexpr (PREFETCH && s + 1 < SUBS)
-                        load_b(bnext, bq + 32 * (s + 1) * LS);
-                    mma_b(acc[ci], bcur);
-                } else {
-                    mma_sub(acc[ci], bq + 32 * s * LS);
-                }
-                if constexpr (s >= 1) {
-                    V nyp = V(0);
-                    if constexpr (NEED_NORMS)
-                        nyp = ncur[32 * (s - 1) + c32];
-                    const bool may = lane_may_match<DT, MET, WMB>(acc[pi], nb, nyp, g);
-                    interleave_mfma_valu<KS * WMB, 8 * WMB + 2>();
-                    if (__builtin_expect(__ballot(may) != 0, 0))
-                        exact_blocks<DT, MET, MODE, WMB>(acc[pi], ibase,
-                                                         t * BN + 32 * (s - 1) + c32, lane, nb,
-                                                         nyp, nrows, g, blk_run, wo);
-                }
-            });
-            j_prev = t * BN + 32 * (SUBS - 1) + c32;
+        i32x4 ring[RING];
+        static_for<0, (LOOK < NSTEP ? LOOK : NSTEP)>([&](auto Q) __attribute__((always_inline)) {
+            constexpr int q = decltype(Q)::value;
+            ring[q] = *(const i32x4 *)(bq + (q / KS) * 32 * LS + (q % KS) * 32);
+        });
+        V ny_sub[SUBS];
+        static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
+            constexpr int s = decltype(S)::value;
+            constexpr int ci = PIPE ? (s & 1) : 0, pi = PIPE ? (ci ^ 1) : 0;
+            ny_sub[s] = V(0);
             if constexpr (NEED_NORMS)
-                ny_prev = ncur[32 * (SUBS - 1) + c32];
+                ny_sub[s] = ncur[32 * s + c32];
+            V m = V(0);
+            static_for<0, KS>([&](auto K) __attribute__((always_inline)) {
+                constexpr int ks = decltype(K)::value, q = s * KS + ks;
+                if constexpr (q + LOOK < NSTEP) {
+                    constexpr int qn = q + LOOK;
+                    ring[qn % RING] =
+                        *(const i32x4 *)(bq + (qn / KS) * 32 * LS + (qn % KS) * 32);
+                }
+#pragma unroll
+                for (int a = 0; a < WMB; ++a)
+                    acc[ci][a] = M::mma(A[a][ks], ring[q % RING], ks == 0 ? acc_t{} : acc[ci][a]);
+                if constexpr (PIPE)
+                    fold_max<ks * NVAL / KS, (ks + 1) * NVAL / KS, WMB>(acc[pi], m);
+                __builtin_amdgcn_sched_barrier(0);
+            });
+            if constexpr (PIPE) {
+                if constexpr (s == 0) {
+                    if (have_prev) {
+                        check(acc[pi], m, j_prev, ny_prev, run_prev);
+                        if constexpr (MODE == MODE_COUNT) {
+                            if (lane == 0)
+                                g.block_counts[blk_prev] = (uint32_t)run_prev;
+                        }
+                    }
+                } else {
+                    check(acc[pi], m, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
+                }
+            } else {
+                fold_max<0, NVAL, WMB>(acc[0], m);
+                check(acc[0], m, t * BN + 32 * s + c32, ny_sub[s], blk_run);
+            }
+        });
+        if constexpr (PIPE) {
+            j_prev = t * BN + 32 * (SUBS - 1) + c32;
+            ny_prev = ny_sub[SUBS - 1];
             blk_prev = blk;
             run_prev = blk_run;
             have_prev = true;
+        } else if constexpr (MODE == MODE_COUNT) {
+            if (lane == 0)
+                g.block_counts[blk] = (uint32_t)blk_run;
         }
         if (more)
             norm_store(nnxt, stn);
@@ -639,7 +650,9 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     }
     if constexpr (PIPE) {
         if (have_prev) {
-            epilogue(acc[1], j_prev, ny_prev, run_prev);
+            V m;
+            fold_max<0, NVAL, WMB>(acc[NACC - 1], m);
+            check(acc[NACC - 1], m, j_prev, ny_prev, run_prev);
             if constexpr (MODE == MODE_COUNT) {
                 if (lane == 0)
                     g.block_counts[blk_prev] = (uint32_t)run_prev;
@@ -678,7 +691,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     __shared__ __attribute__((aligned(16))) uint8_t s_op[2][(ST_BM + ST_BN) * LS];
     __shared__ V s_np[NEED_NORMS ? 4 : 1][NEED_NORMS ? 64 : 1];
     constexpr int OUT_CAP = MODE == MODE_SINGLE ? 128 : 1;
-    __shared__ uint2 s_out[4][OUT_CAP];
+    __shared__ uint64_t s_out[4][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
@@ -768,7 +781,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         nrows = &s_np[wave][4 * half];
     }
     const V nb = bound_base<DT, MET>(nmin, g);
-    WaveOut wo{s_out[wave], (uint32_t)OUT_CAP, 0u};
+    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u};
     const uint64_t blk = (uint64_t)(pt * n_qt + qt) * 4 + wave;
     uint64_t blk_run = 0;
     if constexpr (MODE == MODE_EMIT)
