@@ -289,22 +289,31 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
     // Opaque to the optimiser: keeps the per-result row indices from being
     // hoisted into (and occupying registers of) the caller's main loop.
     asm volatile("" : "+v"(ib));
-    const bool jok = j < g.n_q;
-    auto test = [&](int r) -> bool {
-        const uint32_t i = ib + 8 * (r >> 2) + (r & 3);
+    auto score_ok = [&](int r) -> bool {
         if constexpr (MET == MET_L2)
-            return jok && i < g.n_p &&
-                   pair_matches<DT, MET>(acc[r], nrow[8 * (r >> 2) + (r & 3)], ny, g);
+            return pair_matches<DT, MET>(acc[r], nrow[8 * (r >> 2) + (r & 3)], ny, g);
         else
-            return jok && i < g.n_p && pair_matches<DT, MET>(acc[r], V(0), V(0), g);
+            return pair_matches<DT, MET>(acc[r], V(0), V(0), g);
     };
     uint64_t mk[16];
+    // lane 0 holds the block's first row and column
+    const uint32_t ib0 = __builtin_amdgcn_readfirstlane(ib);
+    const uint32_t j0 = __builtin_amdgcn_readfirstlane(j);
+    if ((uint64_t)ib0 + 32 <= g.n_p && (uint64_t)j0 + 32 <= g.n_q) {
+        // the whole block lies inside P x Q (uniform)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            mk[r] = __ballot(score_ok(r));
+    } else {
+        const bool jok = j < g.n_q;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            mk[r] = __ballot(jok && ib + 8 * (r >> 2) + (r & 3) < g.n_p && score_ok(r));
+    }
     uint32_t tot = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        mk[r] = __ballot(test(r));
+    for (int r = 0; r < 16; ++r)
         tot += (uint32_t)__popcll(mk[r]);
-    }
     if constexpr (MODE == MODE_COUNT) {
         blk_run += tot;
         return;
