@@ -86,6 +86,21 @@ def cpu_baseline(w, target_s: float = 12.0):
                       f"({n_rows * w.n_q:.3g} pair evaluations, {el:.1f} s, {r.total} matches)"}
 
 
+def copy_calibration():
+    """A plain device copy of known size: 256 MiB read and 256 MiB written per
+    launch.  Its counter readings give the factors that turn the join kernel's
+    FETCH_SIZE and WRITE_SIZE into bytes."""
+    import torch
+    a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_launch": 256 << 20, "launches": 3}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -94,7 +109,13 @@ def main():
     import workloads
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.NAMES)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy a 256 MiB buffer three times (the reference kernel for "
+                         "scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters to HBM bytes)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the join shards "
               "by rows of P across GPUs, which this build does not run", file=sys.stderr)

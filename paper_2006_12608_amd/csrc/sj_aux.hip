@@ -13,12 +13,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 // ------------------------------------------------------------------ planning
 // Resident-P limits: 32-byte k-steps of the largest variant (16 for 2-byte
 // elements, 8 for int8, i.e. d <= 256 either way); workgroup of 4 waves over
-// 32 * WMB rows each; Q tiles of 128 rows (64 for the longest rows).  Must
-// agree with sj_join_kernels.h.
+// 32 * WMB rows each (WMB = 4 for int8 rows of at most 64 bytes, else 2); Q
+// tiles of 256 rows for rows of at most 64 bytes, 128 up to 256 bytes and 64
+// for the longest rows.  Must agree with sj_join_kernels.h.
 static const int kResKS16[4] = {2, 4, 8, 16};
 static const int kResKS8[4] = {1, 2, 4, 8};
 static const uint32_t kResNW = 4;
-static uint32_t res_bn(int ks) { return ks <= 8 ? 128 : 64; }
+static uint32_t res_bn(int ks) { return ks <= 2 ? 256 : ks <= 8 ? 128 : 64; }
 static const uint32_t kStBM = 128, kStBN = 128, kStG = 8;
 
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
@@ -35,7 +36,7 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
         }
     if (variant >= 0) {
         const int ks = tab[variant];
-        const uint32_t wmb = 2;
+        const uint32_t wmb = (dtype == DT_I8 && ks <= 2) ? 4 : 2;
         const uint32_t bm = kResNW * 32 * wmb;
         const uint64_t n_pb = (n_p + (uint64_t)bm - 1) / bm;
         const uint64_t bn = res_bn(ks);

@@ -834,19 +834,23 @@ struct ResidentCfg<DT_I8> {
 };
 
 constexpr int RES_NW = 4;
-// Two 32-row A-blocks per wave: with the two accumulator sets of the
-// sub-tile pipeline this keeps every variant within 256 VGPRs.
+// 32-row A-blocks per wave: two, which with the two accumulator sets of the
+// sub-tile pipeline keeps every variant within 256 VGPRs; four for int8 rows
+// of at most 64 bytes, whose A-fragments are small (each B-fragment read from
+// LDS then feeds four MFMAs, and a workgroup covers 512 rows of P).
 template <int DT, int KS>
 constexpr int res_wmb()
 {
-    return 2;
+    return DT == DT_I8 && KS <= 2 ? 4 : 2;
 }
-// Q tile rows: 128 (four sub-tiles per barrier) unless the rows are so long
-// that two double-buffered tiles per CU would not fit in LDS.
+// Q tile rows: 256 for rows of at most 64 bytes (a short tile would spend a
+// large share of its time in the barrier and the next tile's loads), else 128
+// (four sub-tiles per barrier) unless the rows are so long that two
+// double-buffered tiles per CU would not fit in LDS.
 template <int KS>
 constexpr int res_bn()
 {
-    return KS <= 8 ? 128 : 64;
+    return KS <= 2 ? 256 : KS <= 8 ? 128 : 64;
 }
 
 template <int DT, int MET, int MODE, int V>
