@@ -99,13 +99,14 @@ __device__ __forceinline__ uint64_t first_lane_u64(uint64_t v)
 // lds + 16 l (lds is wave-uniform).  The descriptor covers [base, base + n_bytes);
 // offsets at or past n_bytes read zeros.
 __device__ __forceinline__ void buffer_load_lds16(const uint8_t *base, uint32_t n_bytes,
-                                                  uint32_t voff, uint8_t *lds)
+                                                  uint32_t voff, uint8_t *lds,
+                                                  uint32_t soff = 0)
 {
 #if defined(__HIP_DEVICE_COMPILE__)
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, n_bytes, 0x00020000);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)lds,
-                                             16, voff, 0, 0, 0);
+                                             16, voff, soff, 0, 0);
 #endif
 }
 
@@ -692,12 +693,17 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     typedef typename M::val_t V;
     constexpr int CPR = ST_KC / 16;                   // 8 chunks per row per K chunk
     constexpr int LS = (CPR + 1) * 16;                // padded row stride
-    constexpr int TCH = (ST_BM + ST_BN) * CPR;        // 2048 chunks
-    constexpr int CPT = TCH / 256;                    // 8 per thread
+    constexpr int ROWS = ST_BM + ST_BN;               // P rows, then Q rows
+    constexpr int NPOS = ROWS * (CPR + 1);            // 2304 LDS positions per stage
+    constexpr int NLD = NPOS / 256;                   // 9 direct loads per thread
+    constexpr int P_LOADS = ST_BM * (CPR + 1) / 64;   // wave loads 0..17 fill P rows
     constexpr int KSC = ST_KC / 32;                   // 4 k-steps per chunk
     constexpr bool NEED_NORMS = (MET == MET_L2);
+    static_assert(NPOS % 256 == 0 && (ST_BM * (CPR + 1)) % 64 == 0, "load layout");
 
-    __shared__ __attribute__((aligned(16))) uint8_t s_op[2][(ST_BM + ST_BN) * LS];
+    // two stages as distinct arrays (see join_resident)
+    __shared__ __attribute__((aligned(16))) uint8_t s_op0[ROWS * LS];
+    __shared__ __attribute__((aligned(16))) uint8_t s_op1[ROWS * LS];
     __shared__ V s_np[NEED_NORMS ? 4 : 1][NEED_NORMS ? 64 : 1];
     constexpr int OUT_CAP = MODE == MODE_SINGLE ? 128 : 1;
     __shared__ uint64_t s_out[4][OUT_CAP];
@@ -721,21 +727,45 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     const uint32_t p0 = pt * ST_BM, q0 = qt * ST_BN;
     const uint32_t n_chunks = (g.row_bytes + ST_KC - 1) / ST_KC;
 
-    auto stage_load = [&](uint32_t kc, i32x4(&st)[CPT]) {
+    // Direct loads: wave instruction k = wave + 4 i fills LDS positions
+    // [64 k, 64 k + 64); position p holds chunk p % (CPR + 1) (the pad
+    // position repeats chunk 0) of tile row p / (CPR + 1).  Per-lane offsets
+    // within the P or Q descriptor (rows past n_p / n_q read zeros), plus the
+    // chunk's byte offset kc * KC.
+    const uint32_t bytes_p = min(g.n_p - p0, (uint32_t)ST_BM) * g.row_bytes;
+    const uint32_t bytes_q = min(g.n_q - q0, (uint32_t)ST_BN) * g.row_bytes;
+    const uint8_t *base_p = g.P + (size_t)p0 * g.row_bytes;
+    const uint8_t *base_q = g.Q + (size_t)q0 * g.row_bytes;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    uint32_t voff[NLD], vcol[NLD];
 #pragma unroll
-        for (int k = 0; k < CPT; ++k) {
-            const int c = tid + k * 256;
-            const int r = c / CPR, cc = c % CPR;
-            const uint32_t off = kc * ST_KC + 16 * cc;
-            st[k] = r < ST_BM ? load_chunk(g.P, p0 + r, g.n_p, g.row_bytes, off)
-                              : load_chunk(g.Q, q0 + r - ST_BM, g.n_q, g.row_bytes, off);
-        }
-    };
-    auto stage_store = [&](int buf, const i32x4(&st)[CPT]) {
+    for (int i = 0; i < NLD; ++i) {
+        const int pos = 64 * (wv + 4 * i) + lane;
+        const int r = pos / (CPR + 1), cp = pos % (CPR + 1);
+        vcol[i] = 16 * (cp == CPR ? 0 : cp);
+        voff[i] = (uint32_t)(r < ST_BM ? r : r - ST_BM) * g.row_bytes + vcol[i];
+    }
+    auto stage_issue = [&](uint32_t kc, uint8_t *dst) {
+        const uint32_t kb = kc * ST_KC;
+        if (kb + ST_KC <= g.row_bytes) {                 // uniform
 #pragma unroll
-        for (int k = 0; k < CPT; ++k) {
-            const int c = tid + k * 256;
-            *(i32x4 *)&s_op[buf][(c / CPR) * LS + 16 * (c % CPR)] = st[k];
+            for (int i = 0; i < NLD; ++i) {
+                const int k = wv + 4 * i;
+                const bool is_p = k < P_LOADS;
+                buffer_load_lds16(is_p ? base_p : base_q, is_p ? bytes_p : bytes_q, voff[i],
+                                  dst + 1024 * k, kb);
+            }
+        } else {
+            // the last chunk of a row that is not a multiple of KC: columns
+            // past the row read zeros (offset at the descriptor's end)
+#pragma unroll
+            for (int i = 0; i < NLD; ++i) {
+                const int k = wv + 4 * i;
+                const bool is_p = k < P_LOADS;
+                const uint32_t nbytes = is_p ? bytes_p : bytes_q;
+                const uint32_t vo = kb + vcol[i] >= g.row_bytes ? nbytes : voff[i] + kb;
+                buffer_load_lds16(is_p ? base_p : base_q, nbytes, vo, dst + 1024 * k);
+            }
         }
     };
 
@@ -746,39 +776,48 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         for (int s = 0; s < 2; ++s)
             acc[a][s] = acc_t{};
 
-    {
-        i32x4 st[CPT];
-        stage_load(0, st);
-        stage_store(0, st);
-    }
-    __syncthreads();
-    for (uint32_t kc = 0; kc < n_chunks; ++kc) {
-        const int buf = kc & 1;
-        const bool more = kc + 1 < n_chunks;
-        i32x4 st[CPT];
-        if (more)
-            stage_load(kc + 1, st);
-        const uint8_t *pa = &s_op[buf][(64 * wr + c32) * LS + 16 * half];
-        const uint8_t *pbq = &s_op[buf][(ST_BM + 64 * wc + c32) * LS + 16 * half];
-#pragma unroll
-        for (int ks = 0; ks < KSC; ++ks) {
-            i32x4 fa[2], fb[2];
-            const int off = 32 * ks;
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-                fa[a] = *(const i32x4 *)(pa + 32 * a * LS + off);
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-                fb[s] = *(const i32x4 *)(pbq + 32 * s * LS + off);
+    // One K chunk: KSC k-steps, each reading two A- and two B-fragments (a
+    // ring of LOOK + 1 steps, LOOK steps ahead) and issuing four MFMAs.
+    constexpr int LOOK = 2, RING = LOOK + 1;
+    auto chunk = [&](uint32_t kc, const uint8_t *cur, uint8_t *nxt)
+                     __attribute__((always_inline)) {
+        if (kc + 1 < n_chunks)
+            stage_issue(kc + 1, nxt);
+        const uint8_t *pa = cur + (64 * wr + c32) * LS + 16 * half;
+        const uint8_t *pb = cur + (ST_BM + 64 * wc + c32) * LS + 16 * half;
+        i32x4 ring[RING][4];
+        auto fetch = [&](i32x4(&f)[4], int ks) __attribute__((always_inline)) {
+            f[0] = *(const i32x4 *)(pa + 32 * ks);
+            f[1] = *(const i32x4 *)(pa + 32 * LS + 32 * ks);
+            f[2] = *(const i32x4 *)(pb + 32 * ks);
+            f[3] = *(const i32x4 *)(pb + 32 * LS + 32 * ks);
+        };
+        static_for<0, LOOK>([&](auto Q) __attribute__((always_inline)) {
+            fetch(ring[decltype(Q)::value], decltype(Q)::value);
+        });
+        static_for<0, KSC>([&](auto K) __attribute__((always_inline)) {
+            constexpr int ks = decltype(K)::value;
+            if constexpr (ks + LOOK < KSC)
+                fetch(ring[(ks + LOOK) % RING], ks + LOOK);
+            const i32x4(&f)[4] = ring[ks % RING];
 #pragma unroll
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int s = 0; s < 2; ++s)
-                    acc[a][s] = M::mma(fa[a], fb[s], acc[a][s]);
-        }
-        if (more)
-            stage_store(buf ^ 1, st);
+                    acc[a][s] = M::mma(f[a], f[2 + s], acc[a][s]);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of chunk kc + 1 landed
         __syncthreads();
+    };
+
+    stage_issue(0, s_op0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (uint32_t kc = 0; kc < n_chunks; kc += 2) {
+        chunk(kc, s_op0, s_op1);
+        if (kc + 1 < n_chunks)
+            chunk(kc + 1, s_op1, s_op0);
     }
 
     const uint32_t prow0 = p0 + 64 * wr;
