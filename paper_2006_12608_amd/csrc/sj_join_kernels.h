@@ -220,23 +220,33 @@ __device__ __forceinline__ typename Mma<DT>::val_t bound_base(typename Mma<DT>::
         return nmin;
 }
 
-// Per-wave output staging for the single-pass mode: a wave appends its
-// matches to its own LDS buffer (no atomics) and moves them to the global pair
-// buffer in bulk, reserving the global slots with one atomicAdd per flush.
+// Per-wave output staging: a wave appends its matches to its own LDS buffer
+// and moves them to the global pair buffer in bulk, with coalesced stores.
+// Single-pass mode reserves the global slots with one atomicAdd per flush;
+// the emit pass (when a kernel stages there) writes them in order from the
+// output block's offset (`dst`).
 struct WaveOut {
     lds_pair *buf;   // this wave's LDS buffer of `cap` pairs
     uint32_t cap;
     uint32_t fill;   // wave-uniform
+    uint64_t dst;    // emit pass: next global slot of this wave's block
 };
 
+template <int MODE>
 __device__ __forceinline__ void flush_wave_out(WaveOut &wo, int lane, const JoinArgs &g)
 {
     if (wo.fill == 0)
         return;
-    unsigned long long b = 0;
-    if (lane == 0)
-        b = atomicAdd(g.counter, (unsigned long long)wo.fill);
-    const uint64_t base = first_lane_u64(b);
+    uint64_t base;
+    if constexpr (MODE == MODE_EMIT) {
+        base = wo.dst;
+        wo.dst += wo.fill;
+    } else {
+        unsigned long long b = 0;
+        if (lane == 0)
+            b = atomicAdd(g.counter, (unsigned long long)wo.fill);
+        base = first_lane_u64(b);
+    }
     for (uint32_t k = lane; k < wo.fill; k += 64)
         if (base + k < g.cap)
             *pair_slot(g, base + k) = wo.buf[k];
@@ -331,9 +341,10 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
             }
         }
     };
-    if constexpr (MODE == MODE_SINGLE) {
+    // staged (single pass; emit pass when the kernel gives a staging buffer)
+    if (MODE == MODE_SINGLE || wo.cap > 1) {
         if (wo.fill + tot > wo.cap)
-            flush_wave_out(wo, lane, g);
+            flush_wave_out<MODE>(wo, lane, g);
         if (tot <= wo.cap) {
             const uint32_t base = wo.fill;
             wo.fill += tot;
@@ -542,7 +553,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u};
+    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u, 0ull};
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
     // Bound of one wave sub-tile from its running max, then the exact path if
     // any lane may match.
@@ -705,8 +716,6 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     __shared__ __attribute__((aligned(16))) uint8_t s_op0[ROWS * LS];
     __shared__ __attribute__((aligned(16))) uint8_t s_op1[ROWS * LS];
     __shared__ V s_np[NEED_NORMS ? 4 : 1][NEED_NORMS ? 64 : 1];
-    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 128 : 1;
-    __shared__ uint64_t s_out[4][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
@@ -829,11 +838,17 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         nrows = &s_np[wave][4 * half];
     }
     const V nb = bound_base<DT, MET>(nmin, g);
-    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u};
+    // After the last chunk's barrier the operand stages are free: each wave
+    // stages its matches in a quarter of them (2304 pairs), for the single
+    // pass and the emit pass alike.
+    constexpr uint32_t STAGE_BYTES = ROWS * LS / 2;
+    static_assert(STAGE_BYTES / 8 >= 1024, "a whole 32x32 block must fit the staging buffer");
+    uint8_t *stage_mem = (wave < 2 ? s_op0 : s_op1) + (wave & 1) * STAGE_BYTES;
+    WaveOut wo{(lds_pair *)stage_mem, STAGE_BYTES / 8, 0u, 0ull};
     const uint64_t blk = (uint64_t)(pt * n_qt + qt) * 4 + wave;
     uint64_t blk_run = 0;
     if constexpr (MODE == MODE_EMIT)
-        blk_run = g.block_offsets[blk];
+        wo.dst = g.block_offsets[blk];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const uint32_t j = q0 + 64 * wc + 32 * s + c32;
@@ -848,6 +863,8 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     }
     if constexpr (MODE == MODE_SINGLE)
         flush_workgroup_out<4>(wo, wave, lane, g);
+    if constexpr (MODE == MODE_EMIT)
+        flush_wave_out<MODE>(wo, lane, g);
     if constexpr (MODE == MODE_COUNT) {
         if (lane == 0)
             g.block_counts[blk] = (uint32_t)blk_run;
