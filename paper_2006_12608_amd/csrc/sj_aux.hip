@@ -20,7 +20,7 @@ static const int kResKS16[4] = {2, 4, 8, 16};
 static const int kResKS8[4] = {1, 2, 4, 8};
 static const uint32_t kResNW = 4;
 static uint32_t res_bn(int ks) { return ks <= 2 ? 256 : ks <= 8 ? 128 : 64; }
-static const uint32_t kStBM = 128, kStBN = 128, kStG = 8;
+static const uint32_t kStBM = 256, kStBN = 256, kStG = 8, kStNW = 8;
 
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
                Plan *plan)
@@ -67,9 +67,9 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
     plan->family = FAM_STREAMED;
     plan->variant = 0;
     plan->qsplit = 1;
-    plan->block = 256;
+    plan->block = kStNW * 64;
     plan->grid = (uint32_t)grid;
-    plan->n_blocks = n_pt * n_qt * 4;
+    plan->n_blocks = n_pt * n_qt * kStNW;
     return true;
 }
 

@@ -688,16 +688,17 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
 // Family 2: both operands streamed through LDS in chunks of KC bytes of d
 // (for rows too long to keep in registers).
 //
-// A workgroup of 4 waves computes a 128 x 128 output tile; wave (wr, wc) owns
-// rows [64 wr, +64) (two A-blocks) and columns [64 wc, +64) (two sub-tiles), so
-// it holds four 32x32 accumulators.  P and Q chunks are double-buffered in LDS.
-// Tiles are visited in groups of 8 P tiles x 8 Q tiles so that concurrently
-// running workgroups share their operand rows in L2.
-// Output block = one wave's 64 x 64 region; index = tile * 4 + wave.
-constexpr int ST_BM = 128, ST_BN = 128, ST_KC = 128;
+// A workgroup of 8 waves (two per SIMD) computes a 256 x 256 output tile; wave
+// (wr, wc), wr < 4, wc < 2, owns rows [64 wr, +64) (two A-blocks) and columns
+// [128 wc, +128) (four B-blocks), so a k-step reads 2 A- and 4 B-fragments
+// from LDS for 8 MFMAs.  P and Q chunks are double-buffered in LDS (one
+// workgroup per CU).  Tiles are visited in groups of 8 P tiles x 8 Q tiles so
+// that concurrently running workgroups share their operand rows in L2.
+// Output block = one wave's 64 x 128 region; index = tile * 8 + wave.
+constexpr int ST_BM = 256, ST_BN = 256, ST_KC = 128, ST_NW = 8;
 
 template <int DT, int MET, int MODE>
-__global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
+__global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
 {
     typedef Mma<DT> M;
     typedef typename M::acc_t acc_t;
@@ -705,17 +706,19 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     constexpr int CPR = ST_KC / 16;                   // 8 chunks per row per K chunk
     constexpr int LS = (CPR + 1) * 16;                // padded row stride
     constexpr int ROWS = ST_BM + ST_BN;               // P rows, then Q rows
-    constexpr int NPOS = ROWS * (CPR + 1);            // 2304 LDS positions per stage
-    constexpr int NLD = NPOS / 256;                   // 9 direct loads per thread
-    constexpr int P_LOADS = ST_BM * (CPR + 1) / 64;   // wave loads 0..17 fill P rows
-    constexpr int KSC = ST_KC / 32;                   // 4 k-steps per chunk
+    constexpr int NPOS = ROWS * (CPR + 1);            // LDS positions per stage
+    constexpr int NT = ST_NW * 64;                    // threads
+    constexpr int NLD = NPOS / NT;                    // direct loads per thread
+    constexpr int P_LOADS = ST_BM * (CPR + 1) / 64;   // wave loads below this fill P rows
+    constexpr int KSC = ST_KC / 32;                   // k-steps per chunk
+    constexpr int SA = 2, SB = 4;                     // A- and B-blocks per wave
     constexpr bool NEED_NORMS = (MET == MET_L2);
-    static_assert(NPOS % 256 == 0 && (ST_BM * (CPR + 1)) % 64 == 0, "load layout");
+    static_assert(NPOS % NT == 0 && (ST_BM * (CPR + 1)) % 64 == 0, "load layout");
 
     // two stages as distinct arrays (see join_resident)
     __shared__ __attribute__((aligned(16))) uint8_t s_op0[ROWS * LS];
     __shared__ __attribute__((aligned(16))) uint8_t s_op1[ROWS * LS];
-    __shared__ V s_np[NEED_NORMS ? 4 : 1][NEED_NORMS ? 64 : 1];
+    __shared__ V s_np[NEED_NORMS ? ST_NW : 1][NEED_NORMS ? 32 * SA : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
@@ -736,11 +739,11 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     const uint32_t p0 = pt * ST_BM, q0 = qt * ST_BN;
     const uint32_t n_chunks = (g.row_bytes + ST_KC - 1) / ST_KC;
 
-    // Direct loads: wave instruction k = wave + 4 i fills LDS positions
-    // [64 k, 64 k + 64); position p holds chunk p % (CPR + 1) (the pad
-    // position repeats chunk 0) of tile row p / (CPR + 1).  Per-lane offsets
-    // within the P or Q descriptor (rows past n_p / n_q read zeros), plus the
-    // chunk's byte offset kc * KC.
+    // Direct loads: wave instruction k = wave + ST_NW i fills LDS positions
+    // [64 k, 64 k + 64); position p holds chunk p % (CPR + 1) (the pad position
+    // repeats chunk 0) of tile row p / (CPR + 1).  Per-lane offsets within the
+    // P or Q descriptor (rows past n_p / n_q read zeros), plus the chunk's byte
+    // offset kc * KC.
     const uint32_t bytes_p = min(g.n_p - p0, (uint32_t)ST_BM) * g.row_bytes;
     const uint32_t bytes_q = min(g.n_q - q0, (uint32_t)ST_BN) * g.row_bytes;
     const uint8_t *base_p = g.P + (size_t)p0 * g.row_bytes;
@@ -749,7 +752,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     uint32_t voff[NLD], vcol[NLD];
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-        const int pos = 64 * (wv + 4 * i) + lane;
+        const int pos = 64 * (wv + ST_NW * i) + lane;
         const int r = pos / (CPR + 1), cp = pos % (CPR + 1);
         vcol[i] = 16 * (cp == CPR ? 0 : cp);
         voff[i] = (uint32_t)(r < ST_BM ? r : r - ST_BM) * g.row_bytes + vcol[i];
@@ -759,7 +762,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         if (kb + ST_KC <= g.row_bytes) {                 // uniform
 #pragma unroll
             for (int i = 0; i < NLD; ++i) {
-                const int k = wv + 4 * i;
+                const int k = wv + ST_NW * i;
                 const bool is_p = k < P_LOADS;
                 buffer_load_lds16(is_p ? base_p : base_q, is_p ? bytes_p : bytes_q, voff[i],
                                   dst + 1024 * k, kb);
@@ -769,7 +772,7 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
             // past the row read zeros (offset at the descriptor's end)
 #pragma unroll
             for (int i = 0; i < NLD; ++i) {
-                const int k = wv + 4 * i;
+                const int k = wv + ST_NW * i;
                 const bool is_p = k < P_LOADS;
                 const uint32_t nbytes = is_p ? bytes_p : bytes_q;
                 const uint32_t vo = kb + vcol[i] >= g.row_bytes ? nbytes : voff[i] + kb;
@@ -778,28 +781,30 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
         }
     };
 
-    acc_t acc[2][2];
+    acc_t acc[SA][SB];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < SA; ++a)
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
+        for (int s = 0; s < SB; ++s)
             acc[a][s] = acc_t{};
 
-    // One K chunk: KSC k-steps, each reading two A- and two B-fragments (a
-    // ring of LOOK + 1 steps, LOOK steps ahead) and issuing four MFMAs.
+    // One K chunk: KSC k-steps, each reading SA A- and SB B-fragments (a ring
+    // of LOOK + 1 steps, LOOK steps ahead) and issuing SA * SB MFMAs.
     constexpr int LOOK = 2, RING = LOOK + 1;
     auto chunk = [&](uint32_t kc, const uint8_t *cur, uint8_t *nxt)
                      __attribute__((always_inline)) {
         if (kc + 1 < n_chunks)
             stage_issue(kc + 1, nxt);
         const uint8_t *pa = cur + (64 * wr + c32) * LS + 16 * half;
-        const uint8_t *pb = cur + (ST_BM + 64 * wc + c32) * LS + 16 * half;
-        i32x4 ring[RING][4];
-        auto fetch = [&](i32x4(&f)[4], int ks) __attribute__((always_inline)) {
-            f[0] = *(const i32x4 *)(pa + 32 * ks);
-            f[1] = *(const i32x4 *)(pa + 32 * LS + 32 * ks);
-            f[2] = *(const i32x4 *)(pb + 32 * ks);
-            f[3] = *(const i32x4 *)(pb + 32 * LS + 32 * ks);
+        const uint8_t *pb = cur + (ST_BM + 128 * wc + c32) * LS + 16 * half;
+        i32x4 ring[RING][SA + SB];
+        auto fetch = [&](i32x4(&f)[SA + SB], int ks) __attribute__((always_inline)) {
+#pragma unroll
+            for (int a = 0; a < SA; ++a)
+                f[a] = *(const i32x4 *)(pa + 32 * a * LS + 32 * ks);
+#pragma unroll
+            for (int b = 0; b < SB; ++b)
+                f[SA + b] = *(const i32x4 *)(pb + 32 * b * LS + 32 * ks);
         };
         static_for<0, LOOK>([&](auto Q) __attribute__((always_inline)) {
             fetch(ring[decltype(Q)::value], decltype(Q)::value);
@@ -808,12 +813,12 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
             constexpr int ks = decltype(K)::value;
             if constexpr (ks + LOOK < KSC)
                 fetch(ring[(ks + LOOK) % RING], ks + LOOK);
-            const i32x4(&f)[4] = ring[ks % RING];
+            const i32x4(&f)[SA + SB] = ring[ks % RING];
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < SA; ++a)
 #pragma unroll
-                for (int s = 0; s < 2; ++s)
-                    acc[a][s] = M::mma(f[a], f[2 + s], acc[a][s]);
+                for (int b = 0; b < SB; ++b)
+                    acc[a][b] = M::mma(f[a], f[SA + b], acc[a][b]);
             __builtin_amdgcn_sched_barrier(0);
         });
         __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of chunk kc + 1 landed
@@ -834,35 +839,38 @@ __global__ void __launch_bounds__(256) join_streamed(JoinArgs g)
     V nmin = big_val<V>();
     const V *nrows = nullptr;
     if constexpr (NEED_NORMS) {
-        nmin = stage_row_norms<DT, 2>(prow0, lane, s_np[wave], g);
+        nmin = stage_row_norms<DT, SA>(prow0, lane, s_np[wave], g);
         nrows = &s_np[wave][4 * half];
     }
     const V nb = bound_base<DT, MET>(nmin, g);
     // After the last chunk's barrier the operand stages are free: each wave
-    // stages its matches in a quarter of them (2304 pairs), for the single
+    // stages its matches in an eighth of them (2304 pairs), for the single
     // pass and the emit pass alike.
-    constexpr uint32_t STAGE_BYTES = ROWS * LS / 2;
+    constexpr uint32_t STAGE_BYTES = 2 * ROWS * LS / ST_NW;
     static_assert(STAGE_BYTES / 8 >= 1024, "a whole 32x32 block must fit the staging buffer");
-    uint8_t *stage_mem = (wave < 2 ? s_op0 : s_op1) + (wave & 1) * STAGE_BYTES;
+    uint8_t *stage_mem = (wave < ST_NW / 2 ? s_op0 : s_op1) + (wave % (ST_NW / 2)) * STAGE_BYTES;
     WaveOut wo{(lds_pair *)stage_mem, STAGE_BYTES / 8, 0u, 0ull};
-    const uint64_t blk = (uint64_t)(pt * n_qt + qt) * 4 + wave;
+    const uint64_t blk = (uint64_t)(pt * n_qt + qt) * ST_NW + wave;
     uint64_t blk_run = 0;
     if constexpr (MODE == MODE_EMIT)
         wo.dst = g.block_offsets[blk];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const uint32_t j = q0 + 64 * wc + 32 * s + c32;
+    for (int b = 0; b < SB; ++b) {
+        const uint32_t j = q0 + 128 * wc + 32 * b + c32;
         V ny = V(0);
         if constexpr (NEED_NORMS)
             ny = j < g.n_q ? ((const V *)g.norm_q)[j] : big_val<V>();
-        const acc_t blk_acc[2] = {acc[0][s], acc[1][s]};
-        const bool may = lane_may_match<DT, MET, 2>(blk_acc, nb, ny, g);
+        acc_t blk_acc[SA];
+#pragma unroll
+        for (int a = 0; a < SA; ++a)
+            blk_acc[a] = acc[a][b];
+        const bool may = lane_may_match<DT, MET, SA>(blk_acc, nb, ny, g);
         if (__ballot(may) != 0)
-            exact_blocks<DT, MET, MODE, 2>(blk_acc, ibase, j, lane, nb, ny, nrows, g, blk_run,
-                                           wo);
+            exact_blocks<DT, MET, MODE, SA>(blk_acc, ibase, j, lane, nb, ny, nrows, g, blk_run,
+                                            wo);
     }
     if constexpr (MODE == MODE_SINGLE)
-        flush_workgroup_out<4>(wo, wave, lane, g);
+        flush_workgroup_out<ST_NW>(wo, wave, lane, g);
     if constexpr (MODE == MODE_EMIT)
         flush_wave_out<MODE>(wo, lane, g);
     if constexpr (MODE == MODE_COUNT) {
@@ -924,7 +932,8 @@ template <int DT, int MET, int MODE>
 hipError_t launch_mode(const Plan &p, const JoinArgs &g, hipStream_t st)
 {
     if (p.family == FAM_STREAMED) {
-        hipLaunchKernelGGL((join_streamed<DT, MET, MODE>), dim3(p.grid), dim3(256), 0, st, g);
+        hipLaunchKernelGGL((join_streamed<DT, MET, MODE>), dim3(p.grid), dim3(ST_NW * 64), 0, st,
+                           g);
         return hipGetLastError();
     }
     switch (p.variant) {
