@@ -331,13 +331,36 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
     }
     if (tot == 0)
         return;
+    // Sparse blocks: register by register, only registers with matches.
+    // Dense blocks (more than two matches per register on average): lane by
+    // lane, each lane writing its own matches at its exclusive prefix of the
+    // per-lane counts.  Either order is a fixed function of the data.
     auto store_all = [&](auto &&dst, uint64_t base) {
+        if (tot <= 32) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            if (mk[r] != 0) {                      // uniform
-                if ((mk[r] >> lane) & 1)
-                    dst(base + lanes_below(mk[r]), pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
-                base += (uint64_t)__popcll(mk[r]);
+            for (int r = 0; r < 16; ++r) {
+                if (mk[r] != 0) {                      // uniform
+                    if ((mk[r] >> lane) & 1)
+                        dst(base + lanes_below(mk[r]),
+                            pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
+                    base += (uint64_t)__popcll(mk[r]);
+                }
+            }
+        } else {
+            uint32_t m = 0;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                m |= ((mk[r] >> lane) & 1) ? (1u << r) : 0u;
+            const uint32_t cnt = (uint32_t)__builtin_popcount(m);
+            uint32_t pre = 0;                          // exclusive prefix over lanes
+#pragma unroll
+            for (int b = 0; b < 5; ++b)
+                pre += lanes_below(__ballot((cnt >> b) & 1)) << b;
+            uint64_t pos = base + pre;
+            while (m != 0) {
+                const int r = __builtin_ctz(m);
+                m &= m - 1;
+                dst(pos++, pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
             }
         }
     };

@@ -170,6 +170,27 @@ def test_extreme_thresholds(dtype):
         assert sj.count(Pd, Qd, huge, metric) == 130 * 70
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 600), ("f16", 1024), ("i8", 700)])
+def test_streamed_dense_output(dtype, d):
+    """The K-streamed kernel with every pair matching (each wave's staging
+    buffer fills several times per output block) and with about half the pairs
+    matching, in both modes, against the oracle."""
+    import paper_2006_12608_amd as sj
+    w = workloads.random_case(21, 300, 517, d, dtype, lo=-2, hi=2)
+    Pd, Qd = to_device(w.P, dtype), to_device(w.Q, dtype)
+    say("streamed dense", dtype, d)
+    for two_pass in (False, True):
+        allp = sorted_pairs(sj.join_ip(Pd, Qd, -np.inf, two_pass=two_pass))
+        assert allp.shape[0] == 300 * 517
+        assert np.array_equal(allp[:, 0], np.repeat(np.arange(300), 517))
+        assert np.array_equal(allp[:, 1], np.tile(np.arange(517), 300))
+    x = values(dtype, w.P).astype(np.int64)
+    y = values(dtype, w.Q).astype(np.int64)
+    w.threshold = float(np.quantile(x @ y.T, 0.5, method="nearest"))
+    for two_pass in (False, True):
+        run_case(w, two_pass=two_pass)
+
+
 def test_ties_are_inclusive():
     """Rows with known exact scores at the threshold are reported; one above is not."""
     rng = np.random.default_rng(5)
