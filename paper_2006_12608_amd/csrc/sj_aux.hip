@@ -12,20 +12,19 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 // ------------------------------------------------------------------ planning
 // Resident-P limits: 32-byte k-steps of the largest variant (16 for 2-byte
-// elements, 8 for int8, i.e. d <= 256 either way); workgroup of 4 waves over
+// elements, 8 for int8, i.e. d <= 256 either way); workgroup of 8 waves over
 // 32 * WMB rows each (WMB = 4 for int8 rows of at most 64 bytes, else 2); Q
 // tiles of 256 rows for rows of at most 64 bytes, 128 up to 256 bytes and 64
 // for the longest rows.  Must agree with sj_join_kernels.h.
 static const int kResKS16[4] = {2, 4, 8, 16};
 static const int kResKS8[4] = {1, 2, 4, 8};
-static const uint32_t kResNW = 4;
+static const uint32_t kResNW = 8;
 static uint32_t res_bn(int ks) { return ks <= 2 ? 256 : ks <= 8 ? 128 : 64; }
 static const uint32_t kStBM = 256, kStBN = 256, kStG = 8, kStNW = 8;
 
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
                Plan *plan)
 {
-    (void)metric;
     const uint32_t ks_needed = row_bytes == 0 ? 1u : (row_bytes + 31) / 32;
     const int *tab = dtype == DT_I8 ? kResKS8 : kResKS16;
     int variant = -1;
@@ -41,11 +40,17 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
         const uint64_t n_pb = (n_p + (uint64_t)bm - 1) / bm;
         const uint64_t bn = res_bn(ks);
         const uint64_t n_qt = (n_q + bn - 1) / bn;
-        // Enough workgroups for two per CU; splits of Q are powers of two so
-        // that, with workgroups dealt round-robin to the 8 XCDs, each XCD's
-        // workgroups sweep the same Q range (shared in that XCD's L2).
+        // Enough workgroups to fill every CU twice (with exactly one round,
+        // one late workgroup start stretches the whole kernel); splits of Q
+        // are powers of two so that, with workgroups dealt round-robin to the
+        // 8 XCDs, each XCD's workgroups sweep the same Q range (shared in that
+        // XCD's L2).
+        const int occ = dtype == DT_I8    ? resident_occupancy_i8(metric, variant)
+                        : dtype == DT_F16 ? resident_occupancy_f16(metric, variant)
+                                          : resident_occupancy_bf16(metric, variant);
         uint64_t qsplit = 1;
-        while (n_pb * qsplit < 2ull * (uint64_t)num_cus && qsplit * 2 <= n_qt && qsplit < 64)
+        while (n_pb * qsplit < 2ull * (uint64_t)occ * (uint64_t)num_cus && qsplit * 2 <= n_qt &&
+               qsplit < 64)
             qsplit *= 2;
         plan->family = FAM_RESIDENT;
         plan->variant = variant;

@@ -79,5 +79,9 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
 hipError_t launch_join_f16(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
 hipError_t launch_join_bf16(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
 hipError_t launch_join_i8(const Plan &, int metric, int mode, const JoinArgs &, hipStream_t);
+// Workgroups of a resident-kernel variant that one CU holds at once.
+int resident_occupancy_f16(int metric, int variant);
+int resident_occupancy_bf16(int metric, int variant);
+int resident_occupancy_i8(int metric, int variant);
 
 }  // namespace sjk

@@ -10,4 +10,9 @@ hipError_t launch_join_bf16(const Plan &p, int metric, int mode, const JoinArgs 
     return launch_dtype<DT_BF16>(p, metric, mode, g, st);
 }
 
+int resident_occupancy_bf16(int metric, int variant)
+{
+    return resident_occupancy_dtype<DT_BF16>(metric, variant);
+}
+
 }  // namespace sjk

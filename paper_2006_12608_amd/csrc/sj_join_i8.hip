@@ -10,4 +10,9 @@ hipError_t launch_join_i8(const Plan &p, int metric, int mode, const JoinArgs &g
     return launch_dtype<DT_I8>(p, metric, mode, g, st);
 }
 
+int resident_occupancy_i8(int metric, int variant)
+{
+    return resident_occupancy_dtype<DT_I8>(metric, variant);
+}
+
 }  // namespace sjk

@@ -920,7 +920,9 @@ struct ResidentCfg<DT_I8> {
     static constexpr int KS[4] = {1, 2, 4, 8};
 };
 
-constexpr int RES_NW = 4;
+// Eight waves (two per SIMD) per workgroup: one tile load from L2 feeds 256
+// or 512 rows of P, and each Q tile is staged once per CU.
+constexpr int RES_NW = 8;
 // 32-row A-blocks per wave: two, which with the two accumulator sets of the
 // sub-tile pipeline keeps every variant within 256 VGPRs; four for int8 rows
 // of at most 64 bytes, whose A-fragments are small (each B-fragment read from
@@ -949,6 +951,38 @@ hipError_t launch_resident_v(const Plan &p, const JoinArgs &g, hipStream_t st)
     hipLaunchKernelGGL((join_resident<DT, MET, MODE, KS, WMB, RES_NW, BN>), dim3(p.grid),
                        dim3(RES_NW * 64), 0, st, g);
     return hipGetLastError();
+}
+
+// Workgroups of a resident variant that fit on one CU (registers and LDS).
+template <int DT, int MET, int V>
+int resident_occupancy_v()
+{
+    constexpr int KS = ResidentCfg<DT>::KS[V];
+    constexpr int WMB = res_wmb<DT, KS>();
+    constexpr int BN = res_bn<KS>();
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, reinterpret_cast<const void *>(&join_resident<DT, MET, MODE_SINGLE, KS, WMB, RES_NW, BN>),
+            RES_NW * 64, 0) != hipSuccess)
+        n = 1;
+    return n < 1 ? 1 : n;
+}
+
+template <int DT>
+int resident_occupancy_dtype(int metric, int variant)
+{
+    static int cache[2][4];   // written with the same value by any racing caller
+    int &c = cache[metric == MET_L2][variant & 3];
+    if (c == 0) {
+        const bool l2 = metric == MET_L2;
+        switch (variant) {
+        case 0: c = l2 ? resident_occupancy_v<DT, MET_L2, 0>() : resident_occupancy_v<DT, MET_IP, 0>(); break;
+        case 1: c = l2 ? resident_occupancy_v<DT, MET_L2, 1>() : resident_occupancy_v<DT, MET_IP, 1>(); break;
+        case 2: c = l2 ? resident_occupancy_v<DT, MET_L2, 2>() : resident_occupancy_v<DT, MET_IP, 2>(); break;
+        default: c = l2 ? resident_occupancy_v<DT, MET_L2, 3>() : resident_occupancy_v<DT, MET_IP, 3>(); break;
+        }
+    }
+    return c;
 }
 
 template <int DT, int MET, int MODE>
