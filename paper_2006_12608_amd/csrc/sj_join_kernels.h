@@ -458,13 +458,13 @@ __device__ __forceinline__ void static_for(F &&f)
 // A workgroup of NW waves owns BM = NW * 32 * WMB consecutive rows of P; each
 // wave keeps its 32*WMB rows, all KS k-steps, as MFMA A-fragments in VGPRs for
 // the whole kernel.  The workgroup sweeps its range of Q in tiles of BN rows,
-// double-buffered in LDS (rows padded by one chunk); the next tile's
-// direct global-to-LDS loads are issued before the current tile's MFMAs.  Inside a tile the 32-row
-// sub-tiles are software-pipelined: the MFMAs of sub-tile s are issued in the
-// same instruction block as the epilogue bound of sub-tile s - 1 (two
-// accumulator sets), so the VALU work of the epilogue overlaps the matrix
-// cores.  Output block (count/emit passes) = one wave's rows x one Q tile;
-// block index = (global wave row-block) * n_qtiles + tile.
+// double-buffered in LDS (rows padded by one chunk); the next tile's direct
+// global-to-LDS loads are issued before the current tile's MFMAs.  A tile is
+// one stream of k-steps over its 32-row sub-tiles (see the tile loop): the
+// B-fragment reads run a few steps ahead of the MFMAs, and with two
+// accumulator sets the epilogue bound of sub-tile s - 1 is folded in while
+// the MFMAs of sub-tile s run.  Output block (count/emit passes) = one wave's
+// rows x one Q tile; block index = (global wave row-block) * n_qtiles + tile.
 template <int DT, int MET, int MODE, int KS, int WMB, int NW, int BN>
 __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
 {
