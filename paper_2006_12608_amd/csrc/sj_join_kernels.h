@@ -283,13 +283,16 @@ __device__ __forceinline__ void flush_workgroup_out(WaveOut &wo, int wave, int l
 }
 
 // exact_block: every result of one 32x32 block (accumulator `acc`, rows
-// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly; the ballot
-// of result r is the wave's match mask for that register, and only registers
-// with a nonzero mask are stored.  MODE_SINGLE appends the matches to the
-// wave's LDS staging buffer, MODE_EMIT writes them at the output block's
-// running offset, MODE_COUNT only counts.  Each store instruction fills
-// consecutive slots.  L2 row norms come from `nrow` (LDS: this lane's rows of
-// the block).
+// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly into a
+// per-lane 16-bit match mask; per-lane counts give the wave's total and each
+// lane's exclusive prefix (five ballots over the count's bits), and every lane
+// writes its own matches at its prefix, in register order.  MODE_SINGLE
+// appends to the wave's LDS staging buffer (which holds a whole block),
+// MODE_EMIT writes at the output block's running offset (or stages, when the
+// kernel provides a staging buffer), MODE_COUNT only counts.  The code is
+// kept short on purpose: it is inlined at every sub-tile and runs rarely, and
+// a long exact path costs instruction-cache misses when it does run.  L2 row
+// norms come from `nrow` (LDS: this lane's rows of the block).
 template <int DT, int MET, int MODE>
 __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, uint32_t ib,
                                             uint32_t j, int lane, typename Mma<DT>::val_t ny,
@@ -300,99 +303,66 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
     // Opaque to the optimiser: keeps the per-result row indices from being
     // hoisted into (and occupying registers of) the caller's main loop.
     asm volatile("" : "+v"(ib));
-    auto score_ok = [&](int r) -> bool {
+    uint32_t m = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        bool ok;
         if constexpr (MET == MET_L2)
-            return pair_matches<DT, MET>(acc[r], nrow[8 * (r >> 2) + (r & 3)], ny, g);
+            ok = pair_matches<DT, MET>(acc[r], nrow[8 * (r >> 2) + (r & 3)], ny, g);
         else
-            return pair_matches<DT, MET>(acc[r], V(0), V(0), g);
-    };
-    uint64_t mk[16];
-    // lane 0 holds the block's first row and column
+            ok = pair_matches<DT, MET>(acc[r], V(0), V(0), g);
+        m |= ok ? (1u << r) : 0u;
+    }
+    // rows past n_p and columns past n_q (lane 0 holds the block's first row
+    // and column; the test is uniform)
     const uint32_t ib0 = __builtin_amdgcn_readfirstlane(ib);
     const uint32_t j0 = __builtin_amdgcn_readfirstlane(j);
-    if ((uint64_t)ib0 + 32 <= g.n_p && (uint64_t)j0 + 32 <= g.n_q) {
-        // the whole block lies inside P x Q (uniform)
+    if ((uint64_t)ib0 + 32 > g.n_p || (uint64_t)j0 + 32 > g.n_q) {
+        uint32_t valid = 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-            mk[r] = __ballot(score_ok(r));
-    } else {
-        const bool jok = j < g.n_q;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            mk[r] = __ballot(jok && ib + 8 * (r >> 2) + (r & 3) < g.n_p && score_ok(r));
+            valid |= ib + 8 * (r >> 2) + (r & 3) < g.n_p ? (1u << r) : 0u;
+        m &= j < g.n_q ? valid : 0u;
     }
-    uint32_t tot = 0;
+    const uint32_t cnt = (uint32_t)__builtin_popcount(m);
+    uint32_t tot = 0, pre = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-        tot += (uint32_t)__popcll(mk[r]);
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t bits = __ballot((cnt >> b) & 1);
+        tot += (uint32_t)__popcll(bits) << b;
+        pre += lanes_below(bits) << b;
+    }
     if constexpr (MODE == MODE_COUNT) {
         blk_run += tot;
         return;
     }
     if (tot == 0)
         return;
-    // Sparse blocks: register by register, only registers with matches.
-    // Dense blocks (more than two matches per register on average): lane by
-    // lane, each lane writing its own matches at its exclusive prefix of the
-    // per-lane counts.  Either order is a fixed function of the data.
-    auto store_all = [&](auto &&dst, uint64_t base) {
-        if (tot <= 32) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                if (mk[r] != 0) {                      // uniform
-                    if ((mk[r] >> lane) & 1)
-                        dst(base + lanes_below(mk[r]),
-                            pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
-                    base += (uint64_t)__popcll(mk[r]);
-                }
-            }
-        } else {
-            uint32_t m = 0;
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                m |= ((mk[r] >> lane) & 1) ? (1u << r) : 0u;
-            const uint32_t cnt = (uint32_t)__builtin_popcount(m);
-            uint32_t pre = 0;                          // exclusive prefix over lanes
-#pragma unroll
-            for (int b = 0; b < 5; ++b)
-                pre += lanes_below(__ballot((cnt >> b) & 1)) << b;
-            uint64_t pos = base + pre;
-            while (m != 0) {
-                const int r = __builtin_ctz(m);
-                m &= m - 1;
-                dst(pos++, pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
-            }
+    auto write_all = [&](auto &&dst, uint64_t base) {
+        uint64_t pos = base + pre;
+        while (m != 0) {
+            const int r = __builtin_ctz(m);
+            m &= m - 1;
+            dst(pos++, pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
         }
     };
-    // staged (single pass; emit pass when the kernel gives a staging buffer)
     if (MODE == MODE_SINGLE || wo.cap > 1) {
+        // staged: the buffer holds at least one whole block
         if (wo.fill + tot > wo.cap)
             flush_wave_out<MODE>(wo, lane, g);
-        if (tot <= wo.cap) {
-            const uint32_t base = wo.fill;
-            wo.fill += tot;
-            store_all([&](uint64_t k, uint64_t v) { wo.buf[k] = v; }, base);
-            return;
-        }
-    }
-    // Emit pass (block offset) or a block with more matches than the staging
-    // buffer holds (one atomic reserves its slots).
-    uint64_t base;
-    if constexpr (MODE == MODE_SINGLE) {
-        unsigned long long b = 0;
-        if (lane == 0)
-            b = atomicAdd(g.counter, (unsigned long long)tot);
-        base = first_lane_u64(b);
+        const uint32_t base = wo.fill;
+        wo.fill += tot;
+        write_all([&](uint64_t k, uint64_t v) { wo.buf[k] = v; }, base);
     } else {
-        base = blk_run;
+        const uint64_t base = blk_run;
         blk_run += tot;
+        write_all(
+            [&](uint64_t slot, uint64_t v) {
+                if (slot < g.cap)
+                    *pair_slot(g, slot) = v;
+            },
+            base);
     }
-    store_all(
-        [&](uint64_t slot, uint64_t v) {
-            if (slot < g.cap)
-                *pair_slot(g, slot) = v;
-        },
-        base);
 }
 
 // All WMB blocks of a wave's sub-tile that hold a possible match.
@@ -490,7 +460,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __shared__ V s_nq0[NEED_NORMS ? BN : 1];
     __shared__ V s_nq1[NEED_NORMS ? BN : 1];
     __shared__ V s_np[NEED_NORMS ? NW : 1][NEED_NORMS ? 32 * WMB : 1];
-    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 256 : 1;
+    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 1024 : 1;   // a whole 32x32 block
     __shared__ uint64_t s_out[NW][OUT_CAP];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
