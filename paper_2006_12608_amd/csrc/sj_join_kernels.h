@@ -199,6 +199,42 @@ __device__ __forceinline__ void fold_max(const ACC (&acc)[WMB], V &m)
     }
 }
 
+// Running maxima over the results v = 16 a + r, v in [LO, HI), of acc[WMB].
+// With at most two blocks one chain per block (mb[a], so the exact path can
+// skip a block whose own bound fails); with more, one chain in mb[0] (fewer
+// VALU instructions; the exact path then re-derives the block bounds).
+template <int WMB>
+constexpr bool per_block_max()
+{
+    return WMB <= 2;
+}
+
+template <int LO, int HI, int WMB, typename ACC, typename V>
+__device__ __forceinline__ void fold_max_blk(const ACC (&acc)[WMB], V (&mb)[WMB])
+{
+    if constexpr (LO < HI) {
+        constexpr int c = per_block_max<WMB>() ? LO / 16 : 0;
+        constexpr bool first = per_block_max<WMB>() ? LO % 16 == 0 : LO == 0;
+        if constexpr (first)
+            mb[c] = acc[LO / 16][LO % 16];
+        else
+            mb[c] = vmax(mb[c], acc[LO / 16][LO % 16]);
+        fold_max_blk<LO + 1, HI, WMB>(acc, mb);
+    }
+}
+
+template <int WMB, typename V>
+__device__ __forceinline__ V max_of(const V (&mb)[WMB])
+{
+    V m = mb[0];
+    if constexpr (per_block_max<WMB>()) {
+#pragma unroll
+        for (int a = 1; a < WMB; ++a)
+            m = vmax(m, mb[a]);
+    }
+    return m;
+}
+
 template <int DT, int MET, int WMB>
 __device__ __forceinline__ bool lane_may_match(const typename Mma<DT>::acc_t (&acc)[WMB],
                                                typename Mma<DT>::val_t nb,
@@ -365,9 +401,10 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
     }
 }
 
-// All WMB blocks of a wave's sub-tile that hold a possible match.
+// All WMB blocks of a wave's sub-tile whose own bound holds for some lane.
 template <int DT, int MET, int MODE, int WMB>
 __device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc)[WMB],
+                                             const typename Mma<DT>::val_t (&mb)[WMB],
                                              uint32_t ibase, uint32_t j, int lane,
                                              typename Mma<DT>::val_t nb,
                                              typename Mma<DT>::val_t ny,
@@ -376,9 +413,14 @@ __device__ __forceinline__ void exact_blocks(const typename Mma<DT>::acc_t (&acc
 {
 #pragma unroll
     for (int a = 0; a < WMB; ++a) {
-        typename Mma<DT>::acc_t one[1] = {acc[a]};
-        // L2: the block's own bound first (the exact test reads row norms)
-        if (MET == MET_IP || __ballot(lane_may_match<DT, MET, 1>(one, nb, ny, g)) != 0)
+        bool may;
+        if constexpr (per_block_max<WMB>()) {
+            may = lane_bound<DT, MET>(mb[a], nb, ny, g);
+        } else {
+            typename Mma<DT>::acc_t one[1] = {acc[a]};
+            may = lane_may_match<DT, MET, 1>(one, nb, ny, g);
+        }
+        if (__ballot(may) != 0)
             exact_block<DT, MET, MODE>(acc[a], ibase + 32 * a, j, lane, ny, nrows + 32 * a, g,
                                        blk_run, wo);
     }
@@ -550,11 +592,11 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
     // Bound of one wave sub-tile from its running max, then the exact path if
     // any lane may match.
-    auto check = [&](const acc_t(&a)[WMB], V m, uint32_t jp, V nyp, uint64_t &run)
-                     __attribute__((always_inline)) {
-        const bool may = lane_bound<DT, MET>(m, nb, nyp, g);
+    auto check = [&](const acc_t(&a)[WMB], const V(&mb)[WMB], uint32_t jp, V nyp,
+                     uint64_t &run) __attribute__((always_inline)) {
+        const bool may = lane_bound<DT, MET>(max_of<WMB>(mb), nb, nyp, g);
         if (__builtin_expect(__ballot(may) != 0, 0))
-            exact_blocks<DT, MET, MODE, WMB>(a, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
+            exact_blocks<DT, MET, MODE, WMB>(a, mb, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
     };
 
     // A tile is a stream of SUBS * KS k-steps (sub-tile s = step / KS).  Each
@@ -610,7 +652,10 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
             ny_sub[s] = V(0);
             if constexpr (NEED_NORMS)
                 ny_sub[s] = ncur[32 * s + c32];
-            V m = V(0);
+            V mb[WMB];
+#pragma unroll
+            for (int a = 0; a < WMB; ++a)
+                mb[a] = V(0);
             static_for<0, KS>([&](auto K) __attribute__((always_inline)) {
                 constexpr int ks = decltype(K)::value, q = s * KS + ks;
                 if constexpr (q + LOOK < NSTEP) {
@@ -622,24 +667,24 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
                 for (int a = 0; a < WMB; ++a)
                     acc[ci][a] = M::mma(A[a][ks], ring[q % RING], ks == 0 ? acc_t{} : acc[ci][a]);
                 if constexpr (PIPE)
-                    fold_max<ks * NVAL / KS, (ks + 1) * NVAL / KS, WMB>(acc[pi], m);
+                    fold_max_blk<ks * NVAL / KS, (ks + 1) * NVAL / KS, WMB>(acc[pi], mb);
                 __builtin_amdgcn_sched_barrier(0);
             });
             if constexpr (PIPE) {
                 if constexpr (s == 0) {
                     if (have_prev) {
-                        check(acc[pi], m, j_prev, ny_prev, run_prev);
+                        check(acc[pi], mb, j_prev, ny_prev, run_prev);
                         if constexpr (MODE == MODE_COUNT) {
                             if (lane == 0)
                                 g.block_counts[blk_prev] = (uint32_t)run_prev;
                         }
                     }
                 } else {
-                    check(acc[pi], m, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
+                    check(acc[pi], mb, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
                 }
             } else {
-                fold_max<0, NVAL, WMB>(acc[0], m);
-                check(acc[0], m, t * BN + 32 * s + c32, ny_sub[s], blk_run);
+                fold_max_blk<0, NVAL, WMB>(acc[0], mb);
+                check(acc[0], mb, t * BN + 32 * s + c32, ny_sub[s], blk_run);
             }
         });
         if constexpr (PIPE) {
@@ -664,9 +709,9 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     }
     if constexpr (PIPE) {
         if (have_prev) {
-            V m;
-            fold_max<0, NVAL, WMB>(acc[NACC - 1], m);
-            check(acc[NACC - 1], m, j_prev, ny_prev, run_prev);
+            V mb[WMB];
+            fold_max_blk<0, NVAL, WMB>(acc[NACC - 1], mb);
+            check(acc[NACC - 1], mb, j_prev, ny_prev, run_prev);
             if constexpr (MODE == MODE_COUNT) {
                 if (lane == 0)
                     g.block_counts[blk_prev] = (uint32_t)run_prev;
@@ -857,10 +902,12 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
 #pragma unroll
         for (int a = 0; a < SA; ++a)
             blk_acc[a] = acc[a][b];
-        const bool may = lane_may_match<DT, MET, SA>(blk_acc, nb, ny, g);
+        V mb[SA];
+        fold_max_blk<0, 16 * SA, SA>(blk_acc, mb);
+        const bool may = lane_bound<DT, MET>(max_of<SA>(mb), nb, ny, g);
         if (__ballot(may) != 0)
-            exact_blocks<DT, MET, MODE, SA>(blk_acc, ibase, j, lane, nb, ny, nrows, g, blk_run,
-                                            wo);
+            exact_blocks<DT, MET, MODE, SA>(blk_acc, mb, ibase, j, lane, nb, ny, nrows, g,
+                                            blk_run, wo);
     }
     if constexpr (MODE == MODE_SINGLE)
         flush_workgroup_out<ST_NW>(wo, wave, lane, g);
