@@ -489,9 +489,9 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     constexpr int SUBS = BN / 32;
     constexpr int BM = NW * 32 * WMB;
     constexpr bool NEED_NORMS = (MET == MET_L2);
-    // Sub-tile pipeline (two accumulator sets) for rows of up to 8 k-steps; at
-    // 16 k-steps the register file holds only one set at two waves per SIMD.
-    constexpr bool PIPE = KS <= 8;
+    // Sub-tile pipeline (two accumulator sets); at 16 k-steps only the inner
+    // product fits a second set in 256 VGPRs (the L2 epilogue needs more).
+    constexpr bool PIPE = KS <= 8 || MET == MET_IP;
 
     // Two distinct LDS buffers (not one array indexed at run time): the tile
     // loop is unrolled by two so every access names its buffer statically, which
