@@ -89,6 +89,43 @@ def traffic_for(workload: str, launches_bytes_alg: float):
     return rec.get("hbm_bytes_per_launch")
 
 
+def measured_mfma_peak(dtype: str, duration_ms: float, operands=None):
+    """The MFMA-only throughput of this GPU (libsj_peak.so: four accumulator
+    chains per wave, two waves per SIMD) over a run as long as the timed
+    region, with MFMA operands taken from `operands` (a device tensor, e.g. the
+    workload's rows; random values if None), or None when the probe library
+    is not built."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2006_12608_amd", "libsj_peak.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    lib.sj_peak_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_void_p,
+                                 ctypes.c_uint64, ctypes.POINTER(ctypes.c_double),
+                                 ctypes.POINTER(ctypes.c_double)]
+    lib.sj_peak_mfma.restype = ctypes.c_int
+    tops, ms = ctypes.c_double(), ctypes.c_double()
+    code = {"f16": 1, "bf16": 2, "i8": 3}[dtype]
+    ptr = operands.data_ptr() if operands is not None else None
+    nbytes = operands.numel() * operands.element_size() if operands is not None else 0
+    if lib.sj_peak_mfma(code, 2, max(duration_ms, 1.0), ptr, nbytes, ctypes.byref(tops),
+                        ctypes.byref(ms)) != 0:
+        return None
+    return {"value": tops.value, "unit": "TOP/s" if dtype == "i8" else "TFLOP/s",
+            "run_ms": ms.value,
+            "operands": "the workload's P rows" if operands is not None else "random"}
+
+
+def cpu_model() -> str:
+    try:
+        for l in open("/proc/cpuinfo"):
+            if l.startswith("model name"):
+                return l.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, target_s: float = 12.0):
     import numpy as np
     import oracle
@@ -107,6 +144,7 @@ def cpu_baseline(w, target_s: float = 12.0):
     el = time.perf_counter() - t
     return {"value": n_rows * w.n_q / el, "unit": "pair-evaluations/s", "cores": threads,
             "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{n_rows} random rows of P against all {w.n_q} rows of Q "
                       f"({n_rows * w.n_q:.3g} pair evaluations, {el:.1f} s, {r.total} matches)"}
 
@@ -238,6 +276,14 @@ def main():
     }
     if two_pass:
         line["emit_hbm_gbps_algorithmic"] = n_out * 8 / (float(np.mean(emit_ms)) / 1e3) / 1e9
+    # the same fraction against what the matrix cores alone sustain on this GPU
+    # over a run as long as the timed region, on this workload's data (the
+    # clock under load is below the spec peak's 2.4 GHz and depends on the
+    # operands' bit patterns)
+    meas = measured_mfma_peak(w.dtype, el * 1e3, Pd)
+    if meas is not None:
+        meas["frac"] = achieved / meas["value"]
+        line["roofline"]["mfma_only_measured"] = meas
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w)

@@ -20,6 +20,8 @@ BUILD_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["sj_api.cpp", "sj_aux.hip", "sj_join_f16.hip", "sj_join_bf16.hip", "sj_join_i8.hip"]
+PEAK_SOURCE = os.path.join("peak", "mfma_peak.hip")
+PEAK_OUT = os.path.join(HERE, "libsj_peak.so")
 # Packed-fp32 instructions are kept out of the generated code (they are not
 # needed here and some of their forms are unreliable on this hardware).
 # MFMA results stay in arch VGPRs so the fused epilogue reads them directly.
@@ -30,7 +32,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-u
 
 
 def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+    obj = os.path.join(BUILD_DIR, os.path.splitext(os.path.basename(src))[0] + ".o")
     cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd.insert(1, "-xhip")
@@ -40,19 +42,26 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libsj.so; returns its path."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = OUT + ".tmp%d" % os.getpid()
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp%d" % os.getpid()
     r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs],
                        capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"linking libsj.so failed:\n{r.stderr}")
-    os.replace(tmp, OUT)
+        raise RuntimeError(f"linking {os.path.basename(out)} failed:\n{r.stderr}")
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link libsj.so (the join) and libsj_peak.so (the
+    MFMA-only throughput probe bench.py reports beside the spec peak); returns
+    the path of libsj.so."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=min(len(SOURCES) + 1, os.cpu_count() or 4)) as ex:
+        objs = list(ex.map(_compile, SOURCES + [PEAK_SOURCE]))
+    _link(objs[:-1], OUT)
+    _link(objs[-1:], PEAK_OUT)
     if verbose:
-        print(f"built {OUT}")
+        print(f"built {OUT} and {PEAK_OUT}")
     return OUT
 
 
