@@ -223,6 +223,7 @@ def main():
         step()
     torch.cuda.synchronize()
     kern_ms, emit_ms, count_ms, scan_ms, norm_ms = [], [], [], [], []
+    from_bits = False
     t0 = time.perf_counter()
     n_out = 0
     for _ in range(args.steps):
@@ -233,6 +234,7 @@ def main():
         count_ms.append(s.ms_count)
         scan_ms.append(s.ms_scan)
         norm_ms.append(s.ms_norms)
+        from_bits = bool(s.emit_from_bits)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     ms_step = el / args.steps * 1e3
@@ -275,7 +277,13 @@ def main():
         "kernel_sha": kernel_source_hash(),
     }
     if two_pass:
-        line["emit_hbm_gbps_algorithmic"] = n_out * 8 / (float(np.mean(emit_ms)) / 1e3) / 1e9
+        # the second pass's algorithmic HBM bytes: 8 per pair written, plus the
+        # first pass's match bits read (one bit per result of every 256 x 256
+        # tile) when it reads them instead of recomputing the product
+        tiles = -(-w.n_p // 256) * -(-w.n_q // 256)
+        emit_bytes = n_out * 8 + (tiles * 256 * 256 // 8 if from_bits else 0)
+        line["emit"] = {"from_match_bits": from_bits, "hbm_bytes_algorithmic": emit_bytes,
+                        "hbm_gbps_algorithmic": emit_bytes / (float(np.mean(emit_ms)) / 1e3) / 1e9}
     # the same fraction against what the matrix cores alone sustain on this GPU
     # over a run as long as the timed region, on this workload's data (the
     # clock under load is below the spec peak's 2.4 GHz and depends on the

@@ -76,13 +76,21 @@ enum sj_status {
 enum sj_flags {
     /* Count-then-emit: a first pass counts the matches of every output block,
      * an exclusive scan turns the counts into offsets, and a second pass
-     * recomputes the product and writes each block's pairs at its offset.
-     * Costs a second product but never writes beyond `cap`, and the output
-     * order is deterministic (block-major).  Without the flag a single pass
-     * appends pairs through one atomic counter (order unspecified). */
+     * writes each block's pairs at its offset.  Never writes beyond `cap`,
+     * and the output order is deterministic (block-major).  The second pass
+     * recomputes the product, except with the K-streamed kernel (rows of more
+     * than 512 bytes), whose first pass also keeps one match bit per result
+     * in device scratch (n_p n_q / 8 bytes, rounded up to 256 x 256 tiles)
+     * when that fits, so that the second pass only reads the bits and writes
+     * the pairs.  Both second passes write the same array.  Without the flag
+     * a single pass appends pairs through one atomic counter (order
+     * unspecified). */
     SJ_FLAG_TWO_PASS = 1u,
     /* Record GPU timestamps around every phase of the call (see sj_stats). */
-    SJ_FLAG_TIMING = 2u
+    SJ_FLAG_TIMING = 2u,
+    /* With SJ_FLAG_TWO_PASS: always recompute the product in the second pass
+     * (no match bits, no scratch beyond the block counts and offsets). */
+    SJ_FLAG_RECOMPUTE = 4u
 };
 
 /* Diagnostics of the last sj_join_ip / sj_join_l2 / sj_count call. */
@@ -95,6 +103,8 @@ typedef struct sj_stats {
     double ms_emit;        /* two-pass: the emitting pass                      */
     uint32_t kernel;       /* 1 = P rows resident in registers, 2 = K-streamed */
     uint32_t timed;        /* 1 when the ms_* fields were measured             */
+    uint32_t emit_from_bits; /* two-pass: 1 when the second pass read the first
+                                pass's match bits instead of recomputing      */
 } sj_stats;
 
 /* Create a context on `device` (a gfx950 GPU), bound to `stream` (a

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libsj.so")
 SJ_F16, SJ_BF16, SJ_I8 = 1, 2, 3
 SJ_IP, SJ_L2 = 0, 1
 SJ_OK, SJ_E_INVAL, SJ_E_OVERFLOW, SJ_E_NOMEM, SJ_E_HIP, SJ_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING = 1, 2
+SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING, SJ_FLAG_RECOMPUTE = 1, 2, 4
 
 STATUS_NAMES = {0: "SJ_OK", -1: "SJ_E_INVAL", -2: "SJ_E_OVERFLOW", -3: "SJ_E_NOMEM",
                 -4: "SJ_E_HIP", -5: "SJ_E_UNSUPPORTED"}
@@ -36,7 +36,8 @@ class sj_stats(ctypes.Structure):
     _fields_ = [("total", ctypes.c_uint64), ("ms_norms", ctypes.c_double),
                 ("ms_join", ctypes.c_double), ("ms_count", ctypes.c_double),
                 ("ms_scan", ctypes.c_double), ("ms_emit", ctypes.c_double),
-                ("kernel", ctypes.c_uint32), ("timed", ctypes.c_uint32)]
+                ("kernel", ctypes.c_uint32), ("timed", ctypes.c_uint32),
+                ("emit_from_bits", ctypes.c_uint32)]
 
 
 def _load():
@@ -167,11 +168,12 @@ def count(P, Q, threshold: float, metric: str = "ip", ctx=None) -> int:
     return n
 
 
-def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out):
+def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
     import torch
     _check_pair(P, Q)
     ctx = ctx or context(P.device.index)
-    flags = (SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
+    flags = ((SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
+             | (SJ_FLAG_RECOMPUTE if recompute else 0))
     if cap is None and out is None:
         cap = count(P, Q, thr, metric, ctx)
     if out is None:
@@ -188,13 +190,15 @@ def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out):
 
 
 def join_ip(P, Q, s: float, cap: int | None = None, two_pass: bool = False, timing: bool = False,
-            ctx=None, out=None):
+            ctx=None, out=None, recompute: bool = False):
     """All (i, j) with <P_i, Q_j> >= s as an (n, 2) int32 tensor of uint32
-    indices.  With cap=None the exact size is counted first."""
-    return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out)
+    indices.  With cap=None the exact size is counted first.  two_pass selects
+    count-then-emit; recompute makes its second pass repeat the product even
+    where the first pass's match bits would be kept."""
+    return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out, recompute)
 
 
 def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool = False,
-            timing: bool = False, ctx=None, out=None):
+            timing: bool = False, ctx=None, out=None, recompute: bool = False):
     """All (i, j) with ||P_i - Q_j||^2 <= r2 (see join_ip)."""
-    return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out)
+    return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out, recompute)

@@ -156,8 +156,12 @@ struct Request {
     double thr;
     uint32_t *pairs;
     uint64_t cap;
-    bool two_pass, count_only, timing;
+    bool two_pass, count_only, timing, recompute;
 };
+
+// Largest match-bit buffer the two-pass mode keeps (bytes); beyond it, or
+// when it cannot be allocated, the second pass recomputes the product.
+const size_t kMaxMaskBytes = (size_t)64 << 30;
 
 int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
 {
@@ -209,10 +213,17 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     const bool self = rq.P == rq.Q && rq.n_p == rq.n_q;
     const bool l2 = rq.metric == SJ_L2;
     const bool blocks = rq.two_pass || rq.count_only;
+    // Count-then-emit with the K-streamed kernel keeps the first pass's match
+    // bits (one per result) when they fit, so the second pass does not repeat
+    // the product.
+    const size_t mask_bytes = (size_t)plan.n_blocks * sjk::ST_MASK_WORDS * 2;
+    bool use_masks = rq.two_pass && !rq.count_only && !rq.recompute &&
+                     plan.family == sjk::FAM_STREAMED && plan.n_blocks <= kMaxMaskBytes / 1024 &&
+                     mask_bytes <= kMaxMaskBytes;
 
     // scratch layout: [repacked P][repacked Q][norms P][norms Q][block counts]
-    //                 [block offsets][scan partials]
-    size_t off_rp = 0, off_rq = 0;
+    //                 [block offsets][scan partials][match bits]
+    size_t off_rp = 0, off_rq = 0, off_mask = 0;
     size_t off_np = 0, off_nq = 0, off_cnt = 0, off_offs = 0, off_part = 0, need = 0;
     if (!aligned) {
         off_rp = need;
@@ -236,7 +247,15 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         off_part = need;
         need = align_up(need + sjk::scan_partials_size(plan.n_blocks) * 8);
     }
-    if ((st = grow_scratch(c, need)) != SJ_OK)
+    off_mask = need;
+    if (use_masks) {
+        const std::string prev_err = g_err;
+        if (grow_scratch(c, need + mask_bytes) != SJ_OK) {
+            use_masks = false;   // recompute instead
+            g_err = prev_err;
+        }
+    }
+    if ((st = grow_scratch(c, use_masks ? need + mask_bytes : need)) != SJ_OK)
         return st;
     uint8_t *scr = (uint8_t *)c->scratch;
 
@@ -264,6 +283,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     g.counter = c->d_small;
     g.block_counts = (uint32_t *)(scr + off_cnt);
     g.block_offsets = (const unsigned long long *)(scr + off_offs);
+    g.masks = use_masks ? (uint16_t *)(scr + off_mask) : nullptr;
     g.qsplit = plan.qsplit;
 
     hipStream_t s = c->stream;
@@ -301,7 +321,8 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
             c->stats.ms_join = elapsed_ms(c->ev[1], c->ev[2]);
         }
     } else {
-        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_COUNT, g, s));
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric,
+                                use_masks ? sjk::MODE_MASK : sjk::MODE_COUNT, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(sjk::launch_scan(g.block_counts, plan.n_blocks,
@@ -321,7 +342,10 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         if (!rq.count_only && total <= rq.cap && total > 0) {
             if (rq.timing)
                 SJ_HIP(hipEventRecord(c->ev[4], s));
-            SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, g, s));
+            if (use_masks)
+                SJ_HIP(sjk::launch_emit_masks(plan, g, s));
+            else
+                SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, g, s));
             if (rq.timing)
                 SJ_HIP(hipEventRecord(c->ev[5], s));
             SJ_HIP(hipStreamSynchronize(s));
@@ -331,6 +355,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     }
     c->stats.total = total;
     c->stats.kernel = (uint32_t)plan.family;
+    c->stats.emit_from_bits = use_masks ? 1u : 0u;
     c->stats.timed = rq.timing ? 1u : 0u;
     *n_out = total;
     if (!rq.count_only && total > rq.cap)
@@ -393,7 +418,8 @@ int sj_join_ip(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
 {
     g_err.clear();
     Request rq{SJ_IP, dtype, P, Q, n_p, n_q, d, s, pairs, cap,
-               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0};
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
+               (flags & SJ_FLAG_RECOMPUTE) != 0};
     return run(ctx, rq, n_out);
 }
 
@@ -403,7 +429,8 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
 {
     g_err.clear();
     Request rq{SJ_L2, dtype, P, Q, n_p, n_q, d, r2, pairs, cap,
-               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0};
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
+               (flags & SJ_FLAG_RECOMPUTE) != 0};
     return run(ctx, rq, n_out);
 }
 
@@ -411,7 +438,7 @@ int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, co
              uint32_t n_q, uint32_t d, double threshold, uint64_t *count)
 {
     g_err.clear();
-    Request rq{metric, dtype, P, Q, n_p, n_q, d, threshold, nullptr, 0, true, true, false};
+    Request rq{metric, dtype, P, Q, n_p, n_q, d, threshold, nullptr, 0, true, true, false, false};
     return run(ctx, rq, count);
 }
 

@@ -1,5 +1,6 @@
-// sj_aux.hip -- kernel planning and dispatch, the squared-row-norm kernel and
-// the exclusive scan of the count-then-emit protocol (gfx950).
+// sj_aux.hip -- kernel planning and dispatch, the squared-row-norm kernel, the
+// exclusive scan of the count-then-emit protocol and its emit pass from match
+// bits (gfx950).
 #include "sj_internal.h"
 
 #include <type_traits>
@@ -20,7 +21,7 @@ static const int kResKS16[4] = {2, 4, 8, 16};
 static const int kResKS8[4] = {1, 2, 4, 8};
 static const uint32_t kResNW = 8;
 static uint32_t res_bn(int ks) { return ks <= 2 ? 256 : ks <= 8 ? 128 : 64; }
-static const uint32_t kStBM = 256, kStBN = 256, kStG = 8, kStNW = 8;
+static const uint32_t kStBM = ST_BM, kStBN = ST_BN, kStG = 8, kStNW = ST_NW;
 
 bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_bytes, int num_cus,
                Plan *plan)
@@ -310,6 +311,79 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
     if (np)
         hipLaunchKernelGGL(scan_apply, dim3((uint32_t)np), dim3(kScanT), 0, stream, counts, n,
                            partials, offsets);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------ emit from the match bits
+// Second pass of count-then-emit after a MODE_MASK first pass of the
+// K-streamed kernel: one wave per output block reads the block's match bits
+// and writes its pairs from the block's offset, in the order of the emit pass
+// that recomputes the product (column block, row block, lanes by their
+// exclusive prefix of the per-lane counts, register order within a lane), so
+// both second passes produce the same array.  Bound by HBM: 1/8 byte read per
+// result and 8 bytes written per match.
+__global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
+{
+    typedef __attribute__((address_space(1))) const uint16_t gmask;
+    typedef __attribute__((address_space(1))) uint64_t gpair;
+    const uint64_t blk = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (blk >= n_blocks || g.block_counts[blk] == 0)   // uniform per wave
+        return;
+    const uint32_t n_qt = (g.n_q + ST_BN - 1) / ST_BN;
+    const uint64_t tile = blk / ST_NW;
+    const uint32_t wave = (uint32_t)(blk % ST_NW);
+    const uint32_t pt = (uint32_t)(tile / n_qt), qt = (uint32_t)(tile % n_qt);
+    const uint32_t wr = wave >> 1, wc = wave & 1;
+    const uint32_t half = (uint32_t)lane >> 5, c32 = (uint32_t)lane & 31;
+    gmask *mk = (gmask *)g.masks + blk * ST_MASK_WORDS + lane;
+    uint32_t m[ST_SA * ST_SB];
+#pragma unroll
+    for (int s = 0; s < ST_SA * ST_SB; ++s)
+        m[s] = mk[64 * s];
+    gpair *out = (gpair *)g.pairs;
+    uint64_t pos = g.block_offsets[blk];
+    const uint32_t i0 = pt * ST_BM + 32 * ST_SA * wr + 4 * half;
+#pragma unroll
+    for (int b = 0; b < ST_SB; ++b) {
+        const uint32_t j = qt * ST_BN + 32 * ST_SB * wc + 32 * b + c32;
+#pragma unroll
+        for (int a = 0; a < ST_SA; ++a) {
+            uint32_t mm = m[b * ST_SA + a];
+            const uint32_t cnt = (uint32_t)__builtin_popcount(mm);
+            uint32_t tot = 0, pre = 0;
+#pragma unroll
+            for (int k = 0; k < 5; ++k) {
+                const uint64_t bits = __ballot((cnt >> k) & 1);
+                tot += (uint32_t)__popcll(bits) << k;
+                pre += __builtin_amdgcn_mbcnt_hi((uint32_t)(bits >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bits, 0u))
+                       << k;
+            }
+            const uint32_t ib = i0 + 32 * a;
+            uint64_t slot = pos + pre;
+            while (mm != 0) {
+                const uint32_t r = (uint32_t)__builtin_ctz(mm);
+                mm &= mm - 1;
+                if (slot < g.cap)
+                    out[slot] = (uint64_t)(ib + 8 * (r >> 2) + (r & 3)) | ((uint64_t)j << 32);
+                ++slot;
+            }
+            pos += tot;
+        }
+    }
+}
+
+hipError_t launch_emit_masks(const Plan &plan, const JoinArgs &g, hipStream_t stream)
+{
+    if (plan.family != FAM_STREAMED)
+        return hipErrorInvalidValue;
+    const uint64_t grid = (plan.n_blocks + 3) / 4;
+    if (grid > 0x7fffffffull)
+        return hipErrorInvalidValue;
+    if (grid)
+        hipLaunchKernelGGL(emit_masks, dim3((uint32_t)grid), dim3(256), 0, stream, g,
+                           plan.n_blocks);
     return hipGetLastError();
 }
 

@@ -14,7 +14,10 @@ enum { MET_IP = 0, MET_L2 = 1 };
 enum Mode {
     MODE_SINGLE = 0,  // append through one atomic counter per wave (single pass)
     MODE_COUNT = 1,   // count the matches of every output block, write no pairs
-    MODE_EMIT = 2     // write each block's matches at its precomputed offset
+    MODE_EMIT = 2,    // write each block's matches at its precomputed offset
+    MODE_MASK = 3     // count as MODE_COUNT and keep every result's match bit
+                      // (K-streamed kernel only), for an emit pass that reads
+                      // the bits instead of recomputing the product
 };
 
 // Kernel families.
@@ -22,6 +25,20 @@ enum Family {
     FAM_RESIDENT = 1,  // P rows held in VGPRs for the whole of d; Q tiles streamed via LDS
     FAM_STREAMED = 2   // both operands streamed through LDS in K chunks (large d)
 };
+
+// Tile geometry of the K-streamed kernel, shared by its planner and by the
+// pass that emits pairs from its match bits: workgroup tiles of ST_BM rows of
+// P by ST_BN rows of Q, ST_NW waves, each owning ST_SA x ST_SB blocks of 32x32
+// results (rows 32 ST_SA wave_row + ..., columns 32 ST_SB wave_col + ...; the
+// waves of a workgroup form a (ST_NW / 2) x 2 grid).  One output block per
+// wave and tile.
+constexpr int ST_BM = 256, ST_BN = 256, ST_NW = 8, ST_SA = 2, ST_SB = 4;
+static_assert(ST_BM == 32 * ST_SA * (ST_NW / 2) && ST_BN == 32 * ST_SB * 2, "wave grid");
+// Match bits of one output block: ST_SA * ST_SB blocks of 32x32 results, each
+// stored as 64 lanes x 16 bits in the MFMA accumulator layout (bit r of lane l
+// is row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the block), blocks
+// in the order (column block, row block).
+constexpr uint32_t ST_MASK_WORDS = ST_SA * ST_SB * 64;
 
 struct JoinArgs {
     const uint8_t *P;            // n_p rows of row_bytes bytes
@@ -37,6 +54,7 @@ struct JoinArgs {
     unsigned long long *counter; // MODE_SINGLE: running match count
     uint32_t *block_counts;      // MODE_COUNT: one count per output block
     const unsigned long long *block_offsets;  // MODE_EMIT: exclusive prefix of block_counts
+    uint16_t *masks;             // MODE_MASK: ST_MASK_WORDS per output block
     uint32_t qsplit;             // FAM_RESIDENT: Q ranges per P block
 };
 
@@ -57,6 +75,12 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
 
 hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, const JoinArgs &args,
                        hipStream_t stream);
+
+// Second pass of count-then-emit for the K-streamed kernel after a MODE_MASK
+// first pass: every output block's pairs from its match bits, written at its
+// offset in the same order as a MODE_EMIT pass (reads g.masks, g.block_counts,
+// g.block_offsets; writes g.pairs below g.cap).
+hipError_t launch_emit_masks(const Plan &plan, const JoinArgs &g, hipStream_t stream);
 
 // Squared row norms: out[i] = sum_k X[i][k]^2 (int32 for int8, fp32 otherwise).
 // Rows as in JoinArgs (16-byte aligned, row_bytes a multiple of 16).

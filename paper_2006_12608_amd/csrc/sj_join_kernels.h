@@ -318,27 +318,17 @@ __device__ __forceinline__ void flush_workgroup_out(WaveOut &wo, int wave, int l
     wo.fill = 0;
 }
 
-// exact_block: every result of one 32x32 block (accumulator `acc`, rows
-// ib + 8 (r / 4) + r % 4 of this lane, column j) is tested exactly into a
-// per-lane 16-bit match mask; per-lane counts give the wave's total and each
-// lane's exclusive prefix (five ballots over the count's bits), and every lane
-// writes its own matches at its prefix, in register order.  MODE_SINGLE
-// appends to the wave's LDS staging buffer (which holds a whole block),
-// MODE_EMIT writes at the output block's running offset (or stages, when the
-// kernel provides a staging buffer), MODE_COUNT only counts.  The code is
-// kept short on purpose: it is inlined at every sub-tile and runs rarely, and
-// a long exact path costs instruction-cache misses when it does run.  L2 row
-// norms come from `nrow` (LDS: this lane's rows of the block).
-template <int DT, int MET, int MODE>
-__device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, uint32_t ib,
-                                            uint32_t j, int lane, typename Mma<DT>::val_t ny,
-                                            const typename Mma<DT>::val_t *nrow,
-                                            const JoinArgs &g, uint64_t &blk_run, WaveOut &wo)
+// Exact test of every result of one 32x32 block (accumulator `acc`, rows
+// ib + 8 (r / 4) + r % 4 of this lane, column j): bit r of the returned mask is
+// set iff that result is a match and its row and column exist.  L2 row norms
+// come from `nrow` (LDS: this lane's rows of the block).
+template <int DT, int MET>
+__device__ __forceinline__ uint32_t block_mask(const typename Mma<DT>::acc_t &acc, uint32_t ib,
+                                               uint32_t j, typename Mma<DT>::val_t ny,
+                                               const typename Mma<DT>::val_t *nrow,
+                                               const JoinArgs &g)
 {
     typedef typename Mma<DT>::val_t V;
-    // Opaque to the optimiser: keeps the per-result row indices from being
-    // hoisted into (and occupying registers of) the caller's main loop.
-    asm volatile("" : "+v"(ib));
     uint32_t m = 0;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -360,6 +350,28 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
             valid |= ib + 8 * (r >> 2) + (r & 3) < g.n_p ? (1u << r) : 0u;
         m &= j < g.n_q ? valid : 0u;
     }
+    return m;
+}
+
+// exact_block: the block's match mask (block_mask); per-lane counts give the
+// wave's total and each lane's exclusive prefix (five ballots over the
+// count's bits), and every lane writes its own matches at its prefix, in
+// register order.  MODE_SINGLE appends to the wave's LDS staging buffer (which
+// holds a whole block), MODE_EMIT writes at the output block's running offset
+// (or stages, when the kernel provides a staging buffer), MODE_COUNT only
+// counts.  The code is kept short on purpose: it is inlined at every sub-tile
+// and runs rarely, and a long exact path costs instruction-cache misses when
+// it does run.
+template <int DT, int MET, int MODE>
+__device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, uint32_t ib,
+                                            uint32_t j, int lane, typename Mma<DT>::val_t ny,
+                                            const typename Mma<DT>::val_t *nrow,
+                                            const JoinArgs &g, uint64_t &blk_run, WaveOut &wo)
+{
+    // Opaque to the optimiser: keeps the per-result row indices from being
+    // hoisted into (and occupying registers of) the caller's main loop.
+    asm volatile("" : "+v"(ib));
+    uint32_t m = block_mask<DT, MET>(acc, ib, j, ny, nrow, g);
     const uint32_t cnt = (uint32_t)__builtin_popcount(m);
     uint32_t tot = 0, pre = 0;
 #pragma unroll
@@ -733,7 +745,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
 // workgroup per CU).  Tiles are visited in groups of 8 P tiles x 8 Q tiles so
 // that concurrently running workgroups share their operand rows in L2.
 // Output block = one wave's 64 x 128 region; index = tile * 8 + wave.
-constexpr int ST_BM = 256, ST_BN = 256, ST_KC = 128, ST_NW = 8;
+constexpr int ST_KC = 128;   // K chunk bytes (tile geometry in sj_internal.h)
 
 template <int DT, int MET, int MODE>
 __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
@@ -749,7 +761,7 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
     constexpr int NLD = NPOS / NT;                    // direct loads per thread
     constexpr int P_LOADS = ST_BM * (CPR + 1) / 64;   // wave loads below this fill P rows
     constexpr int KSC = ST_KC / 32;                   // k-steps per chunk
-    constexpr int SA = 2, SB = 4;                     // A- and B-blocks per wave
+    constexpr int SA = ST_SA, SB = ST_SB;             // A- and B-blocks per wave
     constexpr bool NEED_NORMS = (MET == MET_L2);
     static_assert(NPOS % NT == 0 && (ST_BM * (CPR + 1)) % 64 == 0, "load layout");
 
@@ -833,8 +845,8 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
                      __attribute__((always_inline)) {
         if (kc + 1 < n_chunks)
             stage_issue(kc + 1, nxt);
-        const uint8_t *pa = cur + (64 * wr + c32) * LS + 16 * half;
-        const uint8_t *pb = cur + (ST_BM + 128 * wc + c32) * LS + 16 * half;
+        const uint8_t *pa = cur + (32 * SA * wr + c32) * LS + 16 * half;
+        const uint8_t *pb = cur + (ST_BM + 32 * SB * wc + c32) * LS + 16 * half;
         i32x4 ring[RING][SA + SB];
         auto fetch = [&](i32x4(&f)[SA + SB], int ks) __attribute__((always_inline)) {
 #pragma unroll
@@ -872,7 +884,7 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
             chunk(kc + 1, s_op1, s_op0);
     }
 
-    const uint32_t prow0 = p0 + 64 * wr;
+    const uint32_t prow0 = p0 + 32 * SA * wr;
     const uint32_t ibase = prow0 + 4 * half;
     V nmin = big_val<V>();
     const V *nrows = nullptr;
@@ -890,11 +902,41 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
     WaveOut wo{(lds_pair *)stage_mem, STAGE_BYTES / 8, 0u, 0ull};
     const uint64_t blk = (uint64_t)(pt * n_qt + qt) * ST_NW + wave;
     uint64_t blk_run = 0;
+    if constexpr (MODE == MODE_MASK) {
+        // Every block is tested exactly and its match bits are kept for the
+        // emit pass (one 128-byte store per block); the output block's count
+        // is the wave's sum of the lanes' popcounts (at most 16 SA SB < 2^8).
+        typedef __attribute__((address_space(1))) uint16_t global_u16;
+        global_u16 *mk = (global_u16 *)g.masks + blk * ST_MASK_WORDS + lane;
+        uint32_t lane_cnt = 0;
+#pragma unroll
+        for (int b = 0; b < SB; ++b) {
+            const uint32_t j = q0 + 32 * SB * wc + 32 * b + c32;
+            V ny = V(0);
+            if constexpr (NEED_NORMS)
+                ny = j < g.n_q ? ((const V *)g.norm_q)[j] : big_val<V>();
+#pragma unroll
+            for (int a = 0; a < SA; ++a) {
+                const uint32_t m =
+                    block_mask<DT, MET>(acc[a][b], ibase + 32 * a, j, ny, nrows + 32 * a, g);
+                mk[(b * SA + a) * 64] = (uint16_t)m;
+                lane_cnt += (uint32_t)__builtin_popcount(m);
+            }
+        }
+        static_assert(16 * SA * SB < 256, "lane count bits");
+        uint32_t tot = 0;
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit)
+            tot += (uint32_t)__popcll(__ballot((lane_cnt >> bit) & 1)) << bit;
+        if (lane == 0)
+            g.block_counts[blk] = tot;
+        return;
+    }
     if constexpr (MODE == MODE_EMIT)
         wo.dst = g.block_offsets[blk];
 #pragma unroll
     for (int b = 0; b < SB; ++b) {
-        const uint32_t j = q0 + 128 * wc + 32 * b + c32;
+        const uint32_t j = q0 + 32 * SB * wc + 32 * b + c32;
         V ny = V(0);
         if constexpr (NEED_NORMS)
             ny = j < g.n_q ? ((const V *)g.norm_q)[j] : big_val<V>();
@@ -1022,6 +1064,18 @@ hipError_t launch_mode(const Plan &p, const JoinArgs &g, hipStream_t st)
 template <int DT>
 hipError_t launch_dtype(const Plan &p, int metric, int mode, const JoinArgs &g, hipStream_t st)
 {
+    if (mode == MODE_MASK) {
+        // K-streamed kernel only
+        if (p.family != FAM_STREAMED || (metric != MET_IP && metric != MET_L2))
+            return hipErrorInvalidValue;
+        if (metric == MET_IP)
+            hipLaunchKernelGGL((join_streamed<DT, MET_IP, MODE_MASK>), dim3(p.grid),
+                               dim3(ST_NW * 64), 0, st, g);
+        else
+            hipLaunchKernelGGL((join_streamed<DT, MET_L2, MODE_MASK>), dim3(p.grid),
+                               dim3(ST_NW * 64), 0, st, g);
+        return hipGetLastError();
+    }
     if (metric == MET_IP) {
         switch (mode) {
         case MODE_SINGLE: return launch_mode<DT, MET_IP, MODE_SINGLE>(p, g, st);

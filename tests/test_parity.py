@@ -191,6 +191,46 @@ def test_streamed_dense_output(dtype, d):
         run_case(w, two_pass=two_pass)
 
 
+@pytest.mark.parametrize("dtype,d,metric", [("bf16", 300, "ip"), ("f16", 520, "l2"),
+                                             ("i8", 700, "ip"), ("i8", 530, "l2")])
+def test_two_pass_match_bits_equal_recompute(dtype, d, metric):
+    """Count-then-emit on the K-streamed kernel: the second pass that reads the
+    first pass's match bits writes the same array (same order) as the one that
+    recomputes the product, over several tiles with ragged edges, and the set
+    is the oracle's; a capacity one short of the total is an overflow with the
+    exact total."""
+    import torch
+    import paper_2006_12608_amd as sj
+    w = workloads.random_case(40 + d, 600, 777, d, dtype, lo=-2, hi=2)
+    w.metric = metric
+    Pd, Qd = to_device(w.P, dtype), to_device(w.Q, dtype)
+    x = values(dtype, w.P).astype(np.int64)
+    y = values(dtype, w.Q).astype(np.int64)
+    if metric == "ip":
+        w.threshold = float(np.quantile(x @ y.T, 0.9, method="nearest"))
+    else:
+        d2 = (x * x).sum(1)[:, None] + (y * y).sum(1)[None, :] - 2 * (x @ y.T)
+        w.threshold = float(np.quantile(d2, 0.1, method="nearest"))
+    say("match bits vs recompute", dtype, d, metric, w.threshold)
+    ctx = sj.context(0)
+    f = sj.join_ip if metric == "ip" else sj.join_l2
+    a = f(Pd, Qd, w.threshold, two_pass=True, ctx=ctx)
+    st = sj.sj_get_stats(ctx)
+    assert st.kernel == 2 and st.emit_from_bits == 1
+    b = f(Pd, Qd, w.threshold, two_pass=True, recompute=True, ctx=ctx)
+    assert sj.sj_get_stats(ctx).emit_from_bits == 0
+    assert a.shape[0] > 0 and torch.equal(a, b)
+    ref = oracle.join(metric, dtype, w.P, w.Q, w.threshold)
+    compare(sorted_pairs(a), ref, False)
+    c = f(Pd, Qd, w.threshold, two_pass=False, ctx=ctx)
+    assert np.array_equal(sorted_pairs(a), sorted_pairs(c))
+    total = a.shape[0]
+    out = torch.empty((total, 2), dtype=torch.int32, device="cuda")
+    with pytest.raises(sj.SjError) as e:
+        f(Pd, Qd, w.threshold, cap=total - 1, out=out, two_pass=True, ctx=ctx)
+    assert e.value.status == sj.SJ_E_OVERFLOW and e.value.n_out == total
+
+
 def test_ties_are_inclusive():
     """Rows with known exact scores at the threshold are reported; one above is not."""
     rng = np.random.default_rng(5)
