@@ -316,60 +316,81 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
 
 // ------------------------------------------------ emit from the match bits
 // Second pass of count-then-emit after a MODE_MASK first pass of the
-// K-streamed kernel: one wave per output block reads the block's match bits
-// and writes its pairs from the block's offset, in the order of the emit pass
-// that recomputes the product (column block, row block, lanes by their
-// exclusive prefix of the per-lane counts, register order within a lane), so
-// both second passes produce the same array.  Bound by HBM: 1/8 byte read per
+// K-streamed kernel: each wave takes kEmitBlocks consecutive output blocks,
+// loads their counts, offsets and match bits at once (one 16-byte load per
+// lane per block, so the loads' latency is paid once per group), and writes
+// every block's pairs from its offset in the order of the emit pass that
+// recomputes the product (column block, row block, lanes by their exclusive
+// prefix of the per-lane counts, register order within a lane), so both
+// second passes produce the same array.  Bound by HBM: 1/8 byte read per
 // result and 8 bytes written per match.
+static const uint32_t kEmitBlocks = 4;
+
 __global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
 {
-    typedef __attribute__((address_space(1))) const uint16_t gmask;
+    typedef __attribute__((address_space(1))) const i32x4 gmask;
     typedef __attribute__((address_space(1))) uint64_t gpair;
-    const uint64_t blk = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    if (blk >= n_blocks || g.block_counts[blk] == 0)   // uniform per wave
+    // wave-uniform block index (scalar registers, scalar arithmetic below)
+    const uint32_t wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint64_t blk0 = ((uint64_t)blockIdx.x * 4 + wv) * kEmitBlocks;
+    if (blk0 >= n_blocks)   // uniform per wave
         return;
+    uint32_t cnt[kEmitBlocks];
+    uint64_t off[kEmitBlocks];
+    i32x4 mw[kEmitBlocks];
+#pragma unroll
+    for (uint32_t k = 0; k < kEmitBlocks; ++k) {
+        const bool in = blk0 + k < n_blocks;
+        cnt[k] = in ? g.block_counts[blk0 + k] : 0u;
+        off[k] = in ? g.block_offsets[blk0 + k] : 0ull;
+        mw[k] = in ? *((gmask *)g.masks + ((blk0 + k) * 64 + lane)) : i32x4{0, 0, 0, 0};
+    }
     const uint32_t n_qt = (g.n_q + ST_BN - 1) / ST_BN;
-    const uint64_t tile = blk / ST_NW;
-    const uint32_t wave = (uint32_t)(blk % ST_NW);
-    const uint32_t pt = (uint32_t)(tile / n_qt), qt = (uint32_t)(tile % n_qt);
-    const uint32_t wr = wave >> 1, wc = wave & 1;
     const uint32_t half = (uint32_t)lane >> 5, c32 = (uint32_t)lane & 31;
-    gmask *mk = (gmask *)g.masks + blk * ST_MASK_WORDS + lane;
-    uint32_t m[ST_SA * ST_SB];
-#pragma unroll
-    for (int s = 0; s < ST_SA * ST_SB; ++s)
-        m[s] = mk[64 * s];
     gpair *out = (gpair *)g.pairs;
-    uint64_t pos = g.block_offsets[blk];
-    const uint32_t i0 = pt * ST_BM + 32 * ST_SA * wr + 4 * half;
+#pragma unroll 1
+    for (uint32_t k = 0; k < kEmitBlocks; ++k) {
+        if (cnt[k] == 0)
+            continue;
+        const uint64_t blk = blk0 + k;
+        // the match bits exist only for at most 2^26 blocks (64 GiB), so the
+        // tile index fits 32 bits
+        const uint32_t tile = (uint32_t)(blk / ST_NW);
+        const uint32_t wave = (uint32_t)(blk % ST_NW);
+        const uint32_t pt = tile / n_qt, qt = tile % n_qt;
+        const uint32_t wr = wave >> 1, wc = wave & 1;
+        const uint32_t i0 = pt * ST_BM + 32 * ST_SA * wr + 4 * half;
+        uint64_t pos = off[k];
 #pragma unroll
-    for (int b = 0; b < ST_SB; ++b) {
-        const uint32_t j = qt * ST_BN + 32 * ST_SB * wc + 32 * b + c32;
+        for (int b = 0; b < ST_SB; ++b) {
+            const uint32_t j = qt * ST_BN + 32 * ST_SB * wc + 32 * b + c32;
 #pragma unroll
-        for (int a = 0; a < ST_SA; ++a) {
-            uint32_t mm = m[b * ST_SA + a];
-            const uint32_t cnt = (uint32_t)__builtin_popcount(mm);
-            uint32_t tot = 0, pre = 0;
+            for (int a = 0; a < ST_SA; ++a) {
+                const int sb = b * ST_SA + a;
+                uint32_t mm = ((uint32_t)mw[k][sb / 2] >> (16 * (sb % 2))) & 0xffffu;
+                const uint32_t c = (uint32_t)__builtin_popcount(mm);
+                uint32_t tot = 0, pre = 0;
 #pragma unroll
-            for (int k = 0; k < 5; ++k) {
-                const uint64_t bits = __ballot((cnt >> k) & 1);
-                tot += (uint32_t)__popcll(bits) << k;
-                pre += __builtin_amdgcn_mbcnt_hi((uint32_t)(bits >> 32),
-                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bits, 0u))
-                       << k;
+                for (int t = 0; t < 5; ++t) {
+                    const uint64_t bits = __ballot((c >> t) & 1);
+                    tot += (uint32_t)__popcll(bits) << t;
+                    pre += __builtin_amdgcn_mbcnt_hi(
+                               (uint32_t)(bits >> 32),
+                               __builtin_amdgcn_mbcnt_lo((uint32_t)bits, 0u))
+                           << t;
+                }
+                const uint32_t ib = i0 + 32 * a;
+                uint64_t slot = pos + pre;
+                while (mm != 0) {
+                    const uint32_t r = (uint32_t)__builtin_ctz(mm);
+                    mm &= mm - 1;
+                    if (slot < g.cap)
+                        out[slot] = (uint64_t)(ib + 8 * (r >> 2) + (r & 3)) | ((uint64_t)j << 32);
+                    ++slot;
+                }
+                pos += tot;
             }
-            const uint32_t ib = i0 + 32 * a;
-            uint64_t slot = pos + pre;
-            while (mm != 0) {
-                const uint32_t r = (uint32_t)__builtin_ctz(mm);
-                mm &= mm - 1;
-                if (slot < g.cap)
-                    out[slot] = (uint64_t)(ib + 8 * (r >> 2) + (r & 3)) | ((uint64_t)j << 32);
-                ++slot;
-            }
-            pos += tot;
         }
     }
 }
@@ -378,7 +399,8 @@ hipError_t launch_emit_masks(const Plan &plan, const JoinArgs &g, hipStream_t st
 {
     if (plan.family != FAM_STREAMED)
         return hipErrorInvalidValue;
-    const uint64_t grid = (plan.n_blocks + 3) / 4;
+    const uint64_t per_wg = 4ull * kEmitBlocks;
+    const uint64_t grid = (plan.n_blocks + per_wg - 1) / per_wg;
     if (grid > 0x7fffffffull)
         return hipErrorInvalidValue;
     if (grid)

@@ -34,11 +34,13 @@ enum Family {
 // wave and tile.
 constexpr int ST_BM = 256, ST_BN = 256, ST_NW = 8, ST_SA = 2, ST_SB = 4;
 static_assert(ST_BM == 32 * ST_SA * (ST_NW / 2) && ST_BN == 32 * ST_SB * 2, "wave grid");
-// Match bits of one output block: ST_SA * ST_SB blocks of 32x32 results, each
-// stored as 64 lanes x 16 bits in the MFMA accumulator layout (bit r of lane l
-// is row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the block), blocks
-// in the order (column block, row block).
+// Match bits of one output block: ST_SA * ST_SB blocks of 32x32 results as
+// 16-bit lane masks in the MFMA accumulator layout (bit r of lane l's mask is
+// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32 of the block), stored
+// lane-major: lane l's masks of blocks s = column block * ST_SA + row block
+// are the 16 contiguous bytes [16 l, 16 l + 16) (mask s in bytes 2 s, 2 s + 1).
 constexpr uint32_t ST_MASK_WORDS = ST_SA * ST_SB * 64;
+static_assert(ST_SA * ST_SB == 8, "one 16-byte access per lane");
 
 struct JoinArgs {
     const uint8_t *P;            // n_p rows of row_bytes bytes

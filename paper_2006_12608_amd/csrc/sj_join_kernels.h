@@ -904,10 +904,10 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
     uint64_t blk_run = 0;
     if constexpr (MODE == MODE_MASK) {
         // Every block is tested exactly and its match bits are kept for the
-        // emit pass (one 128-byte store per block); the output block's count
-        // is the wave's sum of the lanes' popcounts (at most 16 SA SB < 2^8).
-        typedef __attribute__((address_space(1))) uint16_t global_u16;
-        global_u16 *mk = (global_u16 *)g.masks + blk * ST_MASK_WORDS + lane;
+        // emit pass (one 16-byte store per lane); the output block's count is
+        // the wave's sum of the lanes' popcounts (at most 16 SA SB < 2^8).
+        typedef __attribute__((address_space(1))) i32x4 global_i32x4;
+        uint32_t mw[SA * SB / 2] = {};
         uint32_t lane_cnt = 0;
 #pragma unroll
         for (int b = 0; b < SB; ++b) {
@@ -919,11 +919,14 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
             for (int a = 0; a < SA; ++a) {
                 const uint32_t m =
                     block_mask<DT, MET>(acc[a][b], ibase + 32 * a, j, ny, nrows + 32 * a, g);
-                mk[(b * SA + a) * 64] = (uint16_t)m;
+                const int sb = b * SA + a;
+                mw[sb / 2] |= m << (16 * (sb % 2));
                 lane_cnt += (uint32_t)__builtin_popcount(m);
             }
         }
-        static_assert(16 * SA * SB < 256, "lane count bits");
+        static_assert(SA * SB == 8 && 16 * SA * SB < 256, "mask record and count bits");
+        *((global_i32x4 *)g.masks + (blk * 64 + lane)) =
+            i32x4{(int)mw[0], (int)mw[1], (int)mw[2], (int)mw[3]};
         uint32_t tot = 0;
 #pragma unroll
         for (int bit = 0; bit < 8; ++bit)
