@@ -318,16 +318,33 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
 // Second pass of count-then-emit after a MODE_MASK first pass of the
 // K-streamed kernel: each wave takes kEmitBlocks consecutive output blocks,
 // loads their counts, offsets and match bits at once (one 16-byte load per
-// lane per block, so the loads' latency is paid once per group), and writes
-// every block's pairs from its offset in the order of the emit pass that
-// recomputes the product (column block, row block, lanes by their exclusive
-// prefix of the per-lane counts, register order within a lane), so both
-// second passes produce the same array.  Bound by HBM: 1/8 byte read per
-// result and 8 bytes written per match.
+// lane per block), and writes every block's pairs from its offset in the
+// order of the emit pass that recomputes the product (column block, row block,
+// lanes by their exclusive prefix of the per-lane counts, register order
+// within a lane), so both second passes produce the same array.  Bound by HBM:
+// 1/8 byte read per result and 8 bytes written per match.
 static const uint32_t kEmitBlocks = 4;
+
+// Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele steps inside
+// each row of 16 lanes (DPP row shifts by 1, 2, 4, 8; lanes shifted in from
+// outside the row contribute 0), then the totals of rows 0 and 2 into rows 1
+// and 3 (row broadcast of lane 15) and the total of lanes 0-31 into rows 2 and
+// 3 (row broadcast of lane 31).  Sums of packed 16-bit fields stay separate
+// while every field's total stays below 2^16.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x)
+{
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);
+    return x;
+}
 
 __global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
 {
+    static_assert(ST_SA == 2 && ST_SB == 4, "one 32-bit word per column block");
     typedef __attribute__((address_space(1))) const i32x4 gmask;
     typedef __attribute__((address_space(1))) uint64_t gpair;
     const int lane = threadIdx.x & 63;
@@ -349,7 +366,7 @@ __global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
     const uint32_t n_qt = (g.n_q + ST_BN - 1) / ST_BN;
     const uint32_t half = (uint32_t)lane >> 5, c32 = (uint32_t)lane & 31;
     gpair *out = (gpair *)g.pairs;
-#pragma unroll 1
+#pragma unroll
     for (uint32_t k = 0; k < kEmitBlocks; ++k) {
         if (cnt[k] == 0)
             continue;
@@ -361,35 +378,42 @@ __global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
         const uint32_t pt = tile / n_qt, qt = tile % n_qt;
         const uint32_t wr = wave >> 1, wc = wave & 1;
         const uint32_t i0 = pt * ST_BM + 32 * ST_SA * wr + 4 * half;
-        uint64_t pos = off[k];
+        // Word b of the record holds column block b: its 32x32 row block 0 in
+        // the low 16 bits, row block 1 in the high 16 bits.  The lanes' match
+        // counts of both halves, packed, are scanned over the wave at once.
+        uint32_t w[ST_SB], incl[ST_SB];
 #pragma unroll
         for (int b = 0; b < ST_SB; ++b) {
+            w[b] = (uint32_t)mw[k][b];
+            const uint32_t c = (uint32_t)__builtin_popcount(w[b] & 0xffffu) |
+                               ((uint32_t)__builtin_popcount(w[b] >> 16) << 16);
+            incl[b] = wave_incl_scan_u32(c);
+        }
+        // block-relative start of each (column block, row block) segment
+        uint32_t seg = 0;
+#pragma unroll
+        for (int b = 0; b < ST_SB; ++b) {
+            const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl[b], 63);
+            const uint32_t c = (uint32_t)__builtin_popcount(w[b] & 0xffffu) |
+                               ((uint32_t)__builtin_popcount(w[b] >> 16) << 16);
+            const uint32_t excl = incl[b] - c;
+            uint64_t slot0 = off[k] + seg + (excl & 0xffffu);
+            seg += tot & 0xffffu;
+            uint64_t slot1 = off[k] + seg + (excl >> 16);
+            seg += tot >> 16;
             const uint32_t j = qt * ST_BN + 32 * ST_SB * wc + 32 * b + c32;
-#pragma unroll
-            for (int a = 0; a < ST_SA; ++a) {
-                const int sb = b * ST_SA + a;
-                uint32_t mm = ((uint32_t)mw[k][sb / 2] >> (16 * (sb % 2))) & 0xffffu;
-                const uint32_t c = (uint32_t)__builtin_popcount(mm);
-                uint32_t tot = 0, pre = 0;
-#pragma unroll
-                for (int t = 0; t < 5; ++t) {
-                    const uint64_t bits = __ballot((c >> t) & 1);
-                    tot += (uint32_t)__popcll(bits) << t;
-                    pre += __builtin_amdgcn_mbcnt_hi(
-                               (uint32_t)(bits >> 32),
-                               __builtin_amdgcn_mbcnt_lo((uint32_t)bits, 0u))
-                           << t;
-                }
-                const uint32_t ib = i0 + 32 * a;
-                uint64_t slot = pos + pre;
-                while (mm != 0) {
-                    const uint32_t r = (uint32_t)__builtin_ctz(mm);
-                    mm &= mm - 1;
-                    if (slot < g.cap)
-                        out[slot] = (uint64_t)(ib + 8 * (r >> 2) + (r & 3)) | ((uint64_t)j << 32);
-                    ++slot;
-                }
-                pos += tot;
+            // bit r: row block r / 16, register r % 16, i.e. row
+            // i0 + 32 (r / 16) + 8 ((r % 16) / 4) + r % 4 = i0 + 2 (r & 28) + (r & 3)
+            uint32_t mm = w[b];
+            while (mm != 0) {
+                const uint32_t r = (uint32_t)__builtin_ctz(mm);
+                mm &= mm - 1;
+                const bool hi = r >= 16;
+                const uint64_t slot = hi ? slot1 : slot0;
+                slot1 += hi ? 1u : 0u;
+                slot0 += hi ? 0u : 1u;
+                if (slot < g.cap)
+                    out[slot] = (uint64_t)(i0 + 2 * (r & 28) + (r & 3)) | ((uint64_t)j << 32);
             }
         }
     }

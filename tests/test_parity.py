@@ -120,6 +120,21 @@ def test_real_valued_band(dtype, metric):
     say("band", info)
 
 
+@pytest.mark.parametrize("dtype,metric", [("f16", "ip"), ("bf16", "l2")])
+def test_real_valued_band_streamed_two_pass(dtype, metric):
+    """Real-valued rows long enough for the K-streamed kernel, count-then-emit
+    (the first pass's match bits): equal to the oracle outside the band."""
+    w = workloads.random_case(8, 520, 610, 400, dtype, real=True, metric=metric)
+    x, y = values(dtype, w.P), values(dtype, w.Q)
+    if metric == "ip":
+        thr = float(np.quantile(x @ y.T, 0.99))
+    else:
+        D = (x * x).sum(1)[:, None] + (y * y).sum(1)[None, :] - 2 * (x @ y.T)
+        thr = float(np.quantile(D, 0.01))
+    info, _, _ = run_case(w, thr=thr, two_pass=True)
+    say("band", info)
+
+
 # ------------------------------------------------------- protocol / edges
 
 def test_two_pass_is_deterministic_and_equals_single():
@@ -267,9 +282,10 @@ def test_self_join_same_pointer_all_variants():
         w.self_join = True
         x = values(dtype, w.P).astype(np.int64)
         w.threshold = float(np.quantile(x @ x.T, 0.98, method="nearest"))
-        _, g, _ = run_case(w)
-        s = set(map(tuple, g.tolist()))
-        assert s == {(j, i) for (i, j) in s}
+        for two_pass in (False, True):
+            _, g, _ = run_case(w, two_pass=two_pass)
+            s = set(map(tuple, g.tolist()))
+            assert s == {(j, i) for (i, j) in s}
 
 
 # ------------------------------------------------ full-size, sampled rows
