@@ -74,14 +74,16 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(workload: str, launches_bytes_alg: float):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources; otherwise None."""
+def traffic_for(key: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary (key:
+    the workload name for its join or first-pass kernel, "<workload>:emit" for
+    its emit-from-bits kernel), if it was taken on the current kernel sources;
+    otherwise None."""
     p = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(p):
         return None
     try:
-        rec = json.load(open(p)).get(workload)
+        rec = json.load(open(p)).get(key)
     except (ValueError, OSError):
         return None
     if not rec or rec.get("kernel_sha") != kernel_source_hash():
@@ -244,7 +246,7 @@ def main():
     flop = 2.0 * pair_evals * max(w.d, 1)
     achieved = flop / (kms / 1e3) / 1e12
     peak = PEAK[w.dtype]
-    traffic = traffic_for(args.workload, flop)
+    traffic = traffic_for(args.workload)
     line = {
         "metric": "pair-evaluations/sec",
         "value": value,
@@ -283,7 +285,8 @@ def main():
         tiles = -(-w.n_p // 256) * -(-w.n_q // 256)
         emit_bytes = n_out * 8 + (tiles * 256 * 256 // 8 if from_bits else 0)
         line["emit"] = {"from_match_bits": from_bits, "hbm_bytes_algorithmic": emit_bytes,
-                        "hbm_gbps_algorithmic": emit_bytes / (float(np.mean(emit_ms)) / 1e3) / 1e9}
+                        "hbm_gbps_algorithmic": emit_bytes / (float(np.mean(emit_ms)) / 1e3) / 1e9,
+                        "traffic": traffic_for(args.workload + ":emit") if from_bits else None}
     # the same fraction against what the matrix cores alone sustain on this GPU
     # over a run as long as the timed region, on this workload's data (the
     # clock under load is below the spec peak's 2.4 GHz and depends on the
