@@ -323,7 +323,9 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, unsigned long long *o
 // lanes by their exclusive prefix of the per-lane counts, register order
 // within a lane), so both second passes produce the same array.  Bound by HBM:
 // 1/8 byte read per result and 8 bytes written per match.
-static const uint32_t kEmitBlocks = 4;
+// 16 blocks (two tiles) per wave: on the 131072 x 1024 clustered workload
+// 1.59 ms, against 1.77-1.81 ms for 2, 4, 8, 12 or 32 blocks.
+static const uint32_t kEmitBlocks = 16;
 
 // Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele steps inside
 // each row of 16 lanes (DPP row shifts by 1, 2, 4, 8; lanes shifted in from
