@@ -77,14 +77,16 @@ enum sj_flags {
     /* Count-then-emit: a first pass counts the matches of every output block,
      * an exclusive scan turns the counts into offsets, and a second pass
      * writes each block's pairs at its offset.  Never writes beyond `cap`,
-     * and the output order is deterministic (block-major).  The second pass
-     * recomputes the product, except with the K-streamed kernel (rows of more
-     * than 512 bytes), whose first pass also keeps one match bit per result
-     * in device scratch (n_p n_q / 8 bytes, rounded up to 256 x 256 tiles)
-     * when that fits, so that the second pass only reads the bits and writes
-     * the pairs.  Both second passes write the same array.  Without the flag
-     * a single pass appends pairs through one atomic counter (order
-     * unspecified). */
+     * and the output order is deterministic (block-major).  The first pass
+     * also keeps the match bits it found in device scratch, so that the
+     * second pass only reads them and writes the pairs: with the K-streamed
+     * kernel (rows of more than 512 bytes) one bit per result (n_p n_q / 8
+     * bytes, rounded up to 256 x 256 tiles, while at most 64 GiB), with the
+     * resident kernel one 160-byte record per 32 x 32 block that has matches
+     * (room for min(4 Mi, blocks) records).  When the bits do not fit, the
+     * second pass recomputes the product; both second passes write the same
+     * array.  Without the flag a single pass appends pairs through one atomic
+     * counter (order unspecified). */
     SJ_FLAG_TWO_PASS = 1u,
     /* Record GPU timestamps around every phase of the call (see sj_stats). */
     SJ_FLAG_TIMING = 2u,
@@ -104,7 +106,8 @@ typedef struct sj_stats {
     uint32_t kernel;       /* 1 = P rows resident in registers, 2 = K-streamed */
     uint32_t timed;        /* 1 when the ms_* fields were measured             */
     uint32_t emit_from_bits; /* two-pass: 1 when the second pass read the first
-                                pass's match bits instead of recomputing      */
+                                pass's match bits (or match records) instead
+                                of recomputing the product                    */
 } sj_stats;
 
 /* Create a context on `device` (a gfx950 GPU), bound to `stream` (a

@@ -18,7 +18,8 @@ struct sj_ctx {
     int device = 0;
     hipStream_t stream = nullptr;
     int num_cus = 256;
-    unsigned long long *d_small = nullptr;  // [0] match counter, [1] scan total
+    unsigned long long *d_small = nullptr;  // [0] match counter, [1] scan total,
+                                            // [2] largest per-workgroup record count
     unsigned long long *h_small = nullptr;  // pinned host copy of d_small
     void *scratch = nullptr;
     size_t scratch_bytes = 0;
@@ -162,6 +163,11 @@ struct Request {
 // Largest match-bit buffer the two-pass mode keeps (bytes); beyond it, or
 // when it cannot be allocated, the second pass recomputes the product.
 const size_t kMaxMaskBytes = (size_t)64 << 30;
+// Room for match records (resident kernel's two-pass mode), split evenly over
+// the first pass's workgroups: at most 4 Mi records (640 MiB) in all, and per
+// workgroup at most its number of 32x32 blocks; a workgroup that finds more
+// blocks with matches makes the second pass recompute.
+const uint64_t kMaxRecords = (uint64_t)4 << 20;
 
 int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
 {
@@ -220,6 +226,19 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     bool use_masks = rq.two_pass && !rq.count_only && !rq.recompute &&
                      plan.family == sjk::FAM_STREAMED && plan.n_blocks <= kMaxMaskBytes / 1024 &&
                      mask_bytes <= kMaxMaskBytes;
+    // With the resident kernel it appends a record per 32x32 block with
+    // matches instead (its outputs are sparse next to its products).
+    bool use_records = rq.two_pass && !rq.count_only && !rq.recompute &&
+                       plan.family == sjk::FAM_RESIDENT;
+    // a workgroup covers n_blocks / grid output blocks of at most 32 32x32
+    // blocks each (BM x BN <= 1024 x 256 results)
+    uint64_t rec_cap = kMaxRecords / plan.grid;
+    const uint64_t wg_sub = (plan.n_blocks / plan.grid + 1) * 32;
+    rec_cap = rec_cap < wg_sub ? rec_cap : wg_sub;
+    if (rec_cap == 0)
+        use_records = false;
+    const size_t rec_bytes = align_up((size_t)rec_cap * plan.grid * sizeof(sjk::MatchRecord)) +
+                             (size_t)plan.grid * 4;
 
     // scratch layout: [repacked P][repacked Q][norms P][norms Q][block counts]
     //                 [block offsets][scan partials][match bits]
@@ -247,15 +266,16 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         off_part = need;
         need = align_up(need + sjk::scan_partials_size(plan.n_blocks) * 8);
     }
-    off_mask = need;
-    if (use_masks) {
+    off_mask = need;   // match bits or match records
+    const size_t extra = use_masks ? mask_bytes : use_records ? rec_bytes : 0;
+    if (extra) {
         const std::string prev_err = g_err;
-        if (grow_scratch(c, need + mask_bytes) != SJ_OK) {
-            use_masks = false;   // recompute instead
+        if (grow_scratch(c, need + extra) != SJ_OK) {
+            use_masks = use_records = false;   // recompute instead
             g_err = prev_err;
         }
     }
-    if ((st = grow_scratch(c, use_masks ? need + mask_bytes : need)) != SJ_OK)
+    if ((st = grow_scratch(c, use_masks || use_records ? need + extra : need)) != SJ_OK)
         return st;
     uint8_t *scr = (uint8_t *)c->scratch;
 
@@ -284,12 +304,21 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     g.block_counts = (uint32_t *)(scr + off_cnt);
     g.block_offsets = (const unsigned long long *)(scr + off_offs);
     g.masks = use_masks ? (uint16_t *)(scr + off_mask) : nullptr;
+    g.records = use_records ? (sjk::MatchRecord *)(scr + off_mask) : nullptr;
+    g.rec_cap = use_records ? (uint32_t)rec_cap : 0;
+    g.rec_counts = use_records ? (uint32_t *)(scr + off_mask +
+                                              align_up((size_t)rec_cap * plan.grid *
+                                                       sizeof(sjk::MatchRecord)))
+                               : nullptr;
+    g.rec_max = c->d_small + 2;
     g.qsplit = plan.qsplit;
 
     hipStream_t s = c->stream;
     SJ_HIP(hipSetDevice(c->device));
     if (!blocks)
         SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
+    if (use_records)
+        SJ_HIP(hipMemsetAsync(c->d_small + 2, 0, sizeof(unsigned long long), s));
     if (rq.timing)
         SJ_HIP(hipEventRecord(c->ev[0], s));
     if (!aligned) {
@@ -308,6 +337,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         SJ_HIP(hipEventRecord(c->ev[1], s));
 
     uint64_t total = 0;
+    bool emit_from_bits = false;
     if (!blocks) {
         SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_SINGLE, g, s));
         if (rq.timing)
@@ -322,7 +352,10 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         }
     } else {
         SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric,
-                                use_masks ? sjk::MODE_MASK : sjk::MODE_COUNT, g, s));
+                                use_masks     ? sjk::MODE_MASK
+                                : use_records ? sjk::MODE_RECORD
+                                              : sjk::MODE_COUNT,
+                                g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(sjk::launch_scan(g.block_counts, plan.n_blocks,
@@ -330,10 +363,12 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
                                 (unsigned long long *)(scr + off_part), c->d_small + 1, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[3], s));
-        SJ_HIP(hipMemcpyAsync(c->h_small + 1, c->d_small + 1, sizeof(unsigned long long),
+        SJ_HIP(hipMemcpyAsync(c->h_small + 1, c->d_small + 1, 2 * sizeof(unsigned long long),
                               hipMemcpyDeviceToHost, s));
         SJ_HIP(hipStreamSynchronize(s));
         total = c->h_small[1];
+        if (use_records && c->h_small[2] > rec_cap)
+            use_records = false;   // some blocks have no record: recompute
         if (rq.timing) {
             c->stats.ms_norms = l2 ? elapsed_ms(c->ev[0], c->ev[1]) : 0.0;
             c->stats.ms_count = elapsed_ms(c->ev[1], c->ev[2]);
@@ -344,8 +379,11 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
                 SJ_HIP(hipEventRecord(c->ev[4], s));
             if (use_masks)
                 SJ_HIP(sjk::launch_emit_masks(plan, g, s));
+            else if (use_records)
+                SJ_HIP(sjk::launch_emit_records(g, plan.grid, s));
             else
                 SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_EMIT, g, s));
+            emit_from_bits = use_masks || use_records;
             if (rq.timing)
                 SJ_HIP(hipEventRecord(c->ev[5], s));
             SJ_HIP(hipStreamSynchronize(s));
@@ -355,7 +393,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     }
     c->stats.total = total;
     c->stats.kernel = (uint32_t)plan.family;
-    c->stats.emit_from_bits = use_masks ? 1u : 0u;
+    c->stats.emit_from_bits = emit_from_bits ? 1u : 0u;
     c->stats.timed = rq.timing ? 1u : 0u;
     *n_out = total;
     if (!rq.count_only && total > rq.cap)
@@ -394,8 +432,8 @@ int sj_create(sj_ctx **out, int device, void *stream)
     c->device = device;
     c->stream = (hipStream_t)stream;
     c->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
-    if (hipMalloc(&c->d_small, 2 * sizeof(unsigned long long)) != hipSuccess ||
-        hipHostMalloc(&c->h_small, 2 * sizeof(unsigned long long), hipHostMallocDefault) !=
+    if (hipMalloc(&c->d_small, 4 * sizeof(unsigned long long)) != hipSuccess ||
+        hipHostMalloc(&c->h_small, 4 * sizeof(unsigned long long), hipHostMallocDefault) !=
             hipSuccess) {
         (void)hipGetLastError();
         sj_destroy(c);

@@ -421,6 +421,49 @@ __global__ void __launch_bounds__(256) emit_masks(JoinArgs g, uint64_t n_blocks)
     }
 }
 
+// Second pass of count-then-emit after a MODE_RECORD first pass of the
+// resident kernel: workgroup w handles the records of first-pass workgroup w,
+// one wave per record, and writes each record's pairs at its output block's
+// offset plus the record's position, lanes by their exclusive prefix of the
+// per-lane counts, register order within a lane (the order of a MODE_EMIT
+// pass).
+__global__ void __launch_bounds__(256) emit_records(JoinArgs g)
+{
+    typedef __attribute__((address_space(1))) const MatchRecord grec;
+    typedef __attribute__((address_space(1))) const uint16_t gmask16;
+    typedef __attribute__((address_space(1))) uint64_t gpair;
+    const int lane = threadIdx.x & 63;
+    const uint32_t wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t n = min(g.rec_counts[blockIdx.x], g.rec_cap);
+    grec *list = (grec *)g.records + (uint64_t)blockIdx.x * g.rec_cap;
+    gpair *out = (gpair *)g.pairs;
+    const uint32_t half = (uint32_t)lane >> 5, c32 = (uint32_t)lane & 31;
+    for (uint32_t k = wv; k < n; k += 4) {
+        grec *rec = list + k;
+        const uint64_t blk = rec->blk;
+        const uint32_t pos = rec->pos, i0 = rec->i0, j0 = rec->j0;
+        uint32_t m = ((gmask16 *)rec->mask)[lane];
+        const uint32_t cnt = (uint32_t)__builtin_popcount(m);
+        const uint32_t excl = wave_incl_scan_u32(cnt) - cnt;
+        uint64_t slot = g.block_offsets[blk] + pos + excl;
+        const uint32_t ib = i0 + 4 * half, j = j0 + c32;
+        while (m != 0) {
+            const uint32_t r = (uint32_t)__builtin_ctz(m);
+            m &= m - 1;
+            if (slot < g.cap)
+                out[slot] = (uint64_t)(ib + 8 * (r >> 2) + (r & 3)) | ((uint64_t)j << 32);
+            ++slot;
+        }
+    }
+}
+
+hipError_t launch_emit_records(const JoinArgs &g, uint32_t n_wg, hipStream_t stream)
+{
+    if (n_wg)
+        hipLaunchKernelGGL(emit_records, dim3(n_wg), dim3(256), 0, stream, g);
+    return hipGetLastError();
+}
+
 hipError_t launch_emit_masks(const Plan &plan, const JoinArgs &g, hipStream_t stream)
 {
     if (plan.family != FAM_STREAMED)

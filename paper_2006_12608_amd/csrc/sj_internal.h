@@ -15,10 +15,26 @@ enum Mode {
     MODE_SINGLE = 0,  // append through one atomic counter per wave (single pass)
     MODE_COUNT = 1,   // count the matches of every output block, write no pairs
     MODE_EMIT = 2,    // write each block's matches at its precomputed offset
-    MODE_MASK = 3     // count as MODE_COUNT and keep every result's match bit
+    MODE_MASK = 3,    // count as MODE_COUNT and keep every result's match bit
                       // (K-streamed kernel only), for an emit pass that reads
                       // the bits instead of recomputing the product
+    MODE_RECORD = 4   // count as MODE_COUNT and append one MatchRecord per
+                      // 32x32 block with matches to the workgroup's own list
+                      // (resident kernel only), for an emit pass that reads
+                      // the records instead of recomputing
 };
+
+// The matches of one 32x32 block of results, as found by the first pass of
+// count-then-emit (MODE_RECORD): the block's output block, the number of that
+// output block's matches that precede this block's, the block's first row and
+// column, and 64 lane masks in the MFMA accumulator layout (bit r of lane l's
+// mask is row i0 + 8 (r / 4) + 4 (l / 32) + r % 4, column j0 + l % 32).
+struct MatchRecord {
+    uint64_t blk;
+    uint32_t pos, i0, j0, pad[3];
+    uint16_t mask[64];
+};
+static_assert(sizeof(MatchRecord) == 160, "record layout");
 
 // Kernel families.
 enum Family {
@@ -57,6 +73,10 @@ struct JoinArgs {
     uint32_t *block_counts;      // MODE_COUNT: one count per output block
     const unsigned long long *block_offsets;  // MODE_EMIT: exclusive prefix of block_counts
     uint16_t *masks;             // MODE_MASK: ST_MASK_WORDS per output block
+    MatchRecord *records;        // MODE_RECORD: rec_cap records per workgroup, by workgroup
+    uint32_t rec_cap;
+    uint32_t *rec_counts;        // MODE_RECORD: records found per workgroup (may pass rec_cap)
+    unsigned long long *rec_max; // MODE_RECORD: largest of rec_counts (atomic max)
     uint32_t qsplit;             // FAM_RESIDENT: Q ranges per P block
 };
 
@@ -83,6 +103,12 @@ hipError_t launch_join(const Plan &plan, int dtype, int metric, int mode, const 
 // offset in the same order as a MODE_EMIT pass (reads g.masks, g.block_counts,
 // g.block_offsets; writes g.pairs below g.cap).
 hipError_t launch_emit_masks(const Plan &plan, const JoinArgs &g, hipStream_t stream);
+
+// Second pass of count-then-emit after a MODE_RECORD first pass of the
+// resident kernel (n_wg workgroups, none with more than rec_cap records): the
+// pairs of every record, each written at its output block's offset plus its
+// position, in the order of a MODE_EMIT pass.
+hipError_t launch_emit_records(const JoinArgs &g, uint32_t n_wg, hipStream_t stream);
 
 // Squared row norms: out[i] = sum_k X[i][k]^2 (int32 for int8, fp32 otherwise).
 // Rows as in JoinArgs (16-byte aligned, row_bytes a multiple of 16).

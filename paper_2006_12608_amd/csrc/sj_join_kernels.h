@@ -266,7 +266,42 @@ struct WaveOut {
     uint32_t cap;
     uint32_t fill;   // wave-uniform
     uint64_t dst;    // emit pass: next global slot of this wave's block
+    uint64_t blk;    // MODE_RECORD: output block of the blocks being tested
+    __attribute__((address_space(3))) uint32_t *nrec;   // MODE_RECORD: workgroup's record count
 };
+
+// Modes whose first pass only counts (no pairs written).
+template <int MODE>
+constexpr bool counting_mode()
+{
+    return MODE == MODE_COUNT || MODE == MODE_RECORD;
+}
+
+// MODE_RECORD: append the block's MatchRecord to the workgroup's list (an LDS
+// counter, so no global atomics in the product loop; records past rec_cap are
+// counted, not written, and the host then recomputes instead of reading them).
+__device__ __forceinline__ void append_record(uint32_t m, uint32_t ib, uint32_t j, int lane,
+                                              uint64_t pos, const JoinArgs &g, const WaveOut &wo)
+{
+    typedef __attribute__((address_space(1))) uint16_t global_u16;
+    typedef __attribute__((address_space(1))) MatchRecord global_rec;
+    uint32_t k = 0;
+    if (lane == 0)
+        k = __hip_atomic_fetch_add(wo.nrec, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    k = __builtin_amdgcn_readfirstlane(k);
+    if (k >= g.rec_cap)
+        return;
+    global_rec *rec = (global_rec *)g.records + ((uint64_t)blockIdx.x * g.rec_cap + k);
+    ((global_u16 *)rec->mask)[lane] = (uint16_t)m;
+    const uint32_t i0 = __builtin_amdgcn_readfirstlane(ib);
+    const uint32_t j0 = __builtin_amdgcn_readfirstlane(j);
+    if (lane == 0) {
+        rec->blk = wo.blk;
+        rec->pos = (uint32_t)pos;
+        rec->i0 = i0;
+        rec->j0 = j0;
+    }
+}
 
 template <int MODE>
 __device__ __forceinline__ void flush_wave_out(WaveOut &wo, int lane, const JoinArgs &g)
@@ -380,7 +415,11 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
         tot += (uint32_t)__popcll(bits) << b;
         pre += lanes_below(bits) << b;
     }
-    if constexpr (MODE == MODE_COUNT) {
+    if constexpr (counting_mode<MODE>()) {
+        if constexpr (MODE == MODE_RECORD) {
+            if (tot != 0)
+                append_record(m, ib, j, lane, blk_run, g, wo);
+        }
         blk_run += tot;
         return;
     }
@@ -516,6 +555,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __shared__ V s_np[NEED_NORMS ? NW : 1][NEED_NORMS ? 32 * WMB : 1];
     constexpr int OUT_CAP = MODE == MODE_SINGLE ? 1024 : 1;   // a whole 32x32 block
     __shared__ uint64_t s_out[NW][OUT_CAP];
+    __shared__ uint32_t s_nrec;   // MODE_RECORD: records of this workgroup
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
@@ -597,10 +637,15 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         norm_load(t0, stn);
         norm_store(s_nq0, stn);
     }
+    if constexpr (MODE == MODE_RECORD) {
+        if (tid == 0)
+            s_nrec = 0;
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u, 0ull};
+    WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u, 0ull, 0ull,
+               (__attribute__((address_space(3))) uint32_t *)&s_nrec};
     const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
     // Bound of one wave sub-tile from its running max, then the exact path if
     // any lane may match.
@@ -685,17 +730,20 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
             if constexpr (PIPE) {
                 if constexpr (s == 0) {
                     if (have_prev) {
+                        wo.blk = blk_prev;
                         check(acc[pi], mb, j_prev, ny_prev, run_prev);
-                        if constexpr (MODE == MODE_COUNT) {
+                        if constexpr (counting_mode<MODE>()) {
                             if (lane == 0)
                                 g.block_counts[blk_prev] = (uint32_t)run_prev;
                         }
                     }
                 } else {
+                    wo.blk = blk;
                     check(acc[pi], mb, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
                 }
             } else {
                 fold_max_blk<0, NVAL, WMB>(acc[0], mb);
+                wo.blk = blk;
                 check(acc[0], mb, t * BN + 32 * s + c32, ny_sub[s], blk_run);
             }
         });
@@ -705,7 +753,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
             blk_prev = blk;
             run_prev = blk_run;
             have_prev = true;
-        } else if constexpr (MODE == MODE_COUNT) {
+        } else if constexpr (counting_mode<MODE>()) {
             if (lane == 0)
                 g.block_counts[blk] = (uint32_t)blk_run;
         }
@@ -723,8 +771,9 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
         if (have_prev) {
             V mb[WMB];
             fold_max_blk<0, NVAL, WMB>(acc[NACC - 1], mb);
+            wo.blk = blk_prev;
             check(acc[NACC - 1], mb, j_prev, ny_prev, run_prev);
-            if constexpr (MODE == MODE_COUNT) {
+            if constexpr (counting_mode<MODE>()) {
                 if (lane == 0)
                     g.block_counts[blk_prev] = (uint32_t)run_prev;
             }
@@ -732,6 +781,14 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     }
     if constexpr (MODE == MODE_SINGLE)
         flush_workgroup_out<NW>(wo, wave, lane, g);
+    if constexpr (MODE == MODE_RECORD) {
+        __syncthreads();
+        if (tid == 0) {
+            const uint32_t n = s_nrec;
+            g.rec_counts[blockIdx.x] = n;
+            atomicMax(g.rec_max, (unsigned long long)n);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1067,6 +1124,23 @@ hipError_t launch_mode(const Plan &p, const JoinArgs &g, hipStream_t st)
 template <int DT>
 hipError_t launch_dtype(const Plan &p, int metric, int mode, const JoinArgs &g, hipStream_t st)
 {
+    if (mode == MODE_RECORD) {
+        // resident kernel only
+        if (p.family != FAM_RESIDENT || (metric != MET_IP && metric != MET_L2))
+            return hipErrorInvalidValue;
+        const bool l2 = metric == MET_L2;
+        switch (p.variant) {
+        case 0: return l2 ? launch_resident_v<DT, MET_L2, MODE_RECORD, 0>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_RECORD, 0>(p, g, st);
+        case 1: return l2 ? launch_resident_v<DT, MET_L2, MODE_RECORD, 1>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_RECORD, 1>(p, g, st);
+        case 2: return l2 ? launch_resident_v<DT, MET_L2, MODE_RECORD, 2>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_RECORD, 2>(p, g, st);
+        case 3: return l2 ? launch_resident_v<DT, MET_L2, MODE_RECORD, 3>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_RECORD, 3>(p, g, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
     if (mode == MODE_MASK) {
         // K-streamed kernel only
         if (p.family != FAM_STREAMED || (metric != MET_IP && metric != MET_L2))

@@ -207,10 +207,14 @@ def test_streamed_dense_output(dtype, d):
 
 
 @pytest.mark.parametrize("dtype,d,metric", [("bf16", 300, "ip"), ("f16", 520, "l2"),
-                                             ("i8", 700, "ip"), ("i8", 530, "l2")])
+                                             ("i8", 700, "ip"), ("i8", 530, "l2"),
+                                             ("bf16", 128, "ip"), ("f16", 256, "l2"),
+                                             ("i8", 64, "l2"), ("i8", 40, "ip"),
+                                             ("f16", 72, "ip")])
 def test_two_pass_match_bits_equal_recompute(dtype, d, metric):
-    """Count-then-emit on the K-streamed kernel: the second pass that reads the
-    first pass's match bits writes the same array (same order) as the one that
+    """Count-then-emit: the second pass that reads the first pass's match bits
+    (K-streamed kernel: a bit per result; resident kernel: a record per 32x32
+    block with matches) writes the same array (same order) as the one that
     recomputes the product, over several tiles with ragged edges, and the set
     is the oracle's; a capacity one short of the total is an overflow with the
     exact total."""
@@ -231,7 +235,8 @@ def test_two_pass_match_bits_equal_recompute(dtype, d, metric):
     f = sj.join_ip if metric == "ip" else sj.join_l2
     a = f(Pd, Qd, w.threshold, two_pass=True, ctx=ctx)
     st = sj.sj_get_stats(ctx)
-    assert st.kernel == 2 and st.emit_from_bits == 1
+    row_bytes = d * (1 if dtype == "i8" else 2)
+    assert st.kernel == (2 if row_bytes > 512 else 1) and st.emit_from_bits == 1
     b = f(Pd, Qd, w.threshold, two_pass=True, recompute=True, ctx=ctx)
     assert sj.sj_get_stats(ctx).emit_from_bits == 0
     assert a.shape[0] > 0 and torch.equal(a, b)
