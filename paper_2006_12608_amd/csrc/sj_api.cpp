@@ -230,11 +230,8 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     // matches instead (its outputs are sparse next to its products).
     bool use_records = rq.two_pass && !rq.count_only && !rq.recompute &&
                        plan.family == sjk::FAM_RESIDENT;
-    // a workgroup covers n_blocks / grid output blocks of at most 32 32x32
-    // blocks each (BM x BN <= 1024 x 256 results)
     uint64_t rec_cap = kMaxRecords / plan.grid;
-    const uint64_t wg_sub = (plan.n_blocks / plan.grid + 1) * 32;
-    rec_cap = rec_cap < wg_sub ? rec_cap : wg_sub;
+    rec_cap = rec_cap < plan.wg_blocks32 ? rec_cap : plan.wg_blocks32;
     if (rec_cap == 0)
         use_records = false;
     const size_t rec_bytes = align_up((size_t)rec_cap * plan.grid * sizeof(sjk::MatchRecord)) +

@@ -62,6 +62,8 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
             return false;
         plan->grid = (uint32_t)grid;
         plan->n_blocks = n_pb * kResNW * n_qt;
+        // a workgroup sweeps at most ceil(n_qt / qsplit) tiles of bm x bn results
+        plan->wg_blocks32 = ((n_qt + qsplit - 1) / qsplit) * (bm / 32) * (bn / 32);
         return true;
     }
     const uint64_t n_pt = (n_p + (uint64_t)kStBM - 1) / kStBM;
@@ -76,6 +78,7 @@ bool plan_join(int dtype, int metric, uint32_t n_p, uint32_t n_q, uint32_t row_b
     plan->block = kStNW * 64;
     plan->grid = (uint32_t)grid;
     plan->n_blocks = n_pt * n_qt * kStNW;
+    plan->wg_blocks32 = 0;
     return true;
 }
 

@@ -88,6 +88,7 @@ struct Plan {
     uint32_t grid, block;
     uint32_t qsplit;
     uint64_t n_blocks;           // number of output blocks (entries of block_counts)
+    uint64_t wg_blocks32;        // FAM_RESIDENT: most 32x32 result blocks of one workgroup
 };
 
 // Chooses the kernel for (dtype, metric, shape) on a GPU with `num_cus` CUs.

@@ -251,6 +251,29 @@ def test_two_pass_match_bits_equal_recompute(dtype, d, metric):
     assert e.value.status == sj.SJ_E_OVERFLOW and e.value.n_out == total
 
 
+@pytest.mark.parametrize("dtype,d", [("i8", 64), ("bf16", 96)])
+def test_two_pass_records_every_pair(dtype, d):
+    """Resident kernel, count-then-emit with every pair matching: every 32x32
+    block has a record (the workgroup that sweeps two of the three Q tiles
+    holds the most), and the output is every pair, in the same order as the
+    recomputing second pass."""
+    import torch
+    import paper_2006_12608_amd as sj
+    w = workloads.random_case(23, 300, 768, d, dtype, lo=-3, hi=3)
+    Pd, Qd = to_device(w.P, dtype), to_device(w.Q, dtype)
+    say("records, every pair", dtype, d)
+    ctx = sj.context(0)
+    a = sj.join_ip(Pd, Qd, -np.inf, two_pass=True, ctx=ctx)
+    st = sj.sj_get_stats(ctx)
+    assert st.kernel == 1 and st.emit_from_bits == 1
+    b = sj.join_ip(Pd, Qd, -np.inf, two_pass=True, recompute=True, ctx=ctx)
+    assert torch.equal(a, b)
+    allp = sorted_pairs(a)
+    assert allp.shape[0] == 300 * 768
+    assert np.array_equal(allp[:, 0], np.repeat(np.arange(300), 768))
+    assert np.array_equal(allp[:, 1], np.tile(np.arange(768), 300))
+
+
 def test_ties_are_inclusive():
     """Rows with known exact scores at the threshold are reported; one above is not."""
     rng = np.random.default_rng(5)
