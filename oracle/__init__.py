@@ -10,5 +10,7 @@ from .oracle import (  # noqa: F401
     count,
     scores,
     max_threads,
+    lsh_keys,
+    lsh_join,
     JoinResult,
 )

@@ -54,6 +54,11 @@ def load(path: str | None = None):
     lib.or_count.restype = i64
     lib.or_scores.argtypes = [i32, i32, vp, vp, i64, vp, i64, vp]
     lib.or_scores.restype = None
+    lib.or_lsh_keys.argtypes = [i32, vp, i64, i64, i64, i64, vp, vp, i32, vp]
+    lib.or_lsh_keys.restype = i32
+    lib.or_lsh_join.argtypes = [i32, i32, vp, i64, vp, i64, i64, dbl, i64, i64, vp, vp, i32, vp,
+                                i64, i32]
+    lib.or_lsh_join.restype = i64
     lib.or_max_threads.argtypes = []
     lib.or_max_threads.restype = i32
     if path is None:
@@ -152,3 +157,51 @@ def scores(metric: str, dtype: str, P: np.ndarray, Q: np.ndarray, pairs, lib=Non
 def max_threads(lib=None) -> int:
     lib = lib or load()
     return int(lib.or_max_threads())
+
+
+def _lsh_check(L: int, k: int, A: np.ndarray, B, w: int, d: int):
+    if A.dtype != np.int8 or A.shape != (L * k, d) or not A.flags.c_contiguous:
+        raise ValueError(f"A must be a C-contiguous ({L * k}, {d}) int8 array")
+    B = np.zeros(L * k, np.int32) if B is None else np.ascontiguousarray(B, dtype=np.int32)
+    if B.shape != (L * k,):
+        raise ValueError(f"B must hold {L * k} int32 offsets")
+    return B
+
+
+def lsh_keys(dtype: str, X: np.ndarray, L: int, k: int, A: np.ndarray, B=None, w: int = 0,
+             lib=None) -> np.ndarray:
+    """(L, n) uint64 bucket keys of the rows of X (see or_lsh_keys in sj_oracle.c:
+    L tables of k concatenated random-projection hashes, Section 4's LSH
+    join; w == 0 sign hashes, w > 0 quantised projections with offsets B)."""
+    lib = lib or load()
+    _check(X, X, dtype)
+    B = _lsh_check(L, k, A, B, w, X.shape[1])
+    out = np.zeros((max(L, 1), max(X.shape[0], 1)), np.uint64)
+    keys = np.zeros(L * X.shape[0] + 1, np.uint64)
+    st = lib.or_lsh_keys(_DT[dtype], _ptr(X), X.shape[0], X.shape[1], L, k, _ptr(A), _ptr(B),
+                         int(w), _ptr(keys))
+    if st != 0:
+        raise RuntimeError(f"oracle lsh_keys failed ({st})")
+    out = keys[:L * X.shape[0]].reshape(L, X.shape[0]).copy()
+    return out
+
+
+def lsh_join(metric: str, dtype: str, P: np.ndarray, Q: np.ndarray, thr: float, L: int, k: int,
+             A: np.ndarray, B=None, w: int = 0, threads: int | None = None,
+             lib=None) -> np.ndarray:
+    """The LSH-bucketed join (Section 4): all (i, j) sharing a bucket in some
+    table that pass the exact test, as an (m, 2) uint32 array in (i, j) order."""
+    lib = lib or load()
+    _check(P, Q, dtype)
+    B = _lsh_check(L, k, A, B, w, P.shape[1])
+    cap = 1 << 16
+    while True:
+        out = np.zeros((cap, 2), np.uint32)
+        tot = lib.or_lsh_join(_MET[metric], _DT[dtype], _ptr(P), P.shape[0], _ptr(Q),
+                              Q.shape[0], P.shape[1], float(thr), L, k, _ptr(A), _ptr(B),
+                              int(w), _ptr(out), cap, threads or 0)
+        if tot < 0:
+            raise RuntimeError(f"oracle lsh_join failed ({tot})")
+        if tot <= cap:
+            return out[:tot].copy()
+        cap = int(tot)

@@ -285,3 +285,112 @@ int or_max_threads(void)
     return 1;
 #endif
 }
+
+/*
+ * LSH-bucketed join (Section 4, the LSH method behind Theorem 3): points of
+ * P and Q are hashed into buckets by L independent hash tables, each table's
+ * hash being the concatenation of k functions from an LSH family, and a pair
+ * is reported when its points share a bucket in at least one table and the
+ * pair passes the exact distance test.  The oracle computes that set by its
+ * definition: for every pair (i, j), the keys of every table are compared and
+ * the exact test is applied; no bucketing, no sorting.
+ *
+ * The random draws of the LSH are inputs: A holds L*k rows of d int8 entries
+ * (function f = t*k + u of table t is row f), B holds L*k int32 offsets, w is
+ * the bucket width.  With the projection z_f(x) = sum_m A[f][m] * x_m, in
+ * double and in ascending m (every product is exact, so this is the same
+ * number for every evaluation in that order):
+ *   w == 0 (random-hyperplane signs, for inner product / cosine):
+ *       v_f(x) = 1 if z_f(x) >= 0 else 0
+ *   w  > 0 (quantised projections, for squared Euclidean distance):
+ *       v_f(x) = floor((z_f(x) + B[f]) / w)
+ * The key of table t concatenates its k values, each reduced to its low
+ * beta = floor(64 / k) bits (two's complement): key_t(x) = sum_u
+ * (v_{tk+u}(x) mod 2^beta) * 2^(beta u); with k == 0 every key is 0 (one
+ * bucket).  Keys are written table-major: keys[t * n + i].
+ */
+int or_lsh_keys(int dtype, const void *X, int64_t n, int64_t d, int64_t L, int64_t k,
+                const int8_t *A, const int32_t *B, int32_t w, uint64_t *keys)
+{
+    if (n < 0 || d < 0 || L < 0 || k < 0 || k > 64 || w < 0)
+        return -1;
+    if (dtype != OR_F16 && dtype != OR_BF16 && dtype != OR_I8)
+        return -1;
+    const int beta = k > 0 ? (int)(64 / k) : 64;
+    const uint64_t low = beta >= 64 ? ~(uint64_t)0 : (((uint64_t)1 << beta) - 1);
+    for (int64_t t = 0; t < L; ++t)
+        for (int64_t i = 0; i < n; ++i) {
+            uint64_t key = 0;
+            for (int64_t u = 0; u < k; ++u) {
+                const int64_t f = t * k + u;
+                double z = 0.0;
+                for (int64_t m = 0; m < d; ++m)
+                    z += (double)A[f * d + m] * elem(dtype, X, i * d + m);
+                int64_t v;
+                if (w == 0)
+                    v = z >= 0.0 ? 1 : 0;
+                else
+                    v = (int64_t)floor((z + (double)B[f]) / (double)w);
+                key |= ((uint64_t)v & low) << (beta * u);
+            }
+            keys[t * n + i] = key;
+        }
+    return 0;
+}
+
+/*
+ * The LSH-bucketed join: every (i, j) such that key_t(P_i) == key_t(Q_j) for
+ * some table t and the pair passes the exact test of `metric` (as or_join).
+ * Pairs are written in lexicographic (i, j) order, at most `cap`; returns the
+ * total (which may exceed cap), -1 on bad arguments, -2 when out of memory.
+ */
+int64_t or_lsh_join(int metric, int dtype, const void *P, int64_t n_p, const void *Q,
+                    int64_t n_q, int64_t d, double thr, int64_t L, int64_t k, const int8_t *A,
+                    const int32_t *B, int32_t w, uint32_t *out_pairs, int64_t cap, int threads)
+{
+    if (n_p < 0 || n_q < 0 || d < 0 || L < 0 || (metric != OR_IP && metric != OR_L2))
+        return -1;
+    uint64_t *kp = (uint64_t *)malloc((size_t)(L * n_p + 1) * sizeof(uint64_t));
+    uint64_t *kq = (uint64_t *)malloc((size_t)(L * n_q + 1) * sizeof(uint64_t));
+    row_out *ro = (row_out *)calloc((size_t)(n_p ? n_p : 1), sizeof(row_out));
+    int failed = !kp || !kq || !ro;
+    if (!failed && (or_lsh_keys(dtype, P, n_p, d, L, k, A, B, w, kp) != 0 ||
+                    or_lsh_keys(dtype, Q, n_q, d, L, k, A, B, w, kq) != 0)) {
+        free(kp);
+        free(kq);
+        free(ro);
+        return -1;
+    }
+    if (!failed) {
+#ifdef _OPENMP
+        int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
+#endif
+        for (int64_t i = 0; i < n_p; ++i)
+            for (int64_t j = 0; j < n_q; ++j) {
+                int collide = 0;
+                for (int64_t t = 0; t < L && !collide; ++t)
+                    collide = kp[t * n_p + i] == kq[t * n_q + j];
+                if (!collide)
+                    continue;
+                double sc = metric == OR_IP ? or_score_ip(dtype, P, i, Q, j, d)
+                                            : or_score_l2(dtype, P, i, Q, j, d);
+                if (matches(metric, sc, thr) &&
+                    push_u32(&ro[i].pairs, &ro[i].n, &ro[i].cap, (uint32_t)j))
+                    failed = 1;
+            }
+    }
+    int64_t total = 0;
+    for (int64_t i = 0; ro && i < n_p; ++i) {
+        for (int64_t t = 0; t < ro[i].n; ++t, ++total)
+            if (total < cap) {
+                out_pairs[2 * total] = (uint32_t)i;
+                out_pairs[2 * total + 1] = ro[i].pairs[t];
+            }
+        free(ro[i].pairs);
+    }
+    free(ro);
+    free(kp);
+    free(kq);
+    return failed ? -2 : total;
+}

@@ -20,6 +20,7 @@ independently of the oracle's own decoder.
 from __future__ import annotations
 
 import math
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -417,6 +418,162 @@ def pin_band_report(lib):
     want = mask_to_pairs(np.abs(S - 12) <= 2)
     assert np.array_equal(r.band_pairs.astype(np.int64), want)
     assert np.array_equal(r.band_match, S[want[:, 0], want[:, 1]] >= 12)
+
+
+
+
+# ------------------------------------------------- LSH-bucketed join (Thm 3)
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden_lsh():
+    rows = {}
+    for line in open(os.path.join(GOLDEN, "lsh_keys_small.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            name, rest = line.split(None, 1)
+            rows[name] = [[int(v) for v in part.split()] for part in rest.split(";")]
+    return rows
+
+
+def pin_lsh_keys_worked_example(lib):
+    """Keys of a hand-worked example (tests/golden/lsh_keys_small.txt): the
+    inclusive sign at z = 0, floor of negative quotients, two's-complement
+    truncation, the bit position of each function and the table-major layout."""
+    g = _golden_lsh()
+    X = np.array(g["points"], np.int8)
+    A = np.array(g["A"], np.int8)
+    B = np.array(g["B"][0], np.int32)
+    ks = oracle.lsh_keys("i8", X, 2, 2, A, B, 0, lib=lib)
+    assert ks.tolist() == [[v for v in r] for r in g["sign"]], ks
+    kq = oracle.lsh_keys("i8", X, 2, 2, A, B, 4, lib=lib)
+    assert kq.tolist() == [[v for v in r] for r in g["quant4"]], kq
+    # the same points stored as fp16 and bf16 give the same keys
+    for dt in ("f16", "bf16"):
+        Xf = encode(X.astype(np.float64), dt)
+        assert np.array_equal(oracle.lsh_keys(dt, Xf, 2, 2, A, B, 0, lib=lib), ks)
+        assert np.array_equal(oracle.lsh_keys(dt, Xf, 2, 2, A, B, 4, lib=lib), kq)
+
+
+def pin_lsh_one_hot_keys(lib):
+    """On scaled one-hot rows c e_m the projection is c A[f][m], so each key
+    bit is the sign of a single known entry (pins the A index mapping)."""
+    rng = np.random.default_rng(31)
+    d, L, k = 9, 3, 5
+    A = rng.integers(-20, 21, size=(L * k, d)).astype(np.int8)
+    A[A == 0] = 1
+    X = np.zeros((2 * d, d), np.int8)
+    for m in range(d):
+        X[m, m] = 3
+        X[d + m, m] = -2
+    keys = oracle.lsh_keys("i8", X, L, k, A, None, 0, lib=lib)
+    for t in range(L):
+        for r in range(2 * d):
+            m, c = (r, 3) if r < d else (r - d, -2)
+            want = sum(int(c * int(A[t * k + u, m]) >= 0) << (12 * u) for u in range(k))
+            assert int(keys[t, r]) == want
+
+
+def pin_lsh_one_bucket_is_exact_join(lib):
+    """k = 0 (or all-zero projections) puts every point in one bucket: the
+    LSH join is then the exact join."""
+    rng = np.random.default_rng(32)
+    for dtype, metric, thr in (("i8", "ip", 10.0), ("bf16", "ip", 6.0), ("f16", "l2", 60.0)):
+        P = rand_int(rng, 37, 11, -4, 4, dtype)
+        Q = rand_int(rng, 29, 11, -4, 4, dtype)
+        x, y = values(dtype, P), values(dtype, Q)
+        want = mask_to_pairs(x @ y.T >= thr) if metric == "ip" else \
+            mask_to_pairs(((x[:, None, :] - y[None]) ** 2).sum(-1) <= thr)
+        got0 = oracle.lsh_join(metric, dtype, P, Q, thr, 3, 0, np.zeros((0, 11), np.int8),
+                               lib=lib)
+        assert pairset(got0) == pairset(want)
+        gotz = oracle.lsh_join(metric, dtype, P, Q, thr, 2, 4, np.zeros((8, 11), np.int8),
+                               lib=lib)
+        assert pairset(gotz) == pairset(want)
+
+
+def pin_lsh_subset_union_and_planted(lib):
+    """For any draws: the LSH join is the exact join restricted to pairs that
+    share a bucket in some table, so it is a subset of the exact join, equals
+    the union of its single-table joins, and contains every pair of identical
+    rows that matches."""
+    rng = np.random.default_rng(33)
+    d, L, k = 16, 4, 3
+    P = rand_int(rng, 60, d, -6, 6, "i8")
+    Q = rand_int(rng, 50, d, -6, 6, "i8")
+    Q[:10] = P[5:15]
+    A = rng.integers(-30, 31, size=(L * k, d)).astype(np.int8)
+    B = rng.integers(0, 40, size=L * k).astype(np.int32)
+    for metric, thr, w in (("ip", 25.0, 0), ("l2", 500.0, 40)):
+        exact = pairset(oracle.join(metric, "i8", P, Q, thr, lib=lib).pairs)
+        got = pairset(oracle.lsh_join(metric, "i8", P, Q, thr, L, k, A, B, w, lib=lib))
+        assert got <= exact and 0 < len(got) < len(exact)
+        union = set()
+        for t in range(L):
+            union |= pairset(oracle.lsh_join(metric, "i8", P, Q, thr, 1, k,
+                                             A[t * k:(t + 1) * k].copy(), B[t * k:(t + 1) * k],
+                                             w, lib=lib))
+        assert union == got
+        for q in range(10):
+            if (q + 5, q) in exact:
+                assert (q + 5, q) in got
+        # colliding pairs are exactly those with equal keys in some table
+        kp = oracle.lsh_keys("i8", P, L, k, A, B, w, lib=lib)
+        kq = oracle.lsh_keys("i8", Q, L, k, A, B, w, lib=lib)
+        coll = (kp[:, :, None] == kq[:, None, :]).any(0)
+        assert got == {p for p in exact if coll[p]}
+
+
+def pin_lsh_sign_collision_probability(lib):
+    """Random-hyperplane signs collide with probability 1 - theta / pi for
+    points at angle theta (Charikar's SimHash, the classical LSH for angular
+    distance).  Near-Gaussian integer projections (sd 32) on fp16 pairs at
+    theta = pi / 3 and pi / 2: the empirical rate over 40 000 functions x 8
+    pairs is within 0.012 of the law."""
+    rng = np.random.default_rng(34)
+    d, nf = 48, 40_000
+    A = np.clip(np.rint(rng.standard_normal((nf, d)) * 32), -127, 127).astype(np.int8)
+    for theta in (np.pi / 3, np.pi / 2):
+        u = rng.standard_normal((8, d))
+        u /= np.linalg.norm(u, axis=1, keepdims=True)
+        v = rng.standard_normal((8, d))
+        v -= (v * u).sum(1, keepdims=True) * u
+        v /= np.linalg.norm(v, axis=1, keepdims=True)
+        y = np.cos(theta) * u + np.sin(theta) * v
+        Xp, Xq = encode(u, "f16"), encode(y, "f16")
+        kp = oracle.lsh_keys("f16", Xp, nf, 1, A, None, 0, lib=lib)
+        kq = oracle.lsh_keys("f16", Xq, nf, 1, A, None, 0, lib=lib)
+        up, yq = Xp.astype(np.float64), Xq.astype(np.float64)
+        th = np.arccos((up * yq).sum(1) / np.linalg.norm(up, axis=1) / np.linalg.norm(yq, axis=1))
+        rate = (kp == kq).mean()
+        assert abs(rate - (1 - th / np.pi).mean()) < 0.012, (theta, rate)
+
+
+def pin_lsh_quantised_collision_probability(lib):
+    """Quantised Gaussian projections with uniform offsets (the p-stable LSH of
+    Datar et al. for Euclidean distance) collide with probability
+    p(c) = 1 - 2 Phi(-w / c) - 2 c / (sqrt(2 pi) w) (1 - exp(-w^2 / (2 c^2)))
+    when the projected difference has standard deviation c.  Here c = 32 times
+    the pair's distance; over 40 000 functions the rate is within 0.012."""
+    rng = np.random.default_rng(35)
+    d, nf = 32, 40_000
+    A = np.clip(np.rint(rng.standard_normal((nf, d)) * 32), -127, 127).astype(np.int8)
+    for w, delta_norm2 in ((256, 8), (512, 32)):
+        x = rng.integers(-10, 11, size=(6, d))
+        y = x.copy()
+        for r in range(6):   # move delta_norm2 coordinates by one
+            idx = rng.choice(d, size=delta_norm2, replace=False)
+            y[r, idx] += 1
+        B = rng.integers(0, w, size=nf).astype(np.int32)
+        Xp, Xq = encode(x, "i8"), encode(y, "i8")
+        kp = oracle.lsh_keys("i8", Xp, nf, 1, A, B, w, lib=lib)
+        kq = oracle.lsh_keys("i8", Xq, nf, 1, A, B, w, lib=lib)
+        c = 32.0 * math.sqrt(delta_norm2)
+        phi = 0.5 * math.erfc((w / c) / math.sqrt(2))
+        p = 1 - 2 * phi - 2 * c / (math.sqrt(2 * math.pi) * w) * (1 - math.exp(-w * w / (2 * c * c)))
+        rate = (kp == kq).mean()
+        assert abs(rate - p) < 0.012, (w, delta_norm2, rate, p)
 
 
 PINS = {name[4:]: fn for name, fn in sorted(globals().items()) if name.startswith("pin_")}

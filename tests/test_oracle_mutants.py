@@ -49,11 +49,23 @@ MUTANTS = {
                           "        row_out *o",
                           "    for (int64_t r = 0; r < n_rows - 1; ++r) {\n"
                           "        int64_t i = rows ? rows[r] : r;\n        row_out *o")],
+    # LSH-bucketed join
+    "lsh_sign_strict": [("v = z >= 0.0 ? 1 : 0;", "v = z > 0.0 ? 1 : 0;")],
+    "lsh_truncates_quotient": [("(int64_t)floor((z + (double)B[f]) / (double)w)",
+                                "(int64_t)((z + (double)B[f]) / (double)w)")],
+    "lsh_drops_offset": [("floor((z + (double)B[f]) / (double)w)", "floor(z / (double)w)")],
+    "lsh_key_order_reversed": [("<< (beta * u)", "<< (beta * (k - 1 - u))")],
+    "lsh_a_transposed": [("(double)A[f * d + m]", "(double)A[m * (L * k) + f]")],
+    "lsh_skips_last_table": [("for (int64_t t = 0; t < L && !collide; ++t)",
+                              "for (int64_t t = 0; t + 1 < L && !collide; ++t)")],
+    "lsh_no_exact_test": [("if (matches(metric, sc, thr) &&\n                    push_u32(&ro[i]",
+                           "if (push_u32(&ro[i]")],
 }
 
 
 SLOW_PINS = {"decode_bf16_exhaustive", "real_scores_within_summation_bound",
-             "hypercube_ip_counts"}
+             "hypercube_ip_counts", "lsh_sign_collision_probability",
+             "lsh_quantised_collision_probability"}
 
 
 @pytest.fixture(scope="module")

@@ -16,4 +16,6 @@ from .gen import (  # noqa: F401
     DTYPES,
     ESIZE,
     to_torch,
+    LshParams,
+    lsh_params,
 )

@@ -284,3 +284,26 @@ def to_torch(X: np.ndarray, dtype: str, device="cuda"):
     else:
         raise ValueError(dtype)
     return t.to(device)
+
+
+@dataclass
+class LshParams:
+    """The random draws of an LSH-bucketed join: L tables of k concatenated
+    functions, projection rows A ((L*k, d) int8, function t*k + u of table t
+    is row t*k + u), offsets B ((L*k,) int32) and bucket width w (0: sign
+    hashes, > 0: quantised projections)."""
+    L: int
+    k: int
+    A: np.ndarray
+    B: np.ndarray
+    w: int
+
+
+def lsh_params(seed: int, L: int, k: int, d: int, w: int = 0, sigma: float = 32.0) -> LshParams:
+    """Projection entries are N(0, sigma^2) draws rounded to integers and
+    clipped to [-127, 127]; offsets are uniform integers in [0, w) (zero for
+    sign hashes)."""
+    rng = np.random.default_rng(seed)
+    A = np.clip(np.rint(rng.standard_normal((L * k, d)) * sigma), -127, 127).astype(np.int8)
+    B = (rng.integers(0, w, size=L * k) if w > 0 else np.zeros(L * k)).astype(np.int32)
+    return LshParams(int(L), int(k), np.ascontiguousarray(A), B, int(w))
