@@ -103,7 +103,8 @@ typedef struct sj_stats {
     double ms_count;       /* two-pass / count: the counting pass              */
     double ms_scan;        /* two-pass / count: the scan of the block counts   */
     double ms_emit;        /* two-pass: the emitting pass                      */
-    uint32_t kernel;       /* 1 = P rows resident in registers, 2 = K-streamed */
+    uint32_t kernel;       /* 1 = P rows resident in registers, 2 = K-streamed,
+                              3 = LSH bucket join (sj_join_lsh)              */
     uint32_t timed;        /* 1 when the ms_* fields were measured             */
     uint32_t emit_from_bits; /* two-pass: 1 when the second pass read the first
                                 pass's match bits (or match records) instead
@@ -137,6 +138,40 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
  * counting pass and the scan of the count-then-emit protocol. */
 int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
              uint32_t n_q, uint32_t d, double threshold, uint64_t *count);
+
+/* LSH-bucketed join (Section 4, the LSH method of Theorem 3): instead of all
+ * n_p x n_q pairs, only pairs whose points share a bucket of some hash table
+ * are evaluated.  There are L tables; table t hashes a point x with the
+ * concatenation of k functions f = t*k + u (u < k), each a random projection
+ * z_f(x) = sum_m A[f][m] x_m:
+ *   w == 0: v_f(x) = 1 if z_f(x) >= 0 else 0   (random-hyperplane signs, the
+ *           LSH for angular distance: use with SJ_IP on unit rows, i.e. cosine)
+ *   w  > 0: v_f(x) = floor((z_f(x) + B[f]) / w) (quantised projections with
+ *           offsets, the p-stable LSH for Euclidean distance: use with SJ_L2)
+ * and the bucket of x in table t is the tuple of its k values, each reduced to
+ * its low floor(64 / k) bits (two's complement).  z_f is evaluated exactly for
+ * integer-valued inputs, and in double precision in ascending m otherwise.
+ * The result is every pair (i, j) whose points P_i and Q_j share a bucket in at
+ * least one table and pass the exact test of `metric` (SJ_IP: <P_i, Q_j> >= thr,
+ * SJ_L2: ||P_i - Q_j||^2 <= thr, with the arithmetic and threshold rounding
+ * of sj_join_ip / sj_join_l2): a subset of the exact join, each pair
+ * reported once (by the first table in which it collides), in unspecified
+ * order.  The random draws are the caller's:
+ *   A  device, L*k rows of d int8 entries (row-major, row t*k + u);
+ *   B  device, L*k int32 offsets (read only when w > 0; may be NULL when w == 0);
+ *   w  bucket width (0 = sign hashes).
+ * Afterwards sj_get_stats reports kernel = 3, ms_norms = repacking, norms and
+ * hashing, ms_scan = the per-table sorts and the bucket pairing, ms_join = the
+ * bucket join.
+ * Limits: 1 <= L <= 64, 0 <= k <= 64 (k = 0: one bucket per table, the exact
+ * join), L * max(n_p, n_q) < 2^26; other arguments, outputs and errors as
+ * sj_join_ip.  *n_cand (host, may be NULL) receives the number of pair
+ * evaluations made (the sum over tables and shared buckets of |P bucket| x
+ * |Q bucket|).  Device scratch grows to about L * (n_p + n_q) * 40 bytes. */
+int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
+                uint32_t n_q, uint32_t d, double thr, uint32_t L, uint32_t k, const int8_t *A,
+                const int32_t *B, int32_t w, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+                uint64_t *n_cand);
 
 /* Free the context and its scratch; NULL is a no-op. */
 void sj_destroy(sj_ctx *ctx);

@@ -2,9 +2,10 @@
 Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
 
 The raw C-ABI entry points are exposed under their C names (sj_create,
-sj_join_ip, sj_join_l2, sj_count, sj_destroy, sj_get_stats, sj_last_error)
-with plain integer pointers; `join_ip`, `join_l2` and `count` are
-conveniences over PyTorch device tensors.  This module only marshals
+sj_join_ip, sj_join_l2, sj_count, sj_join_lsh, sj_destroy, sj_get_stats,
+sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
+`join_lsh` (the LSH-bucketed join of Theorem 3) are conveniences over PyTorch
+device tensors.  This module only marshals
 arguments: every step of the join runs in the library's HIP kernels.  Import
 fails when libsj.so has not been built (python paper_2006_12608_amd/build.py).
 """
@@ -56,6 +57,10 @@ def _load():
     lib.sj_join_l2.restype = i32
     lib.sj_count.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, ctypes.POINTER(u64)]
     lib.sj_count.restype = i32
+    lib.sj_join_lsh.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, u32, u32, vp, vp,
+                                ctypes.c_int32, vp, u64, ctypes.POINTER(u64),
+                                ctypes.POINTER(u64)]
+    lib.sj_join_lsh.restype = i32
     lib.sj_destroy.argtypes = [vp]
     lib.sj_destroy.restype = None
     lib.sj_get_stats.argtypes = [vp, ctypes.POINTER(sj_stats)]
@@ -108,6 +113,15 @@ def sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, threshold):
     n = ctypes.c_uint64(0)
     st = lib.sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, float(threshold), ctypes.byref(n))
     return st, n.value
+
+
+def sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, L, k, A, B, w, pairs, cap):
+    """Returns (status, n_out, n_cand); pointers are integers (device addresses)."""
+    n = ctypes.c_uint64(0)
+    nc = ctypes.c_uint64(0)
+    st = lib.sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, float(thr), L, k, A, B, int(w),
+                         pairs, cap, ctypes.byref(n), ctypes.byref(nc))
+    return st, n.value, nc.value
 
 
 def sj_get_stats(ctx) -> sj_stats:
@@ -202,3 +216,41 @@ def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool = False,
             timing: bool = False, ctx=None, out=None, recompute: bool = False):
     """All (i, j) with ||P_i - Q_j||^2 <= r2 (see join_ip)."""
     return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out, recompute)
+
+
+def join_lsh(P, Q, thr: float, metric: str = "ip", *, L: int, k: int, A, B=None, w: int = 0,
+             cap: int | None = None, ctx=None, out=None):
+    """LSH-bucketed join (sj_join_lsh): the pairs that share a bucket in one
+    of L tables (k concatenated random projections each: signs when w == 0,
+    quantised with offsets B when w > 0) and pass the exact test of `metric`.
+    A is an (L*k, d) int8 device tensor, B an (L*k,) int32 device tensor (or
+    None for sign hashes).  With cap=None a first call sizes the output.
+    Returns (pairs as an (n, 2) int32 tensor of uint32 indices, number of pair
+    evaluations made)."""
+    import torch
+    _check_pair(P, Q)
+    if A.dtype != torch.int8 or not A.is_cuda or not A.is_contiguous() or \
+            tuple(A.shape) != (L * k, P.shape[1]):
+        raise ValueError(f"A must be a contiguous ({L * k}, {P.shape[1]}) int8 device tensor")
+    if B is not None and (B.dtype != torch.int32 or not B.is_cuda or not B.is_contiguous()
+                          or B.numel() != L * k):
+        raise ValueError(f"B must be a contiguous ({L * k},) int32 device tensor")
+    ctx = ctx or context(P.device.index)
+    m = SJ_IP if metric == "ip" else SJ_L2
+    args = (ctx, m, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0],
+            P.shape[1], thr, L, k, A.data_ptr() if A.numel() else None,
+            None if B is None else B.data_ptr(), w)
+    if out is None:
+        if cap is None:
+            st, n, _ = sj_join_lsh(*args, None, 0)
+            if st not in (SJ_OK, SJ_E_OVERFLOW):
+                raise SjError(st, sj_last_error(), n)
+            cap = n
+        out = torch.empty((max(int(cap), 1), 2), dtype=torch.int32, device=P.device)
+        cap = int(cap)
+    else:
+        cap = out.shape[0] if cap is None else int(cap)
+    st, n, nc = sj_join_lsh(*args, out.data_ptr() if cap else None, cap)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error(), n)
+    return out[:n], nc

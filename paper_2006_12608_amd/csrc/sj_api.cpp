@@ -12,22 +12,10 @@
 #include <cstring>
 #include <string>
 
+#include "sj_host.h"
 #include "sj_internal.h"
 
-struct sj_ctx {
-    int device = 0;
-    hipStream_t stream = nullptr;
-    int num_cus = 256;
-    unsigned long long *d_small = nullptr;  // [0] match counter, [1] scan total,
-                                            // [2] largest per-workgroup record count
-    unsigned long long *h_small = nullptr;  // pinned host copy of d_small
-    void *scratch = nullptr;
-    size_t scratch_bytes = 0;
-    hipEvent_t ev[6] = {};
-    sj_stats stats = {};
-};
-
-namespace {
+namespace sjh {
 
 thread_local std::string g_err;
 
@@ -47,17 +35,8 @@ int hip_fail(hipError_t e, const char *what)
     return fail(SJ_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-#define SJ_HIP(call)                                \
-    do {                                            \
-        hipError_t e_ = (call);                     \
-        if (e_ != hipSuccess)                       \
-            return hip_fail(e_, #call);             \
-    } while (0)
-
 size_t esize(int dtype) { return dtype == SJ_I8 ? 1 : 2; }
 
-// `p` must be device memory of the context's GPU holding at least `bytes`
-// bytes from p on (checked against its allocation's range).
 int check_device_ptr(const sj_ctx *c, const void *p, size_t bytes, const char *name)
 {
     if (bytes == 0)
@@ -138,8 +117,6 @@ int grow_scratch(sj_ctx *c, size_t bytes)
     return SJ_OK;
 }
 
-size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
-
 double elapsed_ms(hipEvent_t a, hipEvent_t b)
 {
     float ms = 0.f;
@@ -149,6 +126,12 @@ double elapsed_ms(hipEvent_t a, hipEvent_t b)
     }
     return ms;
 }
+
+}  // namespace sjh
+
+namespace {
+
+using namespace sjh;
 
 struct Request {
     int metric, dtype;

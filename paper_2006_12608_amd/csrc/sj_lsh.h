@@ -1,0 +1,76 @@
+// sj_lsh.h -- interface between the LSH-bucketed join's host code (sj_lsh_api.cpp)
+// and its gfx950 kernels (sj_lsh.hip).  Not part of the public C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sjl {
+
+// Rows of one operand as the kernels read them: n rows of row_bytes bytes
+// (a multiple of 16, 16-byte aligned, zero beyond the d stored elements).
+struct Rows {
+    const uint8_t *X;
+    uint32_t n, row_bytes;
+};
+
+// Bucket keys of every row in every table, table-major: keys[t * n + i].
+// Sign hashes (w == 0) are stored compressed, bit u = v_{t k + u}; quantised
+// hashes (w > 0) as the concatenation of their values' low floor(64 / k) bits.
+// Either way two rows share a bucket exactly when their keys are equal.
+// `key_bits` receives the number of low bits a key can occupy.
+hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
+                       const int8_t *A, const int32_t *B, int32_t w, uint64_t *keys,
+                       hipStream_t s);
+uint32_t key_bits(uint32_t k, int32_t w);
+
+// Sorts each table's keys with the row indices as values (n rows per table):
+// sorted[t * n + p], perm[t * n + p] = the p-th smallest key of table t and its
+// row.  `temp` must hold sort_temp_bytes(n) bytes.
+size_t sort_temp_bytes(uint32_t n, uint32_t bits);
+hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
+                       uint32_t n, uint32_t L, uint32_t bits, void *temp, size_t temp_bytes,
+                       hipStream_t s);
+
+// Tile edge of the bucket join (rows of P and of Q per workgroup tile).
+constexpr uint32_t TILE = 64;
+// Low bits of the packed bucket-pair counter that hold the running tile count.
+constexpr int TILE_BITS = 38;
+
+// Bucket pairs: for every table and every key present in both P and Q, one
+// record (t, first sorted position in P, P rows, first sorted position in Q)
+// plus its Q rows and its first tile; records are numbered by one packed
+// atomic (slot << TILE_BITS | tiles), so first tiles increase with the slot.
+// counters[0] = packed count, [1] = tiles, [2] = pair evaluations.
+struct BucketPairs {
+    uint4 *head;          // {t, p0, np, q0}
+    uint32_t *nq;
+    unsigned long long *tile0;
+    unsigned long long *counters;
+    uint32_t cap;         // records the arrays hold
+};
+
+hipError_t launch_bucket_pairs(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
+                               uint32_t n_q, uint32_t L, const BucketPairs &bp, hipStream_t s);
+
+struct JoinArgs {
+    Rows P, Q;
+    uint32_t L;
+    const uint32_t *perm_p, *perm_q;      // L x n sorted-position -> row
+    const uint64_t *keys_p, *keys_q;      // L x n row -> key (first-table rule)
+    const uint4 *head;
+    const uint32_t *nq;
+    const unsigned long long *tile0;
+    uint32_t n_bp;
+    uint64_t n_tiles;
+    float thr_f;                          // as sjk::JoinArgs
+    int32_t thr_i;
+    const void *norm_p, *norm_q;
+    uint32_t *pairs;
+    uint64_t cap;
+    unsigned long long *counter;
+};
+
+hipError_t launch_join(int dtype, int metric, const JoinArgs &g, int num_cus, hipStream_t s);
+
+}  // namespace sjl

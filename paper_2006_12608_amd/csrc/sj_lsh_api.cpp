@@ -1,0 +1,211 @@
+// sj_lsh_api.cpp -- host side of the LSH-bucketed join (sj_join_lsh; contract in
+// include/sj.h): argument checks, scratch layout and the sequence
+// hash -> sort -> bucket pairs -> bucket join on the context's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+
+#include "sj.h"
+#include "sj_host.h"
+#include "sj_internal.h"
+#include "sj_lsh.h"
+
+using namespace sjh;
+
+namespace {
+
+// Tables and records are addressed with 32-bit positions and the packed
+// bucket-pair counter keeps 26 bits of record number.
+const uint64_t kMaxTableRows = (uint64_t)1 << (64 - sjl::TILE_BITS);
+
+}  // namespace
+
+extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint32_t n_p,
+                           const void *Q, uint32_t n_q, uint32_t d, double thr, uint32_t L,
+                           uint32_t k, const int8_t *A, const int32_t *B, int32_t w,
+                           uint32_t *pairs, uint64_t cap, uint64_t *n_out, uint64_t *n_cand)
+{
+    g_err.clear();
+    if (!c)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (!n_out)
+        return fail(SJ_E_INVAL, "result pointer is NULL");
+    *n_out = 0;
+    if (n_cand)
+        *n_cand = 0;
+    if (dtype != SJ_F16 && dtype != SJ_BF16 && dtype != SJ_I8)
+        return fail(SJ_E_INVAL, "unknown dtype %d", dtype);
+    if (metric != SJ_IP && metric != SJ_L2)
+        return fail(SJ_E_INVAL, "unknown metric %d", metric);
+    if (std::isnan(thr))
+        return fail(SJ_E_INVAL, "threshold is NaN");
+    if (L < 1 || L > 64)
+        return fail(SJ_E_INVAL, "L = %u tables: 1 <= L <= 64", L);
+    if (k > 64)
+        return fail(SJ_E_INVAL, "k = %u functions per table: k <= 64", k);
+    if (w < 0)
+        return fail(SJ_E_INVAL, "bucket width w = %d is negative", w);
+    if (d > (dtype == SJ_I8 ? 32768u : 65536u))
+        return fail(SJ_E_UNSUPPORTED, "d = %u is above the limit for this dtype", d);
+    const uint64_t n_max = n_p > n_q ? n_p : n_q;
+    if ((uint64_t)L * n_max >= kMaxTableRows)
+        return fail(SJ_E_UNSUPPORTED, "L * max(n_p, n_q) = %llu is not below 2^26",
+                    (unsigned long long)L * n_max);
+    const size_t row_bytes = (size_t)d * esize(dtype);
+    int st;
+    if ((st = check_device_ptr(c, P, (size_t)n_p * row_bytes, "P")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(c, Q, (size_t)n_q * row_bytes, "Q")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(c, A, (size_t)L * k * d, "A")) != SJ_OK)
+        return st;
+    if (w > 0 && (st = check_device_ptr(c, B, (size_t)L * k * 4, "B")) != SJ_OK)
+        return st;
+    if (cap > 0) {
+        if (cap > (uint64_t)SIZE_MAX / 8)
+            return fail(SJ_E_INVAL, "cap too large");
+        if ((st = check_device_ptr(c, pairs, (size_t)cap * 8, "pairs")) != SJ_OK)
+            return st;
+        if ((uintptr_t)pairs % 8 != 0)
+            return fail(SJ_E_INVAL, "pairs must be 8-byte aligned");
+    }
+    c->stats = sj_stats{};
+    if (n_p == 0 || n_q == 0)
+        return SJ_OK;
+
+    // Rows as the kernels read them (16-byte aligned, zero-padded to a
+    // multiple of 16 bytes; repacked when the caller's are not).
+    const bool aligned = row_bytes > 0 && row_bytes % 16 == 0 && (uintptr_t)P % 16 == 0 &&
+                         (uintptr_t)Q % 16 == 0;
+    const size_t krow = row_bytes == 0 ? 16 : (row_bytes + 15) & ~(size_t)15;
+    const bool self = P == Q && n_p == n_q;
+    const bool l2 = metric == SJ_L2;
+    const uint32_t bits = sjl::key_bits(k, w);
+    const uint64_t bp_cap = (uint64_t)L * (n_p < n_q ? n_p : n_q);
+    size_t temp_bytes = sjl::sort_temp_bytes(n_p, bits);
+    const size_t tq = sjl::sort_temp_bytes(n_q, bits);
+    temp_bytes = temp_bytes > tq ? temp_bytes : tq;
+
+    // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
+    //          [sorted Q][perm P][perm Q][iota][bucket pairs][counters][sort temp]
+    size_t need = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = need;
+        need = align_up(need + bytes);
+        return at;
+    };
+    const size_t off_rp = aligned ? 0 : take((size_t)n_p * krow);
+    const size_t off_rq = aligned || self ? off_rp : take((size_t)n_q * krow);
+    const size_t off_np = l2 ? take((size_t)n_p * 4) : 0;
+    const size_t off_nq = l2 && !self ? take((size_t)n_q * 4) : off_np;
+    const size_t off_kp = take((size_t)L * n_p * 8);
+    const size_t off_kq = self ? off_kp : take((size_t)L * n_q * 8);
+    const size_t off_sp = take((size_t)L * n_p * 8);
+    const size_t off_sq = self ? off_sp : take((size_t)L * n_q * 8);
+    const size_t off_pp = take((size_t)L * n_p * 4);
+    const size_t off_pq = self ? off_pp : take((size_t)L * n_q * 4);
+    const size_t off_iota = take((size_t)n_max * 4);
+    const size_t off_head = take((size_t)bp_cap * 16);
+    const size_t off_bnq = take((size_t)bp_cap * 4);
+    const size_t off_t0 = take((size_t)bp_cap * 8);
+    const size_t off_cnt = take(4 * 8);
+    const size_t off_temp = take(temp_bytes);
+    if ((st = grow_scratch(c, need)) != SJ_OK)
+        return st;
+    uint8_t *scr = (uint8_t *)c->scratch;
+    hipStream_t s = c->stream;
+    SJ_HIP(hipSetDevice(c->device));
+
+    sjl::Rows rp{aligned ? (const uint8_t *)P : scr + off_rp, n_p, (uint32_t)krow};
+    sjl::Rows rq{aligned ? (const uint8_t *)Q : scr + off_rq, n_q, (uint32_t)krow};
+    unsigned long long *cnt = (unsigned long long *)(scr + off_cnt);
+    SJ_HIP(hipMemsetAsync(cnt, 0, 4 * 8, s));
+    SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
+    SJ_HIP(hipEventRecord(c->ev[0], s));
+    if (!aligned) {
+        SJ_HIP(sjk::launch_repack((const uint8_t *)P, n_p, (uint32_t)row_bytes, scr + off_rp,
+                                  (uint32_t)krow, s));
+        if (!self)
+            SJ_HIP(sjk::launch_repack((const uint8_t *)Q, n_q, (uint32_t)row_bytes,
+                                      scr + off_rq, (uint32_t)krow, s));
+    }
+    if (l2) {
+        SJ_HIP(sjk::launch_norms(dtype, rp.X, n_p, rp.row_bytes, scr + off_np, s));
+        if (!self)
+            SJ_HIP(sjk::launch_norms(dtype, rq.X, n_q, rq.row_bytes, scr + off_nq, s));
+    }
+    uint64_t *keys_p = (uint64_t *)(scr + off_kp), *keys_q = (uint64_t *)(scr + off_kq);
+    SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, A, B, w, keys_p, s));
+    if (!self)
+        SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, A, B, w, keys_q, s));
+    SJ_HIP(hipEventRecord(c->ev[1], s));
+    uint64_t *sorted_p = (uint64_t *)(scr + off_sp), *sorted_q = (uint64_t *)(scr + off_sq);
+    uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
+    uint32_t *iota = (uint32_t *)(scr + off_iota);
+    SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, iota, n_p, L, bits, scr + off_temp,
+                            temp_bytes, s));
+    if (!self)
+        SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, scr + off_temp,
+                                temp_bytes, s));
+    sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
+                        (unsigned long long *)(scr + off_t0), cnt, (uint32_t)bp_cap};
+    SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));
+    SJ_HIP(hipEventRecord(c->ev[2], s));
+    SJ_HIP(hipMemcpyAsync(c->h_small + 1, cnt, 3 * 8, hipMemcpyDeviceToHost, s));
+    SJ_HIP(hipStreamSynchronize(s));
+    const uint64_t n_bp = c->h_small[1] >> sjl::TILE_BITS;
+    const uint64_t n_tiles = c->h_small[2], cand = c->h_small[3];
+    if (n_tiles >> sjl::TILE_BITS)
+        return fail(SJ_E_UNSUPPORTED, "%llu candidate tiles are more than 2^%d",
+                    (unsigned long long)n_tiles, sjl::TILE_BITS);
+
+    sjl::JoinArgs g = {};
+    g.P = rp;
+    g.Q = rq;
+    g.L = L;
+    g.perm_p = perm_p;
+    g.perm_q = perm_q;
+    g.keys_p = keys_p;
+    g.keys_q = keys_q;
+    g.head = bp.head;
+    g.nq = bp.nq;
+    g.tile0 = bp.tile0;
+    g.n_bp = (uint32_t)n_bp;
+    g.n_tiles = n_tiles;
+    if (dtype == SJ_I8) {
+        if (!l2) {
+            const double sc = std::ceil(thr);
+            g.thr_i = sc < -1073741824.0 ? -1073741824 : sc > 1073741824.0 ? 1073741824
+                                                                          : (int32_t)sc;
+        } else {
+            const double r = std::floor(thr);
+            g.thr_i = r < -1.0 ? -1 : r > 2147483647.0 ? 2147483647 : (int32_t)r;
+        }
+    } else {
+        g.thr_f = l2 ? float_at_or_below(thr) : float_at_or_above(thr);
+    }
+    g.norm_p = scr + off_np;
+    g.norm_q = scr + off_nq;
+    g.pairs = pairs;
+    g.cap = cap;
+    g.counter = c->d_small;
+    SJ_HIP(sjl::launch_join(dtype, metric, g, c->num_cus, s));
+    SJ_HIP(hipEventRecord(c->ev[3], s));
+    SJ_HIP(hipMemcpyAsync(c->h_small, c->d_small, 8, hipMemcpyDeviceToHost, s));
+    SJ_HIP(hipStreamSynchronize(s));
+    const uint64_t total = c->h_small[0];
+    c->stats.total = total;
+    c->stats.ms_norms = elapsed_ms(c->ev[0], c->ev[1]);
+    c->stats.ms_scan = elapsed_ms(c->ev[1], c->ev[2]);
+    c->stats.ms_join = elapsed_ms(c->ev[2], c->ev[3]);
+    c->stats.kernel = 3;
+    c->stats.timed = 1;
+    *n_out = total;
+    if (n_cand)
+        *n_cand = cand;
+    if (total > cap)
+        return fail(SJ_E_OVERFLOW, "%llu matches exceed the capacity of %llu pairs",
+                    (unsigned long long)total, (unsigned long long)cap);
+    return SJ_OK;
+}

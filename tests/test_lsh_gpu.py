@@ -1,0 +1,193 @@
+"""GPU LSH-bucketed join (sj_join_lsh) vs the oracle's LSH join, pair set by
+pair set, on seeded inputs and seeded LSH draws.
+
+The bucket keys are integers computed exactly (or in double precision in the
+same order) on both sides, so the candidate sets agree exactly; the exact
+test then follows the all-pairs join's rules: identical sets for
+integer-valued inputs, identical outside the boundary band for real-valued
+ones.  Cases cover both hash families, every dtype, both metrics, ragged
+sizes against the 64-row tiles, buckets spanning several tiles, unaligned
+rows, the self-join, k = 0 (the exact join), the first-table rule (no
+duplicates), the candidate count, overflow and argument errors.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_util import compare, sorted_pairs, to_device, keys
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2006_12608_amd  # noqa: F401  (fails loudly when libsj.so is missing)
+    yield
+    torch.cuda.synchronize()
+
+
+def lsh_device(h):
+    import torch
+    A = torch.from_numpy(h.A).cuda()
+    B = torch.from_numpy(h.B).cuda() if h.w > 0 else None
+    return A, B
+
+
+def expected_candidates(w, h):
+    """Sum over tables and keys of (#P rows with the key) x (#Q rows with it),
+    from the oracle's keys."""
+    kp = oracle.lsh_keys(w.dtype, w.P, h.L, h.k, h.A, h.B, h.w)
+    kq = oracle.lsh_keys(w.dtype, w.Q, h.L, h.k, h.A, h.B, h.w)
+    tot = 0
+    for t in range(h.L):
+        up, cp = np.unique(kp[t], return_counts=True)
+        uq, cq = np.unique(kq[t], return_counts=True)
+        _, ip, iq = np.intersect1d(up, uq, return_indices=True)
+        tot += int((cp[ip].astype(np.int64) * cq[iq]).sum())
+    return tot
+
+
+def run_lsh(w, h, thr=None, self_join=False, check_cand=True):
+    import paper_2006_12608_amd as sj
+    thr = w.threshold if thr is None else thr
+    Pd = to_device(w.P, w.dtype)
+    Qd = Pd if self_join else to_device(w.Q, w.dtype)
+    A, B = lsh_device(h)
+    say(w.name, w.metric, w.dtype, w.n_p, w.n_q, w.d, thr, f"L={h.L} k={h.k} w={h.w}")
+    got, cand = sj.join_lsh(Pd, Qd, thr, w.metric, L=h.L, k=h.k, A=A, B=B, w=h.w)
+    g = sorted_pairs(got)
+    ref_pairs = oracle.lsh_join(w.metric, w.dtype, w.P, w.Q, thr, h.L, h.k, h.A, h.B, h.w)
+    band = 1e-3 * abs(thr) if w.real_valued else 0.0
+    exact = oracle.join(w.metric, w.dtype, w.P, w.Q, thr, band=band)
+    ref = oracle.JoinResult(ref_pairs, len(ref_pairs), exact.band_pairs, exact.band_match)
+    info = compare(g, ref, w.real_valued)
+    if check_cand:
+        assert cand == expected_candidates(w, h)
+    return g, ref_pairs, exact, cand, info
+
+
+def case(seed, n_p, n_q, d, dtype, metric, thr, lo=-4, hi=4, real=False):
+    w = workloads.random_case(seed, n_p, n_q, d, dtype, lo, hi, real=real, metric=metric,
+                              threshold=thr)
+    return w
+
+
+@pytest.mark.parametrize("dtype,metric,thr,d,wid", [
+    ("i8", "ip", 20.0, 64, 0),
+    ("bf16", "ip", 18.0, 128, 0),
+    ("f16", "ip", 30.0, 72, 0),
+    ("i8", "l2", 400.0, 48, 300),
+    ("bf16", "l2", 420.0, 96, 400),
+    ("f16", "l2", 500.0, 40, 350),
+])
+def test_lsh_parity_integer(dtype, metric, thr, d, wid):
+    w = case(700 + d, 333, 290, d, dtype, metric, thr)
+    # planted near-duplicates so the buckets share close pairs
+    w.Q[:40] = w.P[100:140]
+    h = workloads.lsh_params(900 + d, L=6, k=3, d=d, w=wid)
+    g, ref, exact, cand, _ = run_lsh(w, h)
+    assert 0 < len(ref) <= exact.total
+    assert cand < w.n_p * w.n_q * h.L
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_lsh_parity_real_cosine(dtype):
+    """Unit rows (real-valued), sign hashes: identical outside the band."""
+    wl = workloads.make_config("cos_f16_262144x256", n=1500)
+    if dtype == "bf16":
+        P = workloads.bf16_bits_from_f32(wl.P.astype(np.float32))
+        Q = workloads.bf16_bits_from_f32(wl.Q.astype(np.float32))
+        wl = workloads.Workload(wl.name + "-bf16", "ip", "bf16", P, Q, wl.threshold,
+                                wl.planted, real_valued=True)
+    h = workloads.lsh_params(77, L=8, k=6, d=wl.d)
+    g, ref, exact, cand, info = run_lsh(wl, h)
+    assert len(ref) > 0
+    say("band", info)
+
+
+def test_lsh_buckets_span_tiles_and_ragged():
+    """k = 1: two big buckets per table, each hundreds of rows (several 64-row
+    tiles plus ragged tails on both sides)."""
+    w = case(41, 517, 389, 33, "i8", "ip", 15.0, -6, 6)   # 33-byte rows: repacked
+    h = workloads.lsh_params(42, L=3, k=1, d=33)
+    run_lsh(w, h)
+
+
+def test_lsh_k0_is_exact_join():
+    import paper_2006_12608_amd as sj
+    w = case(43, 200, 150, 64, "bf16", "ip", 12.0)
+    h = workloads.lsh_params(44, L=2, k=0, d=64)
+    g, ref, exact, cand, _ = run_lsh(w, h)
+    assert np.array_equal(keys(g), keys(exact.pairs))
+    assert cand == w.n_p * w.n_q * h.L
+    full = sorted_pairs(sj.join_ip(to_device(w.P, "bf16"), to_device(w.Q, "bf16"), 12.0))
+    assert np.array_equal(full, g)
+
+
+def test_lsh_self_join_same_pointer():
+    w = case(45, 300, 300, 32, "i8", "l2", 300.0, -5, 5)
+    w.Q = w.P
+    w.P[50:60] = w.P[0:10]
+    h = workloads.lsh_params(46, L=5, k=2, d=32, w=250)
+    g, ref, *_ = run_lsh(w, h, self_join=True)
+    s = set(map(tuple, g.tolist()))
+    assert all((i, i) in s for i in range(300))      # every point collides with itself
+    assert all((j, i) in s for (i, j) in s)          # symmetric
+
+
+def test_lsh_many_tables_first_table_rule():
+    """Many tables and few functions: most pairs collide in several tables;
+    each must still be reported once."""
+    w = case(47, 260, 240, 16, "i8", "ip", 6.0, -3, 3)
+    h = workloads.lsh_params(48, L=24, k=2, d=16)
+    g, ref, *_ = run_lsh(w, h)
+    assert len(g) == len(ref)
+
+
+def test_lsh_overflow_and_errors():
+    import torch
+    import paper_2006_12608_amd as sj
+    w = case(49, 128, 128, 32, "i8", "ip", 4.0)
+    h = workloads.lsh_params(50, L=4, k=2, d=32)
+    Pd, Qd = to_device(w.P, "i8"), to_device(w.Q, "i8")
+    A, B = lsh_device(h)
+    n_ref = len(oracle.lsh_join("ip", "i8", w.P, w.Q, 4.0, h.L, h.k, h.A, h.B, h.w))
+    assert n_ref > 10
+    out = torch.empty((5, 2), dtype=torch.int32, device="cuda")
+    with pytest.raises(sj.SjError) as e:
+        sj.join_lsh(Pd, Qd, 4.0, "ip", L=4, k=2, A=A, w=0, cap=5, out=out)
+    assert e.value.status == sj.SJ_E_OVERFLOW and e.value.n_out == n_ref
+    ctx = sj.context()
+    args = (ctx, sj.SJ_IP, sj.SJ_I8, Pd.data_ptr(), 128, Qd.data_ptr(), 128, 32, 4.0)
+    assert sj.sj_join_lsh(*args, 0, 2, A.data_ptr(), None, 0, None, 0)[0] == sj.SJ_E_INVAL
+    assert sj.sj_join_lsh(*args, 4, 65, A.data_ptr(), None, 0, None, 0)[0] == sj.SJ_E_INVAL
+    assert sj.sj_join_lsh(*args, 4, 2, None, None, 0, None, 0)[0] == sj.SJ_E_INVAL
+    assert sj.sj_join_lsh(*args, 4, 2, A.data_ptr(), None, 5, None, 0)[0] == sj.SJ_E_INVAL
+    assert sj.sj_join_lsh(*args, 4, 2, A.data_ptr(), None, -1, None, 0)[0] == sj.SJ_E_INVAL
+    st, n, nc = sj.sj_join_lsh(ctx, sj.SJ_IP, sj.SJ_I8, Pd.data_ptr(), 0, Qd.data_ptr(), 128,
+                               32, 4.0, 4, 2, A.data_ptr(), None, 0, None, 0)
+    assert (st, n, nc) == (sj.SJ_OK, 0, 0)
+
+
+def test_lsh_cosine_workload_recall():
+    """The cosine workload's distribution at 16384 rows with the LSH
+    parameters the benchmark uses at full size (16 tables of 10 signs):
+    parity with the oracle's LSH join, and every planted neighbour that
+    matches is found unless no table makes it collide."""
+    wl = workloads.make_config("cos_f16_262144x256", n=16384)
+    h = workloads.lsh_params(1302, L=16, k=10, d=wl.d)
+    g, ref, exact, cand, info = run_lsh(wl, h, check_cand=False)
+    say("pairs", len(g), "exact", exact.total, "candidates", cand, "band", info)
+    assert cand < wl.n_p * wl.n_q // 8
+    assert len(ref) >= 0.9 * exact.total
