@@ -7,7 +7,7 @@
 // The bucket join is the brute-force join of Section 4 restricted to a pair of
 // buckets: Theorem 3's cost is the sum over tables and shared buckets of
 // |P bucket| x |Q bucket| inner products, each bucket pair handled as a
-// blocked product on 64 x 64 workgroup tiles (32 x 32 MFMA blocks), with the
+// blocked product on 128 x 128 workgroup tiles (32 x 32 MFMA blocks), with the
 // same fused threshold test and wave-ballot compaction as the all-pairs join.
 #include "sj_lsh.h"
 
@@ -28,7 +28,11 @@ using sjk::MET_L2;
 
 // ----------------------------------------------------------------- keys
 
-// The E stored elements of one 16-byte chunk as exact values.
+// The E stored elements of one 16-byte chunk as exact values; `acc_t` is the
+// projection's accumulator and `a_t` the type the projection entries are
+// converted to once, before the hash (so that the inner loop is one fused
+// multiply-add per element and function, its entry read through the scalar
+// path: the entries are the same for every row of a workgroup).
 template <int DT>
 struct Chunk;
 
@@ -36,6 +40,7 @@ template <>
 struct Chunk<DT_F16> {
     static constexpr int E = 8;
     typedef double acc_t;
+    typedef double a_t;
     static __device__ __forceinline__ double at(const i32x4 &v, int e)
     {
         const uint16_t h = (uint16_t)((uint32_t)v[e >> 1] >> (16 * (e & 1)));
@@ -47,6 +52,7 @@ template <>
 struct Chunk<DT_BF16> {
     static constexpr int E = 8;
     typedef double acc_t;
+    typedef double a_t;
     static __device__ __forceinline__ double at(const i32x4 &v, int e)
     {
         const uint32_t h = ((uint32_t)v[e >> 1] >> (16 * (e & 1))) & 0xffffu;
@@ -58,76 +64,198 @@ template <>
 struct Chunk<DT_I8> {
     static constexpr int E = 16;
     typedef int32_t acc_t;   // |z| <= 32768 * 128 * 128 = 2^29: exact
+    typedef int32_t a_t;
     static __device__ __forceinline__ int32_t at(const i32x4 &v, int e)
     {
         return (int32_t)(int8_t)((uint32_t)v[e >> 2] >> (8 * (e & 3)));
     }
 };
 
-// Functions evaluated per pass over a row.
-constexpr int KG = 4;
-
-// One thread per (row, table): z_f = sum_m A[f][m] x_m in ascending m (exact
-// products; for fp16/bf16 a double sum in that order, for int8 an exact int32
-// sum), then the function value and the key (see launch_keys).
+// Projection rows are widened with their length padded to a multiple of the
+// chunk's E elements (zeros past d): together with the zero padding of the
+// rows this adds only exact zeros to each sum, and the inner loop needs no
+// bounds test.
 template <int DT>
-__global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t k,
-                                                   const int8_t *A, const int32_t *B, int32_t w,
+constexpr uint32_t padded_d(uint32_t d)
+{
+    return (d + Chunk<DT>::E - 1) / Chunk<DT>::E * Chunk<DT>::E;
+}
+
+template <typename T>
+__global__ void widen_kernel(const int8_t *A, T *out, uint32_t d, uint32_t dp, uint64_t n_out)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n_out) {
+        const uint64_t f = i / dp, m = i - f * dp;
+        out[i] = m < d ? T(A[f * d + m]) : T(0);
+    }
+}
+
+// Rows a workgroup of the key kernel stages in LDS at once (one per lane of a
+// wave), and the bytes of a row it stages per pass.
+constexpr int KROWS = 64;
+constexpr int KSEG = 512;
+
+// G consecutive functions of one row segment: z[g] += sum_m A[f0 + g][m0 + m] x_m
+// over the segment's nch chunks (x: this lane's row in LDS) in ascending m.
+// The entries' addresses are the same for every lane (the compiler reads them
+// with scalar loads).
+template <int DT, int G>
+__device__ __forceinline__ void project(const uint8_t *x, uint32_t nch, uint32_t dp,
+                                        const typename Chunk<DT>::a_t *a,
+                                        typename Chunk<DT>::acc_t (&z)[G])
+{
+    typedef Chunk<DT> C;
+    typedef typename C::acc_t acc_t;
+    for (uint32_t c = 0; c < nch; ++c) {
+        const i32x4 v = *(const i32x4 *)(x + 16 * c);
+        acc_t xe[C::E];
+#pragma unroll
+        for (int e = 0; e < C::E; ++e)
+            xe[e] = C::at(v, e);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const typename C::a_t *ag = a + (size_t)g * dp + c * C::E;
+#pragma unroll
+            for (int e = 0; e < C::E; ++e)
+                z[g] += acc_t(ag[e]) * xe[e];
+        }
+    }
+}
+
+// Function u's value folded into the key (see launch_keys).
+template <typename T>
+__device__ __forceinline__ void fold_value(uint64_t &key, T z, uint32_t u, uint32_t beta,
+                                           uint64_t low, const int32_t *B, uint32_t f,
+                                           int32_t w)
+{
+    if (w == 0) {
+        key |= (uint64_t)(z >= T(0)) << u;
+    } else {
+        const double q = ((double)z + (double)B[f]) / (double)w;
+        const int64_t v = (int64_t)floor(q);
+        key |= ((uint64_t)v & low) << (beta * u);
+    }
+}
+
+// A workgroup of 4 waves takes KROWS rows: it stages them in LDS in segments
+// of KSEG bytes per row (coalesced loads; rows padded by 16 bytes so that the
+// lanes' 16-byte reads of their own rows hit distinct banks) and each lane
+// computes the keys of its row; wave v takes the tables v, v + 4, ...  Per
+// table: z_f = sum_m A[f][m] x_m in ascending m (exact products; for
+// fp16/bf16 a double sum in that order, for int8 an exact int32 sum), then the
+// function values and the key (see launch_keys); `tshift` > 0 also places the
+// table number above the key's bits (one sort for all tables).  Rows of at
+// most KSEG bytes are staged once for every table; longer rows once per table
+// and segment, with the partial sums kept for at most 16 functions per pass.
+template <int DT, bool LONG>
+__global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t L, uint32_t k,
+                                                   const typename Chunk<DT>::a_t *A,
+                                                   const int32_t *B, int32_t w, uint32_t tshift,
                                                    uint64_t *keys)
 {
     typedef Chunk<DT> C;
     typedef typename C::acc_t acc_t;
-    const uint32_t row = blockIdx.x * 256 + threadIdx.x;
-    const uint32_t t = blockIdx.y;
-    if (row >= r.n)
-        return;
-    const uint8_t *x = r.X + (size_t)row * r.row_bytes;
-    const uint32_t nch = (d + C::E - 1) / C::E;
+    constexpr int RS = KSEG + 16;   // LDS row stride
+    __shared__ __attribute__((aligned(16))) uint8_t xs[KROWS * RS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t row0 = blockIdx.x * KROWS;
+    const uint32_t rows = min(r.n - row0, (uint32_t)KROWS);
+    const uint32_t dp = padded_d<DT>(d);
+    const uint32_t rb = dp * (DT == DT_I8 ? 1 : 2);   // bytes hashed per row (<= row_bytes)
     const uint32_t beta = k ? 64 / k : 64;
     const uint64_t low = beta >= 64 ? ~0ull : (1ull << beta) - 1;
-    uint64_t key = 0;
-    for (uint32_t u0 = 0; u0 < k; u0 += KG) {
-        acc_t z[KG];
-#pragma unroll
-        for (int g = 0; g < KG; ++g)
-            z[g] = acc_t(0);
-        const int8_t *a = A + (size_t)(t * k + u0) * d;
-        for (uint32_t c = 0; c < nch; ++c) {
-            const i32x4 v = *(const i32x4 *)(x + 16 * c);
-#pragma unroll
-            for (int e = 0; e < C::E; ++e) {
-                const uint32_t m = c * C::E + e;
-                if (m < d) {
-                    const acc_t xe = C::at(v, e);
-#pragma unroll
-                    for (int g = 0; g < KG; ++g)
-                        if (u0 + g < k)
-                            z[g] += acc_t(a[(size_t)g * d + m]) * xe;
-                }
-            }
+
+    auto stage = [&](uint32_t seg0, uint32_t segb) {
+        // segb bytes of every row from byte seg0; 16 bytes per lane per step
+        const uint32_t cpr = segb / 16;
+        for (uint32_t q = tid; q < KROWS * cpr; q += 256) {
+            const uint32_t rr = q / cpr, cc = q - rr * cpr;
+            i32x4 v = {0, 0, 0, 0};
+            if (rr < rows)
+                v = *(const i32x4 *)(r.X + (size_t)(row0 + rr) * r.row_bytes + seg0 + 16 * cc);
+            *(i32x4 *)(xs + rr * RS + 16 * cc) = v;
         }
+    };
+    const uint8_t *mine = xs + lane * RS;
+    if constexpr (!LONG) {
+        if (rb)
+            stage(0, rb);
+        __syncthreads();
+        const uint32_t nch = rb / 16;
+        for (uint32_t t = wave; t < L; t += 4) {
+            uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
+            uint32_t u = 0;
+            for (; u + 4 <= k; u += 4) {
+                acc_t z[4] = {};
+                project<DT, 4>(mine, nch, dp, A + (size_t)(t * k + u) * dp, z);
 #pragma unroll
-        for (int g = 0; g < KG; ++g) {
-            const uint32_t u = u0 + g;
+                for (int g = 0; g < 4; ++g)
+                    fold_value(key, z[g], u + g, beta, low, B, t * k + u + g, w);
+            }
+            if (u + 2 <= k) {
+                acc_t z[2] = {};
+                project<DT, 2>(mine, nch, dp, A + (size_t)(t * k + u) * dp, z);
+#pragma unroll
+                for (int g = 0; g < 2; ++g)
+                    fold_value(key, z[g], u + g, beta, low, B, t * k + u + g, w);
+                u += 2;
+            }
             if (u < k) {
-                if (w == 0) {
-                    key |= (uint64_t)(z[g] >= acc_t(0)) << u;
-                } else {
-                    const double q = ((double)z[g] + (double)B[t * k + u]) / (double)w;
-                    const int64_t v = (int64_t)floor(q);
-                    key |= ((uint64_t)v & low) << (beta * u);
+                acc_t z[1] = {};
+                project<DT, 1>(mine, nch, dp, A + (size_t)(t * k + u) * dp, z);
+                fold_value(key, z[0], u, beta, low, B, t * k + u, w);
+            }
+            if ((uint32_t)lane < rows)
+                keys[(size_t)t * r.n + row0 + lane] = key;
+        }
+        return;
+    } else {
+    // long rows: segments of KSEG bytes, every wave takes table t = wave + 4 j
+    // in turn (all waves pass every barrier: the table loop is uniform)
+    const uint32_t tl = (L + 3) / 4 * 4;
+    for (uint32_t t0 = 0; t0 < tl; t0 += 4) {
+        const uint32_t t = t0 + wave;
+        uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
+        for (uint32_t u = 0; u < k; u += 16) {
+            acc_t z[16] = {};
+            for (uint32_t seg0 = 0; seg0 < rb; seg0 += KSEG) {
+                const uint32_t segb = min(rb - seg0, (uint32_t)KSEG);
+                __syncthreads();   // the previous segment is consumed
+                stage(seg0, segb);
+                __syncthreads();
+                if (t < L) {
+                    const typename C::a_t *a = A + (size_t)(t * k + u) * dp +
+                                               seg0 / 16 * C::E;
+                    if (u + 16 <= k)
+                        project<DT, 16>(mine, segb / 16, dp, a, z);
+                    else
+#pragma unroll
+                        for (int g = 0; g < 16; ++g)
+                            if (u + g < k) {
+                                acc_t zg[1] = {z[g]};
+                                project<DT, 1>(mine, segb / 16, dp, a + (size_t)g * dp, zg);
+                                z[g] = zg[0];
+                            }
                 }
             }
+#pragma unroll
+            for (int g = 0; g < 16; ++g)
+                if (t < L && u + g < k)
+                    fold_value(key, z[g], u + g, beta, low, B, t * k + u + g, w);
         }
+        if (t < L && (uint32_t)lane < rows)
+            keys[(size_t)t * r.n + row0 + lane] = key;
     }
-    keys[(size_t)t * r.n + row] = key;
+    }
 }
 
-__global__ void iota_kernel(uint32_t *v, uint32_t n)
+// v[i] = i mod n for i < total (the row of entry i of table-major arrays).
+__global__ void iota_kernel(uint32_t *v, uint32_t n, uint32_t total)
 {
     const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < n)
-        v[i] = i;
+    if (i < total)
+        v[i] = i % n;
 }
 
 // ------------------------------------------------------------ bucket pairs
@@ -215,27 +343,29 @@ __device__ __forceinline__ bool matches(typename sjk::Mma<DT>::val_t acc,
     }
 }
 
-// A workgroup of 4 waves takes 64 x 64 tiles of bucket pairs (grid-stride):
-// the tile's rows of P and Q are gathered through the tables' sorted
-// permutations into LDS in chunks of 128 bytes of each row (16-byte chunks,
-// rows padded by one chunk), wave (wr, wc) multiplies its 32 x 32 block on the
-// matrix cores over the chunk's k-steps, and the epilogue applies the exact
+// A workgroup of 4 waves takes TILE x TILE tiles of bucket pairs
+// (grid-stride): the tile's rows of P and Q are gathered through the tables'
+// sorted permutations into LDS in chunks of 128 bytes of each row (16-byte
+// chunks, rows padded by one chunk), wave (wr, wc) multiplies its 64 x 64
+// quarter (2 x 2 blocks of 32 x 32: per k-step two A- and two B-fragments for
+// four MFMAs) over the chunk's k-steps, and the epilogue applies the exact
 // test, drops pairs that share a bucket in an earlier table (so every pair is
-// reported once) and appends the rest with one atomic per wave.
+// reported once) and appends the rest with one atomic per wave and block.
 template <int DT, int MET>
 __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
 {
     typedef sjk::Mma<DT> M;
     typedef typename M::acc_t acc_t;
     typedef typename M::val_t V;
-    constexpr int CS = 9;    // LDS positions per tile row: 8 chunks + 1 pad
+    constexpr int CS = 9;            // LDS positions per tile row: 8 chunks + 1 pad
+    constexpr int LPT = TILE / 32;   // rows each thread loads per operand and chunk
     __shared__ i32x4 sA[TILE * CS], sB[TILE * CS];
     __shared__ uint32_t sIP[TILE], sIQ[TILE];
     __shared__ V sNP[TILE], sNQ[TILE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1, half = lane >> 5, c32 = lane & 31;
     const uint32_t rb = g.P.row_bytes;   // == g.Q.row_bytes
-    const uint32_t lc = tid & 7, lr = tid >> 3;   // this thread's load chunk and rows lr, lr + 32
+    const uint32_t lc = tid & 7, lr = tid >> 3;   // load chunk; rows lr + 32 e
 
     for (uint64_t T = blockIdx.x; T < g.n_tiles; T += gridDim.x) {
         uint32_t lo = 0, hi = g.n_bp;
@@ -255,112 +385,146 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
 
         __syncthreads();   // the previous tile's reads of sIP/sIQ/sA/sB are done
         if (tid < (int)TILE) {
-            const bool ok = (uint32_t)tid < rows_p;
-            const uint32_t i = ok ? g.perm_p[(size_t)t * g.P.n + h.y + tp * TILE + tid] : 0u;
+            const bool okp = (uint32_t)tid < rows_p;
+            const uint32_t i = okp ? g.perm_p[(size_t)t * g.P.n + h.y + tp * TILE + tid] : 0u;
             sIP[tid] = i;
-            if constexpr (MET == MET_L2)
-                sNP[tid] = ok ? ((const V *)g.norm_p)[i] : V(0);
-        } else if (tid < (int)(2 * TILE)) {
-            const int c = tid - TILE;
-            const bool ok = (uint32_t)c < rows_q;
-            const uint32_t j = ok ? g.perm_q[(size_t)t * g.Q.n + h.w + tq * TILE + c] : 0u;
-            sIQ[c] = j;
-            if constexpr (MET == MET_L2)
-                sNQ[c] = ok ? ((const V *)g.norm_q)[j] : V(0);
+            const bool okq = (uint32_t)tid < rows_q;
+            const uint32_t j = okq ? g.perm_q[(size_t)t * g.Q.n + h.w + tq * TILE + tid] : 0u;
+            sIQ[tid] = j;
+            if constexpr (MET == MET_L2) {
+                sNP[tid] = okp ? ((const V *)g.norm_p)[i] : V(0);
+                sNQ[tid] = okq ? ((const V *)g.norm_q)[j] : V(0);
+            }
         }
         __syncthreads();
-        const uint8_t *pa0 = g.P.X + (size_t)sIP[lr] * rb;
-        const uint8_t *pa1 = g.P.X + (size_t)sIP[lr + 32] * rb;
-        const uint8_t *pb0 = g.Q.X + (size_t)sIQ[lr] * rb;
-        const uint8_t *pb1 = g.Q.X + (size_t)sIQ[lr + 32] * rb;
-        const bool va0 = lr < rows_p, va1 = lr + 32 < rows_p;
-        const bool vb0 = lr < rows_q, vb1 = lr + 32 < rows_q;
+        const uint8_t *pa[LPT], *pb[LPT];
+        bool va[LPT], vb[LPT];
+#pragma unroll
+        for (int e = 0; e < LPT; ++e) {
+            pa[e] = g.P.X + (size_t)sIP[lr + 32 * e] * rb;
+            pb[e] = g.Q.X + (size_t)sIQ[lr + 32 * e] * rb;
+            va[e] = lr + 32 * e < rows_p;
+            vb[e] = lr + 32 * e < rows_q;
+        }
 
-        acc_t acc = acc_t{};
+        acc_t acc[2][2];
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                acc[a][b] = acc_t{};
         for (uint32_t kc = 0; kc < rb; kc += 128) {
             const uint32_t off = kc + 16 * lc;
             const i32x4 z = {0, 0, 0, 0};
             const bool in = off < rb;
-            const i32x4 a0 = va0 && in ? *(const i32x4 *)(pa0 + off) : z;
-            const i32x4 a1 = va1 && in ? *(const i32x4 *)(pa1 + off) : z;
-            const i32x4 b0 = vb0 && in ? *(const i32x4 *)(pb0 + off) : z;
-            const i32x4 b1 = vb1 && in ? *(const i32x4 *)(pb1 + off) : z;
+            i32x4 la[LPT], lb[LPT];
+#pragma unroll
+            for (int e = 0; e < LPT; ++e) {
+                la[e] = va[e] && in ? *(const i32x4 *)(pa[e] + off) : z;
+                lb[e] = vb[e] && in ? *(const i32x4 *)(pb[e] + off) : z;
+            }
             if (kc)
                 __syncthreads();   // the previous chunk's fragments are read
-            sA[lr * CS + lc] = a0;
-            sA[(lr + 32) * CS + lc] = a1;
-            sB[lr * CS + lc] = b0;
-            sB[(lr + 32) * CS + lc] = b1;
+#pragma unroll
+            for (int e = 0; e < LPT; ++e) {
+                sA[(lr + 32 * e) * CS + lc] = la[e];
+                sB[(lr + 32 * e) * CS + lc] = lb[e];
+            }
             __syncthreads();
             const uint32_t nks = min(4u, (rb - kc + 31) / 32);
 #pragma unroll
             for (uint32_t ks = 0; ks < 4; ++ks)
                 if (ks < nks) {
-                    const i32x4 a = sA[(wr * 32 + c32) * CS + 2 * ks + half];
-                    const i32x4 b = sB[(wc * 32 + c32) * CS + 2 * ks + half];
-                    acc = M::mma(a, b, acc);
+                    i32x4 fa[2], fb[2];
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        fa[a] = sA[(wr * 64 + 32 * a + c32) * CS + 2 * ks + half];
+                        fb[a] = sB[(wc * 64 + 32 * a + c32) * CS + 2 * ks + half];
+                    }
+#pragma unroll
+                    for (int a = 0; a < 2; ++a)
+#pragma unroll
+                        for (int b = 0; b < 2; ++b)
+                            acc[a][b] = M::mma(fa[a], fb[b], acc[a][b]);
                 }
         }
 
-        // epilogue: result register r of this lane is (row wr*32 + 8(r/4) +
-        // 4 half + r%4, column wc*32 + c32) of the tile
-        const uint32_t jl = wc * 32 + c32;
-        const bool jok = jl < rows_q;
-        const uint32_t j = sIQ[jl];
-        const V ny = MET == MET_L2 ? sNQ[jl] : V(0);
-        uint32_t m = 0;
+        // epilogue, block (a, b): result register r of this lane is (row
+        // wr*64 + 32a + 8(r/4) + 4 half + r%4, column wc*64 + 32b + c32)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const uint32_t il = wr * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            const V nx = MET == MET_L2 ? sNP[il] : V(0);
-            const bool ok = jok && il < rows_p && matches<DT, MET>(acc[r], nx, ny, g);
-            m |= ok ? (1u << r) : 0u;
-        }
-        if (t > 0 && m != 0) {
-            uint32_t mm = m;
-            while (mm) {
-                const int r = __builtin_ctz(mm);
-                mm &= mm - 1;
-                const uint32_t i = sIP[wr * 32 + 8 * (r >> 2) + 4 * half + (r & 3)];
-                for (uint32_t t2 = 0; t2 < t; ++t2)
-                    if (g.keys_p[(size_t)t2 * g.P.n + i] == g.keys_q[(size_t)t2 * g.Q.n + j]) {
-                        m &= ~(1u << r);
-                        break;
-                    }
-            }
-        }
-        const uint32_t cnt = (uint32_t)__builtin_popcount(m);
-        uint32_t tot = 0, pre = 0;
+        for (int b = 0; b < 2; ++b) {
+            const uint32_t jl = wc * 64 + 32 * b + c32;
+            const bool jok = jl < rows_q;
+            const uint32_t j = sIQ[jl];
+            const V ny = MET == MET_L2 ? sNQ[jl] : V(0);
 #pragma unroll
-        for (int b = 0; b < 5; ++b) {
-            const uint64_t bits = __ballot((cnt >> b) & 1);
-            tot += (uint32_t)__popcll(bits) << b;
-            pre += sjk::lanes_below(bits) << b;
-        }
-        if (tot != 0) {
-            unsigned long long base = 0;
-            if (lane == 0)
-                base = atomicAdd(g.counter, (unsigned long long)tot);
-            uint64_t pos = sjk::first_lane_u64(base) + pre;
-            while (m) {
-                const int r = __builtin_ctz(m);
-                m &= m - 1;
-                if (pos < g.cap) {
-                    const uint32_t i = sIP[wr * 32 + 8 * (r >> 2) + 4 * half + (r & 3)];
-                    ((sjk::global_pair *)g.pairs)[pos] = sjk::pack_pair(i, j);
+            for (int a = 0; a < 2; ++a) {
+                const uint32_t ib = wr * 64 + 32 * a + 4 * half;
+                uint32_t m = 0;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const uint32_t il = ib + 8 * (r >> 2) + (r & 3);
+                    const V nx = MET == MET_L2 ? sNP[il] : V(0);
+                    const bool ok = jok && il < rows_p && matches<DT, MET>(acc[a][b][r], nx, ny, g);
+                    m |= ok ? (1u << r) : 0u;
                 }
-                ++pos;
+                if (__ballot(m != 0) == 0)
+                    continue;
+                if (t > 0 && m != 0) {
+                    uint32_t mm = m;
+                    while (mm) {
+                        const int r = __builtin_ctz(mm);
+                        mm &= mm - 1;
+                        const uint32_t i = sIP[ib + 8 * (r >> 2) + (r & 3)];
+                        for (uint32_t t2 = 0; t2 < t; ++t2)
+                            if (g.keys_p[(size_t)t2 * g.P.n + i] ==
+                                g.keys_q[(size_t)t2 * g.Q.n + j]) {
+                                m &= ~(1u << r);
+                                break;
+                            }
+                    }
+                }
+                const uint32_t cnt = (uint32_t)__builtin_popcount(m);
+                uint32_t tot = 0, pre = 0;
+#pragma unroll
+                for (int bit = 0; bit < 5; ++bit) {
+                    const uint64_t bits = __ballot((cnt >> bit) & 1);
+                    tot += (uint32_t)__popcll(bits) << bit;
+                    pre += sjk::lanes_below(bits) << bit;
+                }
+                if (tot != 0) {
+                    unsigned long long base = 0;
+                    if (lane == 0)
+                        base = atomicAdd(g.counter, (unsigned long long)tot);
+                    uint64_t pos = sjk::first_lane_u64(base) + pre;
+                    while (m) {
+                        const int r = __builtin_ctz(m);
+                        m &= m - 1;
+                        if (pos < g.cap) {
+                            const uint32_t i = sIP[ib + 8 * (r >> 2) + (r & 3)];
+                            ((sjk::global_pair *)g.pairs)[pos] = sjk::pack_pair(i, j);
+                        }
+                        ++pos;
+                    }
+                }
             }
         }
     }
 }
 
 template <int DT>
-hipError_t launch_keys_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k, const int8_t *A,
-                         const int32_t *B, int32_t w, uint64_t *keys, hipStream_t s)
+hipError_t launch_keys_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k, const void *Aw,
+                         const int32_t *B, int32_t w, uint32_t tshift, uint64_t *keys,
+                         hipStream_t s)
 {
-    const dim3 grid((r.n + 255) / 256, L);
-    hipLaunchKernelGGL(keys_kernel<DT>, grid, dim3(256), 0, s, r, d, k, A, B, w, keys);
+    const dim3 grid((r.n + KROWS - 1) / KROWS);
+    const uint32_t rb = padded_d<DT>(d) * (DT == DT_I8 ? 1 : 2);
+    if (rb <= KSEG)
+        hipLaunchKernelGGL((keys_kernel<DT, false>), grid, dim3(256), 0, s, r, d, L, k,
+                           (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, keys);
+    else
+        hipLaunchKernelGGL((keys_kernel<DT, true>), grid, dim3(256), 0, s, r, d, L, k,
+                           (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, keys);
     return hipGetLastError();
 }
 
@@ -385,20 +549,51 @@ uint32_t key_bits(uint32_t k, int32_t w)
     return b > 64 ? 64 : b;
 }
 
+uint32_t table_bits(uint32_t L)
+{
+    uint32_t b = 0;
+    while ((1u << b) < L)
+        ++b;
+    return b;
+}
+
+size_t widened_bytes(int dtype, uint32_t L, uint32_t k, uint32_t d)
+{
+    return dtype == DT_I8 ? (size_t)L * k * padded_d<DT_I8>(d) * 4
+                          : (size_t)L * k * padded_d<DT_F16>(d) * 8;
+}
+
 hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                       const int8_t *A, const int32_t *B, int32_t w, uint64_t *keys,
-                       hipStream_t s)
+                       const void *Aw, const int32_t *B, int32_t w, uint32_t tshift,
+                       uint64_t *keys, hipStream_t s)
 {
     if (r.n == 0 || L == 0)
         return hipSuccess;
     switch (dtype) {
     case DT_F16:
-        return launch_keys_t<DT_F16>(r, d, L, k, A, B, w, keys, s);
+        return launch_keys_t<DT_F16>(r, d, L, k, Aw, B, w, tshift, keys, s);
     case DT_BF16:
-        return launch_keys_t<DT_BF16>(r, d, L, k, A, B, w, keys, s);
+        return launch_keys_t<DT_BF16>(r, d, L, k, Aw, B, w, tshift, keys, s);
     default:
-        return launch_keys_t<DT_I8>(r, d, L, k, A, B, w, keys, s);
+        return launch_keys_t<DT_I8>(r, d, L, k, Aw, B, w, tshift, keys, s);
     }
+}
+
+hipError_t launch_widen(int dtype, const int8_t *A, uint32_t n_fn, uint32_t d, void *out,
+                        hipStream_t s)
+{
+    const uint32_t dp = dtype == DT_I8 ? padded_d<DT_I8>(d) : padded_d<DT_F16>(d);
+    const uint64_t n = (uint64_t)n_fn * dp;
+    if (n == 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (dtype == DT_I8)
+        hipLaunchKernelGGL(widen_kernel<int32_t>, grid, dim3(256), 0, s, A, (int32_t *)out, d,
+                           dp, n);
+    else
+        hipLaunchKernelGGL(widen_kernel<double>, grid, dim3(256), 0, s, A, (double *)out, d, dp,
+                           n);
+    return hipGetLastError();
 }
 
 size_t sort_temp_bytes(uint32_t n, uint32_t bits)
@@ -411,13 +606,23 @@ size_t sort_temp_bytes(uint32_t n, uint32_t bits)
 }
 
 hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
-                       uint32_t n, uint32_t L, uint32_t bits, void *temp, size_t temp_bytes,
-                       hipStream_t s)
+                       uint32_t n, uint32_t L, uint32_t bits, bool joint, void *temp,
+                       size_t temp_bytes, hipStream_t s)
 {
     if (n == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, iota, n);
+    const uint32_t total = joint ? n * L : n;
+    hipLaunchKernelGGL(iota_kernel, dim3((total + 255) / 256), dim3(256), 0, s, iota, n, total);
     hipError_t e = hipGetLastError();
+    if (joint) {
+        // keys carry their table above `bits`: one sort orders every table
+        // within its own segment [t n, (t + 1) n)
+        size_t tb = temp_bytes;
+        if (e == hipSuccess)
+            e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys, sorted, iota, perm, total, 0,
+                                                   (int)(bits + table_bits(L)), s);
+        return e;
+    }
     for (uint32_t t = 0; t < L && e == hipSuccess; ++t) {
         size_t tb = temp_bytes;
         e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys + (size_t)t * n,

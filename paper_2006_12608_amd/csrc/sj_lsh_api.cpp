@@ -82,13 +82,19 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const bool self = P == Q && n_p == n_q;
     const bool l2 = metric == SJ_L2;
     const uint32_t bits = sjl::key_bits(k, w);
+    // one sort for all tables when the table number fits above the key
+    const bool joint = bits + sjl::table_bits(L) <= 64;
+    const uint32_t tshift = joint && L > 1 ? bits : 0;
+    const uint32_t sbits = joint ? bits + sjl::table_bits(L) : bits;
     const uint64_t bp_cap = (uint64_t)L * (n_p < n_q ? n_p : n_q);
-    size_t temp_bytes = sjl::sort_temp_bytes(n_p, bits);
-    const size_t tq = sjl::sort_temp_bytes(n_q, bits);
+    size_t temp_bytes = sjl::sort_temp_bytes(joint ? L * n_p : n_p, sbits);
+    const size_t tq = sjl::sort_temp_bytes(joint ? L * n_q : n_q, sbits);
     temp_bytes = temp_bytes > tq ? temp_bytes : tq;
+    const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
     // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
     //          [sorted Q][perm P][perm Q][iota][bucket pairs][counters][sort temp]
+    //          [widened projections]
     size_t need = 0;
     auto take = [&](size_t bytes) {
         const size_t at = need;
@@ -105,12 +111,13 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_sq = self ? off_sp : take((size_t)L * n_q * 8);
     const size_t off_pp = take((size_t)L * n_p * 4);
     const size_t off_pq = self ? off_pp : take((size_t)L * n_q * 4);
-    const size_t off_iota = take((size_t)n_max * 4);
+    const size_t off_iota = take((size_t)L * n_max * 4);
     const size_t off_head = take((size_t)bp_cap * 16);
     const size_t off_bnq = take((size_t)bp_cap * 4);
     const size_t off_t0 = take((size_t)bp_cap * 8);
     const size_t off_cnt = take(4 * 8);
     const size_t off_temp = take(temp_bytes);
+    const size_t off_aw = take(a_bytes);
     if ((st = grow_scratch(c, need)) != SJ_OK)
         return st;
     uint8_t *scr = (uint8_t *)c->scratch;
@@ -136,18 +143,19 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
             SJ_HIP(sjk::launch_norms(dtype, rq.X, n_q, rq.row_bytes, scr + off_nq, s));
     }
     uint64_t *keys_p = (uint64_t *)(scr + off_kp), *keys_q = (uint64_t *)(scr + off_kq);
-    SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, A, B, w, keys_p, s));
+    SJ_HIP(sjl::launch_widen(dtype, A, L * k, d, scr + off_aw, s));
+    SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, scr + off_aw, B, w, tshift, keys_p, s));
     if (!self)
-        SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, A, B, w, keys_q, s));
+        SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, tshift, keys_q, s));
     SJ_HIP(hipEventRecord(c->ev[1], s));
     uint64_t *sorted_p = (uint64_t *)(scr + off_sp), *sorted_q = (uint64_t *)(scr + off_sq);
     uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
     uint32_t *iota = (uint32_t *)(scr + off_iota);
-    SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, iota, n_p, L, bits, scr + off_temp,
-                            temp_bytes, s));
+    SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, iota, n_p, L, bits, joint,
+                            scr + off_temp, temp_bytes, s));
     if (!self)
-        SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, scr + off_temp,
-                                temp_bytes, s));
+        SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, joint,
+                                scr + off_temp, temp_bytes, s));
     sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
                         (unsigned long long *)(scr + off_t0), cnt, (uint32_t)bp_cap};
     SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));
