@@ -249,6 +249,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 256 MiB buffer three times (the reference kernel for "
                          "scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters to HBM bytes)")
+    ap.add_argument("--self-join", action="store_true",
+                    help="join the workload's P with itself (same pointer: the single pass "
+                         "computes the upper triangle and mirrors its pairs)")
     ap.add_argument("--lsh", default=None, metavar="L,k[,w]",
                     help="time the LSH-bucketed join (sj_join_lsh) on the workload instead: "
                          "L tables of k concatenated projections (w = 0: signs; w > 0: "
@@ -270,9 +273,10 @@ def main():
 
     k = args.workload
     log(f"generating workload {k} ...")
-    w = workloads.make_config(k)
+    w = workloads.make_config(k, self_join=args.self_join)
     torch.cuda.set_device(0)
-    Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
+    Pd = to_device(w.P, w.dtype)
+    Qd = Pd if w.self_join else to_device(w.Q, w.dtype)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ctx = sj.context(0, stream)
@@ -323,9 +327,14 @@ def main():
     value = pair_evals / (ms_step / 1e3)
     kms = float(np.mean(kern_ms))
     flop = 2.0 * pair_evals * max(w.d, 1)
-    achieved = flop / (kms / 1e3) / 1e12
+    # a self-join's distinct pairs: the upper triangle, diagonal included
+    # (the kernel computes those and mirrors the rest)
+    kflop = 2.0 * (w.n_p * (w.n_p + 1) // 2) * max(w.d, 1) if w.self_join and not two_pass \
+        else flop
+    achieved_k = kflop / (kms / 1e3) / 1e12
+    achieved = achieved_k
     peak = PEAK[w.dtype]
-    traffic = traffic_for(args.workload)
+    traffic = None if w.self_join else traffic_for(args.workload)
     line = {
         "metric": "pair-evaluations/sec",
         "value": value,
@@ -339,7 +348,8 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic (seeded generator, inputs resident in HBM)",
-        "config": {"workload": w.name, "metric": w.metric, "n_p": w.n_p, "n_q": w.n_q, "d": w.d,
+        "config": {"workload": w.name + ("+self-join" if w.self_join else ""),
+                   "metric": w.metric, "n_p": w.n_p, "n_q": w.n_q, "d": w.d,
                    "threshold": w.threshold, "mode": "two-pass" if two_pass else "single-pass",
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak,

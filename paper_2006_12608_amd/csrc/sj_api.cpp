@@ -319,7 +319,10 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     uint64_t total = 0;
     bool emit_from_bits = false;
     if (!blocks) {
-        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, sjk::MODE_SINGLE, g, s));
+        // a self-join computes the upper triangle only and mirrors its pairs
+        const int mode = self && plan.family == sjk::FAM_RESIDENT ? sjk::MODE_TRI
+                                                                  : sjk::MODE_SINGLE;
+        SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, mode, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(hipMemcpyAsync(c->h_small, c->d_small, sizeof(unsigned long long),

@@ -18,10 +18,14 @@ enum Mode {
     MODE_MASK = 3,    // count as MODE_COUNT and keep every result's match bit
                       // (K-streamed kernel only), for an emit pass that reads
                       // the bits instead of recomputing the product
-    MODE_RECORD = 4   // count as MODE_COUNT and append one MatchRecord per
+    MODE_RECORD = 4,  // count as MODE_COUNT and append one MatchRecord per
                       // 32x32 block with matches to the workgroup's own list
                       // (resident kernel only), for an emit pass that reads
                       // the records instead of recomputing
+    MODE_TRI = 5      // single pass of a self-join (Q is P) over the upper
+                      // triangle only: Q tiles below a workgroup's rows are
+                      // skipped, each match (i, j) with i < j is written as
+                      // (i, j) and (j, i), and (i, i) once (resident kernel only)
 };
 
 // The matches of one 32x32 block of results, as found by the first pass of

@@ -277,6 +277,13 @@ constexpr bool counting_mode()
     return MODE == MODE_COUNT || MODE == MODE_RECORD;
 }
 
+// Single-pass modes: pairs staged per wave, slots reserved by atomics.
+template <int MODE>
+constexpr bool single_mode()
+{
+    return MODE == MODE_SINGLE || MODE == MODE_TRI;
+}
+
 // MODE_RECORD: append the block's MatchRecord to the workgroup's list (an LDS
 // counter, so no global atomics in the product loop; records past rec_cap are
 // counted, not written, and the host then recomputes instead of reading them).
@@ -357,7 +364,7 @@ __device__ __forceinline__ void flush_workgroup_out(WaveOut &wo, int wave, int l
 // ib + 8 (r / 4) + r % 4 of this lane, column j): bit r of the returned mask is
 // set iff that result is a match and its row and column exist.  L2 row norms
 // come from `nrow` (LDS: this lane's rows of the block).
-template <int DT, int MET>
+template <int DT, int MET, bool TRI = false>
 __device__ __forceinline__ uint32_t block_mask(const typename Mma<DT>::acc_t &acc, uint32_t ib,
                                                uint32_t j, typename Mma<DT>::val_t ny,
                                                const typename Mma<DT>::val_t *nrow,
@@ -385,7 +392,48 @@ __device__ __forceinline__ uint32_t block_mask(const typename Mma<DT>::acc_t &ac
             valid |= ib + 8 * (r >> 2) + (r & 3) < g.n_p ? (1u << r) : 0u;
         m &= j < g.n_q ? valid : 0u;
     }
+    if constexpr (TRI) {
+        // self-join, upper triangle: only rows i <= j (a block whose last row
+        // is at most its first column needs no test)
+        if (ib0 + 31 > j0) {
+            uint32_t up = 0;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                up |= ib + 8 * (r >> 2) + (r & 3) <= j ? (1u << r) : 0u;
+            m &= up;
+        }
+    }
     return m;
+}
+
+// Single-pass staging of the pairs selected by per-lane masks m (bit r:
+// accumulator register r): the wave's total and each lane's prefix come from
+// five ballots over the lanes' counts, and every lane writes pair(r) for its
+// set bits in register order at its prefix in the wave's LDS buffer (flushed
+// first when the block would not fit).
+template <int MODE, typename F>
+__device__ __forceinline__ void stage_pairs(uint32_t m, int lane, const JoinArgs &g, WaveOut &wo,
+                                            F &&pair)
+{
+    const uint32_t cnt = (uint32_t)__builtin_popcount(m);
+    uint32_t tot = 0, pre = 0;
+#pragma unroll
+    for (int b = 0; b < 5; ++b) {
+        const uint64_t bits = __ballot((cnt >> b) & 1);
+        tot += (uint32_t)__popcll(bits) << b;
+        pre += lanes_below(bits) << b;
+    }
+    if (tot == 0)
+        return;
+    if (wo.fill + tot > wo.cap)
+        flush_wave_out<MODE>(wo, lane, g);
+    uint32_t pos = wo.fill + pre;
+    wo.fill += tot;
+    while (m != 0) {
+        const int r = __builtin_ctz(m);
+        m &= m - 1;
+        wo.buf[pos++] = pair(r);
+    }
 }
 
 // exact_block: the block's match mask (block_mask); per-lane counts give the
@@ -406,7 +454,22 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
     // Opaque to the optimiser: keeps the per-result row indices from being
     // hoisted into (and occupying registers of) the caller's main loop.
     asm volatile("" : "+v"(ib));
-    uint32_t m = block_mask<DT, MET>(acc, ib, j, ny, nrow, g);
+    uint32_t m = block_mask<DT, MET, MODE == MODE_TRI>(acc, ib, j, ny, nrow, g);
+    if constexpr (MODE == MODE_TRI) {
+        // the mirror images (j, i) of the matches off the diagonal, staged
+        // like the block's own pairs
+        uint32_t off = m;
+        const uint32_t ib0 = __builtin_amdgcn_readfirstlane(ib);
+        const uint32_t j0 = __builtin_amdgcn_readfirstlane(j);
+        if (ib0 + 31 > j0) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                off &= ib + 8 * (r >> 2) + (r & 3) == j ? ~(1u << r) : ~0u;
+        }
+        stage_pairs<MODE>(off, lane, g, wo, [&](int r) {
+            return pack_pair(j, ib + 8 * (r >> 2) + (r & 3));
+        });
+    }
     const uint32_t cnt = (uint32_t)__builtin_popcount(m);
     uint32_t tot = 0, pre = 0;
 #pragma unroll
@@ -433,7 +496,7 @@ __device__ __forceinline__ void exact_block(const typename Mma<DT>::acc_t &acc, 
             dst(pos++, pack_pair(ib + 8 * (r >> 2) + (r & 3), j));
         }
     };
-    if (MODE == MODE_SINGLE || wo.cap > 1) {
+    if (single_mode<MODE>() || wo.cap > 1) {
         // staged: the buffer holds at least one whole block
         if (wo.fill + tot > wo.cap)
             flush_wave_out<MODE>(wo, lane, g);
@@ -553,7 +616,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     __shared__ V s_nq0[NEED_NORMS ? BN : 1];
     __shared__ V s_nq1[NEED_NORMS ? BN : 1];
     __shared__ V s_np[NEED_NORMS ? NW : 1][NEED_NORMS ? 32 * WMB : 1];
-    constexpr int OUT_CAP = MODE == MODE_SINGLE ? 1024 : 1;   // a whole 32x32 block
+    constexpr int OUT_CAP = single_mode<MODE>() ? 1024 : 1;   // a whole 32x32 block
     __shared__ uint64_t s_out[NW][OUT_CAP];
     __shared__ uint32_t s_nrec;   // MODE_RECORD: records of this workgroup
 
@@ -562,8 +625,11 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     const uint32_t qsplit = g.qsplit;
     const uint32_t pb = blockIdx.x / qsplit, qs = blockIdx.x - pb * qsplit;
     const uint32_t n_qt = (g.n_q + BN - 1) / BN;
-    const uint32_t t0 = (uint32_t)((uint64_t)qs * n_qt / qsplit);
-    const uint32_t t1 = (uint32_t)((uint64_t)(qs + 1) * n_qt / qsplit);
+    // self-join triangle: tiles whose columns all lie below the workgroup's
+    // first row hold no pair (i, j) with i <= j
+    const uint32_t t_lo = MODE == MODE_TRI ? min(pb * BM / BN, n_qt) : 0u;
+    const uint32_t t0 = t_lo + (uint32_t)((uint64_t)qs * (n_qt - t_lo) / qsplit);
+    const uint32_t t1 = t_lo + (uint32_t)((uint64_t)(qs + 1) * (n_qt - t_lo) / qsplit);
     const uint32_t prow0 = pb * BM + wave * 32 * WMB;
     const uint32_t ibase = prow0 + 4 * half;
 
@@ -779,7 +845,7 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
             }
         }
     }
-    if constexpr (MODE == MODE_SINGLE)
+    if constexpr (single_mode<MODE>())
         flush_workgroup_out<NW>(wo, wave, lane, g);
     if constexpr (MODE == MODE_RECORD) {
         __syncthreads();
@@ -1138,6 +1204,23 @@ hipError_t launch_dtype(const Plan &p, int metric, int mode, const JoinArgs &g, 
                           : launch_resident_v<DT, MET_IP, MODE_RECORD, 2>(p, g, st);
         case 3: return l2 ? launch_resident_v<DT, MET_L2, MODE_RECORD, 3>(p, g, st)
                           : launch_resident_v<DT, MET_IP, MODE_RECORD, 3>(p, g, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
+    if (mode == MODE_TRI) {
+        // resident kernel only
+        if (p.family != FAM_RESIDENT || (metric != MET_IP && metric != MET_L2))
+            return hipErrorInvalidValue;
+        const bool l2 = metric == MET_L2;
+        switch (p.variant) {
+        case 0: return l2 ? launch_resident_v<DT, MET_L2, MODE_TRI, 0>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_TRI, 0>(p, g, st);
+        case 1: return l2 ? launch_resident_v<DT, MET_L2, MODE_TRI, 1>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_TRI, 1>(p, g, st);
+        case 2: return l2 ? launch_resident_v<DT, MET_L2, MODE_TRI, 2>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_TRI, 2>(p, g, st);
+        case 3: return l2 ? launch_resident_v<DT, MET_L2, MODE_TRI, 3>(p, g, st)
+                          : launch_resident_v<DT, MET_IP, MODE_TRI, 3>(p, g, st);
         default: return hipErrorInvalidValue;
         }
     }

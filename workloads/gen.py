@@ -137,6 +137,13 @@ def make_config(name: str, n: int | None = None, seed: int | None = None,
     d = cfg["d"]
     builder = (_ip_f16_small, _ip_bf16, _cos_f16, _l2_i8, _ip_bf16_clustered)[pos]
     w = builder(rng, n, d, _scaled(cfg["planted"], n, n_full), self_join)
+    if self_join and not w.self_join:
+        # the workload's P joined with itself (its planted pairs refer to Q)
+        w.Q = w.P
+        w.self_join = True
+        w.planted = np.zeros((0, 2), np.int64)
+        w.decoys = np.zeros((0, 2), np.int64)
+        w.description += "; Q is P"
     w.name = name if n == n_full else f"{name}@n={n}"
     return w
 
