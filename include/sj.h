@@ -17,7 +17,9 @@
  *     elements), resident in device memory of the context's GPU and owned by
  *     the caller.  Elements are IEEE binary16 (SJ_F16), bfloat16 (SJ_BF16) or
  *     int8 (SJ_I8); inputs must be finite.  P and Q may be the same pointer
- *     (self-join: every ordered pair, (i, i) included).
+ *     (self-join: every ordered pair, (i, i) included; with n_p == n_q the
+ *     single pass then computes only the upper triangle i <= j of the product
+ *     and writes each match (i, j), i < j, also as (j, i)).
  *   - Results are ordered index pairs (i, j), i indexing P and j indexing Q,
  *     both 0-based uint32, stored as interleaved {i, j} (8 bytes per pair) in
  *     the caller's device buffer `pairs` of `cap` pairs (8-byte aligned).

@@ -14,3 +14,4 @@ from .oracle import (  # noqa: F401
     lsh_join,
     JoinResult,
 )
+from . import jl  # noqa: F401,E402
