@@ -171,6 +171,65 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes_per_launch": 256 << 20, "launches": 3}))
 
 
+def jl_chain(d, k, zeta):
+    """Lemma 3's level sizes (k_i, c_i, r_i): k_i = i k (k_l = k), c_1 = zeta k,
+    c_i = zeta k_{i-1}, r_i = zeta^(l - i), zeta^l = d / k."""
+    import math
+    l = int(round(math.log(d / k) / math.log(zeta)))
+    if zeta ** l * k != d:
+        raise SystemExit(f"--jl: d = {d} is not k zeta^l")
+    shapes = []
+    for i in range(1, l + 1):
+        ki = k if i == l else i * k
+        ci = zeta * k if i == 1 else zeta * shapes[-1][0]
+        shapes.append((ki, ci, zeta ** (l - i)))
+    return shapes
+
+
+def bench_jl(args, w, Pd, ctx):
+    """The TCU JL transform of P: one JSON line with its throughput and its
+    HBM roofline (each level reads its input and writes its output once)."""
+    import numpy as np
+    import torch
+    import paper_2006_12608_amd as sj
+    k, zeta = (int(v) for v in args.jl.split(","))
+    shapes = jl_chain(w.d, k, zeta)
+    rng = np.random.default_rng(1400 + __import__("workloads").NAMES.index(args.workload))
+    As = [torch.from_numpy((rng.standard_normal((kk, c)) / np.sqrt(kk)).astype(np.float32)).cuda()
+          for (kk, c, r) in shapes]
+    for _ in range(args.warmup):
+        sj.jl_transform(Pd, shapes, As, ctx=ctx)
+    torch.cuda.synchronize()
+    ms = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        sj.jl_transform(Pd, shapes, As, ctx=ctx)
+        ms.append(sj.sj_get_stats(ctx).ms_join)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) / args.steps * 1e3
+    kms = float(np.mean(ms))
+    esz = 1 if w.dtype == "i8" else 2
+    nbytes = w.n_p * w.d * esz
+    for i, (kk, c, r) in enumerate(shapes):
+        nbytes += w.n_p * r * kk * 4 * (2 if i + 1 < len(shapes) else 1)
+    flop = sum(2.0 * w.n_p * r * kk * c for (kk, c, r) in shapes)
+    print(json.dumps({
+        "metric": "rows reduced/sec (TCU JL transform)",
+        "value": w.n_p / (ms_step / 1e3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32 (inputs " + w.dtype + ")",
+        "data": "synthetic (the workload's P; factors N(0, 1/k_i), seeded)",
+        "config": {"workload": w.name, "n": w.n_p, "d": w.d, "k": k, "zeta": zeta,
+                   "levels": [list(s) for s in shapes], "parallelism": "single GPU"},
+        "phases_ms": {"transform": kms},
+        "flop": flop,
+        "roofline": {"bound": "hbm", "kernel": "jl_level (all levels)", "kernel_ms": kms,
+                     "achieved": nbytes / (kms / 1e3) / 1e9, "peak": 8000.0, "unit": "GB/s",
+                     "frac": nbytes / (kms / 1e3) / 1e9 / 8000.0, "traffic": None,
+                     "algorithmic_bytes": nbytes},
+    }), flush=True)
+
+
 def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
     """The LSH-bucketed join of Theorem 3 on the workload: one JSON line with
     its whole-call throughput, the share of the exact join it finds, its
@@ -252,6 +311,9 @@ def main():
     ap.add_argument("--self-join", action="store_true",
                     help="join the workload's P with itself (same pointer: the single pass "
                          "computes the upper triangle and mirrors its pairs)")
+    ap.add_argument("--jl", default=None, metavar="k,zeta",
+                    help="time the TCU JL transform (sj_jl) of the workload's P to dimension k "
+                         "with Lemma 3's levels for zeta; prints its own JSON line")
     ap.add_argument("--lsh", default=None, metavar="L,k[,w]",
                     help="time the LSH-bucketed join (sj_join_lsh) on the workload instead: "
                          "L tables of k concatenated projections (w = 0: signs; w > 0: "
@@ -285,6 +347,9 @@ def main():
     flags = sj.SJ_FLAG_TIMING | (sj.SJ_FLAG_TWO_PASS if two_pass else 0)
     fn = sj.sj_join_ip if w.metric == "ip" else sj.sj_join_l2
 
+    if args.jl:
+        bench_jl(args, w, Pd, ctx)
+        return
     total = sj.count(Pd, Qd, w.threshold, w.metric, ctx=ctx)
     if args.lsh:
         bench_lsh(args, w, Pd, Qd, ctx, total)

@@ -175,6 +175,25 @@ int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p,
                 const int32_t *B, int32_t w, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
                 uint64_t *n_cand);
 
+/* TCU Johnson-Lindenstrauss transform (Lemma 3 / Theorem 2): the reduced
+ * rows Y_j = M X_j of the n rows of X (n x d, row-major, dtype as the joins,
+ * device) with
+ *   M = (I_{r_l} (x) A_l) ... (I_{r_1} (x) A_1),
+ * where A_i is k_i x c_i and I_r (x) A_i applies A_i to each of r consecutive
+ * blocks of c_i entries.  shape (host) holds (k_i, c_i, r_i) for i = 1..l
+ * (`levels` = l, at most 32); the sizes must chain as d = r_1 c_1 and
+ * r_i k_i = r_{i+1} c_{i+1}; the output dimension is r_l k_l.  A (device,
+ * fp32) holds A_1, ..., A_l one after the other, each row-major.  Y (device,
+ * fp32) receives n x (r_l k_l) values.  Each level is one fp32 product on the
+ * matrix cores (inputs decoded exactly to fp32; intermediate levels in fp32
+ * device scratch of at most 2 n max_i(r_i k_i) floats).  The JL guarantee
+ * (norms kept within 1 +- eps with probability 1 - delta) is a property of
+ * the caller's A_i (e.g. i.i.d. N(0, 1/k_i) entries), not of this call.
+ * Errors as sj_join_ip (SJ_E_INVAL for a broken size chain); afterwards
+ * sj_get_stats reports ms_join = the transform's GPU time. */
+int sj_jl(sj_ctx *ctx, int dtype, const void *X, uint32_t n, uint32_t d, uint32_t levels,
+          const uint32_t *shape, const float *A, float *Y);
+
 /* Free the context and its scratch; NULL is a no-op. */
 void sj_destroy(sj_ctx *ctx);
 

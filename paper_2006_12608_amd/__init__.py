@@ -61,6 +61,8 @@ def _load():
                                 ctypes.c_int32, vp, u64, ctypes.POINTER(u64),
                                 ctypes.POINTER(u64)]
     lib.sj_join_lsh.restype = i32
+    lib.sj_jl.argtypes = [vp, i32, vp, u32, u32, u32, vp, vp, vp]
+    lib.sj_jl.restype = i32
     lib.sj_destroy.argtypes = [vp]
     lib.sj_destroy.restype = None
     lib.sj_get_stats.argtypes = [vp, ctypes.POINTER(sj_stats)]
@@ -122,6 +124,14 @@ def sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, L, k, A, B, w, pairs
     st = lib.sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, float(thr), L, k, A, B, int(w),
                          pairs, cap, ctypes.byref(n), ctypes.byref(nc))
     return st, n.value, nc.value
+
+
+def sj_jl(ctx, dtype, X, n, d, levels, shape, A, Y):
+    """Returns the status; shape is a sequence of (k_i, c_i, r_i), pointers
+    are integers (device addresses)."""
+    flat = [int(v) for s in shape for v in s]
+    arr = (ctypes.c_uint32 * max(len(flat), 1))(*flat)
+    return lib.sj_jl(ctx, dtype, X, n, d, levels, arr, A, Y)
 
 
 def sj_get_stats(ctx) -> sj_stats:
@@ -254,3 +264,28 @@ def join_lsh(P, Q, thr: float, metric: str = "ip", *, L: int, k: int, A, B=None,
     if st != SJ_OK:
         raise SjError(st, sj_last_error(), n)
     return out[:n], nc
+
+
+def jl_transform(X, shapes, As, ctx=None):
+    """TCU Johnson-Lindenstrauss transform (sj_jl): the rows of X (n x d device
+    tensor: float16, bfloat16 or int8) reduced by M = (I_{r_l} (x) A_l) ...
+    (I_{r_1} (x) A_1); shapes is the list of (k_i, c_i, r_i), As the list of
+    k_i x c_i float32 device tensors.  Returns an (n, r_l k_l) float32 tensor."""
+    import torch
+    if X.dim() != 2 or not X.is_cuda or not X.is_contiguous():
+        raise ValueError("X must be a contiguous 2-D device tensor")
+    shapes = [tuple(int(v) for v in s) for s in shapes]
+    if len(As) != len(shapes):
+        raise ValueError("one factor per level")
+    for (k, c, r), A in zip(shapes, As):
+        if tuple(A.shape) != (k, c) or A.dtype != torch.float32 or not A.is_cuda:
+            raise ValueError(f"factor of shape {(k, c)} float32 on the device expected")
+    Acat = torch.cat([A.reshape(-1) for A in As]).contiguous()
+    out_dim = shapes[-1][0] * shapes[-1][2]
+    Y = torch.empty((X.shape[0], out_dim), dtype=torch.float32, device=X.device)
+    ctx = ctx or context(X.device.index)
+    st = sj_jl(ctx, dtype_code(X), X.data_ptr(), X.shape[0], X.shape[1], len(shapes), shapes,
+               Acat.data_ptr(), Y.data_ptr())
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return Y
