@@ -7,8 +7,8 @@
 // product, and the result (n r_i rows of k_i entries) read back as n rows of
 // r_i k_i entries is the next level's input -- no data moves between levels.
 // Each level is one fp32 product Y = X A_i^T on the matrix cores
-// (v_mfma_f32_32x32x2_f32); the first level decodes fp16 / bf16 / int8 rows
-// exactly to fp32.
+// (v_mfma_f32_32x32x2_f32) with its operands staged through LDS; the first
+// level decodes fp16 / bf16 / int8 rows exactly to fp32.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -23,6 +23,32 @@ using sjk::DT_I8;
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int SRC_F32 = 0;
+
+// Four consecutive entries from idx (idx a multiple of 4, the row 4-entry
+// aligned) decoded to fp32.
+template <int SRC>
+__device__ __forceinline__ void load4(const void *X, uint64_t idx, float (&v)[4])
+{
+    if constexpr (SRC == SRC_F32) {
+        const float4 f = *(const float4 *)((const float *)X + idx);
+        v[0] = f.x, v[1] = f.y, v[2] = f.z, v[3] = f.w;
+    } else if constexpr (SRC == DT_I8) {
+        const uint32_t w = *(const uint32_t *)((const int8_t *)X + idx);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            v[j] = (float)(int8_t)(w >> (8 * j));
+    } else {
+        const uint2 w = *(const uint2 *)((const uint16_t *)X + idx);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t hbits = ((j < 2 ? w.x : w.y) >> (16 * (j & 1))) & 0xffffu;
+            if constexpr (SRC == DT_F16)
+                v[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)hbits);
+            else
+                v[j] = __builtin_bit_cast(float, hbits << 16);
+        }
+    }
+}
 
 template <int SRC>
 __device__ __forceinline__ float load_elem(const void *X, uint64_t idx)
@@ -39,40 +65,77 @@ __device__ __forceinline__ float load_elem(const void *X, uint64_t idx)
     }
 }
 
-// Column blocks of 32 a wave keeps accumulators for at once.
+// Column blocks of 32 a wave keeps accumulators for at once, rows per
+// workgroup tile and entries of K per LDS chunk.
 constexpr int NCB = 4;
+constexpr int TR = 128;
+constexpr int KC = 32;
+constexpr int XS = KC + 1;   // LDS row stride (floats): lanes of a fragment read distinct banks
 
-// Y (rows x N, fp32) = X (rows x K) A^T, A N x K fp32 row-major.  A wave owns
-// 32 rows and sweeps the columns NCB blocks of 32 at a time; per k-step
-// (two entries of K) lane l supplies X[row l % 32][k + l / 32] and
-// A[column l % 32][k + l / 32].  Rows past `rows`, columns past N and entries
-// past K read as zero; results outside rows x N are not stored.
-template <int SRC>
+// Y (rows x N, fp32) = X (rows x K) A^T, A N x K fp32 row-major.  A workgroup
+// of 4 waves owns TR rows; for each group of NCB column blocks it walks K in
+// chunks of KC entries, staging the chunk of its TR rows and of the group's
+// rows of A in LDS as fp32 (consecutive threads load consecutive entries of
+// a row: coalesced), and wave w multiplies rows 32 w .. 32 w + 31 on the
+// matrix cores (per k-step, lane l supplies X[row l % 32][k + l / 32] and
+// A[column l % 32][k + l / 32]).  Entries past the matrices read as zero;
+// results outside rows x N are not stored.
+template <int SRC, bool VEC>
 __global__ void __launch_bounds__(256) jl_level(const void *X, uint64_t rows, uint32_t K,
                                                 const float *A, uint32_t N, float *Y)
 {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __shared__ float sx[TR * XS];
+    __shared__ float sa[32 * NCB * XS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int h = lane >> 5, c32 = lane & 31;
-    const uint64_t row0 = ((uint64_t)blockIdx.x * 4 + wave) * 32;
-    if (row0 >= rows)
-        return;
-    const uint64_t row = row0 + c32;
-    const bool rok = row < rows;
+    const uint64_t tile0 = (uint64_t)blockIdx.x * TR;
+    const uint64_t row0 = tile0 + 32 * wave;
     for (uint32_t cb0 = 0; cb0 < N; cb0 += 32 * NCB) {
         f32x16 acc[NCB];
 #pragma unroll
         for (int b = 0; b < NCB; ++b)
             acc[b] = f32x16{};
-        for (uint32_t k = 0; k < K; k += 2) {
-            const uint32_t kk = k + h;
-            const float a = rok && kk < K ? load_elem<SRC>(X, row * K + kk) : 0.0f;
+        for (uint32_t k0 = 0; k0 < K; k0 += KC) {
+            __syncthreads();   // the previous chunk is consumed
+            if constexpr (VEC) {
+                // K is a multiple of 4 and X aligned for 4-entry loads
 #pragma unroll
-            for (int b = 0; b < NCB; ++b) {
-                const uint32_t col = cb0 + 32 * b + c32;
-                if (cb0 + 32 * b < N) {   // uniform
-                    const float bv = col < N && kk < K ? A[(uint64_t)col * K + kk] : 0.0f;
-                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc[b], 0, 0, 0);
+                for (int q = tid; q < TR * KC / 4; q += 256) {
+                    const int r = q / (KC / 4), e = 4 * (q % (KC / 4));
+                    const uint64_t row = tile0 + r;
+                    const uint32_t k = k0 + e;
+                    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (row < rows && k < K)
+                        load4<SRC>(X, row * K + k, v);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        sx[r * XS + e + j] = v[j];
                 }
+            } else {
+#pragma unroll
+                for (int q = tid; q < TR * KC; q += 256) {
+                    const int r = q / KC, e = q % KC;
+                    const uint64_t row = tile0 + r;
+                    const uint32_t k = k0 + e;
+                    sx[r * XS + e] = row < rows && k < K ? load_elem<SRC>(X, row * K + k) : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int q = tid; q < 32 * NCB * KC; q += 256) {
+                const int r = q / KC, e = q % KC;
+                const uint32_t col = cb0 + r, k = k0 + e;
+                sa[r * XS + e] = col < N && k < K ? A[(uint64_t)col * K + k] : 0.0f;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int ks = 0; ks < KC / 2; ++ks) {
+                const float a = sx[(32 * wave + c32) * XS + 2 * ks + h];
+#pragma unroll
+                for (int b = 0; b < NCB; ++b)
+                    if (cb0 + 32 * b < N) {   // uniform
+                        const float bv = sa[(32 * b + c32) * XS + 2 * ks + h];
+                        acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc[b], 0, 0, 0);
+                    }
             }
         }
         // register r of lane l: (row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32)
@@ -95,9 +158,15 @@ template <int SRC>
 hipError_t launch_level_t(const void *X, uint64_t rows, uint32_t K, const float *A, uint32_t N,
                           float *Y, hipStream_t s)
 {
-    const uint64_t blocks = (rows + 127) / 128;
-    hipLaunchKernelGGL(jl_level<SRC>, dim3((uint32_t)blocks), dim3(256), 0, s, X, rows, K, A, N,
-                       Y);
+    const uint64_t blocks = (rows + TR - 1) / TR;
+    const size_t esz = SRC == SRC_F32 ? 4 : SRC == DT_I8 ? 1 : 2;
+    const bool vec = K % 4 == 0 && (uintptr_t)X % (4 * esz) == 0;
+    if (vec)
+        hipLaunchKernelGGL((jl_level<SRC, true>), dim3((uint32_t)blocks), dim3(256), 0, s, X, rows,
+                           K, A, N, Y);
+    else
+        hipLaunchKernelGGL((jl_level<SRC, false>), dim3((uint32_t)blocks), dim3(256), 0, s, X,
+                           rows, K, A, N, Y);
     return hipGetLastError();
 }
 
