@@ -343,8 +343,8 @@ __device__ __forceinline__ bool matches(typename sjk::Mma<DT>::val_t acc,
     }
 }
 
-// A workgroup of 4 waves takes TILE x TILE tiles of bucket pairs
-// (grid-stride): the tile's rows of P and Q are gathered through the tables'
+// A workgroup of 4 waves takes a contiguous range of the TILE x TILE tiles of
+// the bucket pairs: the tile's rows of P and Q are gathered through the tables'
 // sorted permutations into LDS in chunks of 128 bytes of each row (16-byte
 // chunks, rows padded by one chunk), wave (wr, wc) multiplies its 64 x 64
 // quarter (2 x 2 blocks of 32 x 32: per k-step two A- and two B-fragments for
@@ -367,21 +367,36 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
     const uint32_t rb = g.P.row_bytes;   // == g.Q.row_bytes
     const uint32_t lc = tid & 7, lr = tid >> 3;   // load chunk; rows lr + 32 e
 
-    for (uint64_t T = blockIdx.x; T < g.n_tiles; T += gridDim.x) {
-        uint32_t lo = 0, hi = g.n_bp;
-        while (hi - lo > 1) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if (g.tile0[mid] <= T)
-                lo = mid;
+    // a contiguous range of tiles per workgroup: one search for its first
+    // tile's bucket pair, then a walk (consecutive tiles of a pair share rows)
+    const uint64_t per = (g.n_tiles + gridDim.x - 1) / gridDim.x;
+    const uint64_t T0 = (uint64_t)blockIdx.x * per;
+    const uint64_t T1 = min(T0 + per, g.n_tiles);
+    if (T0 >= T1)
+        return;   // the whole workgroup: no barrier is skipped by part of it
+    uint32_t slot = 0;
+    {
+        uint32_t hi = g.n_bp;
+        while (hi - slot > 1) {
+            const uint32_t mid = (slot + hi) >> 1;
+            if (g.tile0[mid] <= T0)
+                slot = mid;
             else
                 hi = mid;
         }
-        const uint4 h = g.head[lo];
-        const uint32_t t = h.x, nq = g.nq[lo];
-        const uint64_t local = T - g.tile0[lo];
+    }
+    uint64_t local = T0 - g.tile0[slot];
+    for (uint64_t T = T0; T < T1; ++T) {
+        const uint4 h = g.head[slot];
+        const uint32_t t = h.x, nq = g.nq[slot];
         const uint32_t ntq = (nq + TILE - 1) / TILE;
+        const uint32_t ntp = (h.z + TILE - 1) / TILE;
         const uint32_t tp = (uint32_t)(local / ntq), tq = (uint32_t)(local % ntq);
         const uint32_t rows_p = min(h.z - tp * TILE, TILE), rows_q = min(nq - tq * TILE, TILE);
+        if (++local == (uint64_t)ntp * ntq) {   // the next tile starts the next pair
+            ++slot;
+            local = 0;
+        }
 
         __syncthreads();   // the previous tile's reads of sIP/sIQ/sA/sB are done
         if (tid < (int)TILE) {
@@ -413,16 +428,20 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
                 acc[a][b] = acc_t{};
-        for (uint32_t kc = 0; kc < rb; kc += 128) {
+        // the next chunk's loads are issued before this chunk's MFMAs
+        i32x4 la[LPT], lb[LPT];
+        auto fetch = [&](uint32_t kc) {
             const uint32_t off = kc + 16 * lc;
             const i32x4 z = {0, 0, 0, 0};
             const bool in = off < rb;
-            i32x4 la[LPT], lb[LPT];
 #pragma unroll
             for (int e = 0; e < LPT; ++e) {
                 la[e] = va[e] && in ? *(const i32x4 *)(pa[e] + off) : z;
                 lb[e] = vb[e] && in ? *(const i32x4 *)(pb[e] + off) : z;
             }
+        };
+        fetch(0);
+        for (uint32_t kc = 0; kc < rb; kc += 128) {
             if (kc)
                 __syncthreads();   // the previous chunk's fragments are read
 #pragma unroll
@@ -431,6 +450,8 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
                 sB[(lr + 32 * e) * CS + lc] = lb[e];
             }
             __syncthreads();
+            if (kc + 128 < rb)
+                fetch(kc + 128);
             const uint32_t nks = min(4u, (rb - kc + 31) / 32);
 #pragma unroll
             for (uint32_t ks = 0; ks < 4; ++ks)
