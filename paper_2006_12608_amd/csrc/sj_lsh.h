@@ -33,6 +33,20 @@ hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_
                        const void *Aw, const int32_t *B, int32_t w, uint32_t tshift,
                        uint64_t *keys, hipStream_t s);
 
+// The same keys with the projections on the matrix cores (fp16 / bf16 rows of
+// at most 512 bytes, L k <= 256, k >= 2 for quantised hashes:
+// keys_fast_applies): decisions the fp32 sums make certain are kept, the
+// other (row, table) keys are recomputed exactly.  `ws` is workspace of
+// keys_fast_bytes(n_max, L, k, row_bytes) bytes whose first part (the fp16 /
+// bf16 projection rows and their norms) is filled when `widen` is set and
+// reused otherwise; `nfix` a zeroed device counter per call; Aw as launch_keys.
+bool keys_fast_applies(int dtype, uint32_t row_bytes, uint32_t L, uint32_t k, int32_t w);
+size_t keys_fast_bytes(uint32_t n_max, uint32_t L, uint32_t k, uint32_t row_bytes);
+hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
+                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
+                            uint32_t tshift, uint64_t *keys, void *ws, bool widen,
+                            unsigned long long *nfix, hipStream_t s);
+
 // Sorts each table's keys with the row indices as values (n rows per table):
 // sorted[t * n + p], perm[t * n + p] = the p-th smallest key of table t and its
 // row.  joint: the keys carry their table above `bits` and one sort of all

@@ -250,6 +250,200 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
     }
 }
 
+// ------------------------------------------------ keys on the matrix cores
+//
+// For fp16 / bf16 rows of at most 512 bytes and at most HF_MAX functions in
+// all: the projections z_f(x) of 32 rows by 32 functions come from one MFMA
+// block (fp16 / bf16 products are exact in fp32, the sums are rounded).  A
+// decision (sign, or floor((z + B) / w)) is taken from the fp32 value only when
+// it is certain: the fp32 sum and the double sum in ascending m both differ
+// from the exact sum by at most gamma(d) sum_m |A_m x_m| <= gamma(d) ||A|| ||x||
+// (any summation order; gamma(d) = d u / (1 - d u)), so when |z| exceeds twice
+// the sum of both bounds the sign is the double sum's, and when the interval
+// z +- that margin maps to one bucket the quantised value is.  A (row, table)
+// with any uncertain function is queued and its key recomputed with the exact
+// double evaluation (fix_kernel), so the keys equal keys_kernel's.
+constexpr int HF_MAX = 256;
+
+template <int DT>
+__global__ void widen_h_kernel(const int8_t *A, uint16_t *Ah, uint32_t d, uint32_t rl,
+                               uint64_t n_out)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n_out) {
+        const uint64_t f = i / rl, m = i - f * rl;
+        const float a = m < d ? (float)A[f * d + m] : 0.0f;   // |a| <= 128: exact in both
+        if constexpr (DT == DT_F16)
+            Ah[i] = __builtin_bit_cast(uint16_t, (_Float16)a);
+        else
+            Ah[i] = (uint16_t)(__builtin_bit_cast(uint32_t, a) >> 16);
+    }
+}
+
+// Upper bounds of Euclidean norms: rows of A (int8, d entries) or of X
+// (stored rows); the double sum is rounded up by a relative 2^-20.
+__global__ void anorm_kernel(const int8_t *A, uint32_t d, uint32_t n_fn, float *out)
+{
+    const uint32_t f = blockIdx.x * 256 + threadIdx.x;
+    if (f < n_fn) {
+        double s = 0.0;
+        for (uint32_t m = 0; m < d; ++m)
+            s += (double)A[(uint64_t)f * d + m] * A[(uint64_t)f * d + m];
+        out[f] = (float)(sqrt(s) * (1.0 + 0x1p-20));
+    }
+}
+
+template <int DT>
+__global__ void xnorm_kernel(Rows r, uint32_t d, float *out)
+{
+    const uint32_t row = blockIdx.x * 256 + threadIdx.x;
+    if (row < r.n) {
+        const uint8_t *x = r.X + (size_t)row * r.row_bytes;
+        double s = 0.0;
+        for (uint32_t c = 0; c < padded_d<DT>(d) / Chunk<DT>::E; ++c) {
+            const i32x4 v = *(const i32x4 *)(x + 16 * c);
+#pragma unroll
+            for (int e = 0; e < Chunk<DT>::E; ++e) {
+                const double xe = (double)Chunk<DT>::at(v, e);
+                s += xe * xe;
+            }
+        }
+        out[row] = (float)(sqrt(s) * (1.0 + 0x1p-20));
+    }
+}
+
+// A wave takes 32 rows (A-fragments of KS k-steps in registers) and sweeps the
+// L k functions in MFMA blocks of 32; each lane folds its function's value
+// into the (row, table) key in LDS (64-bit atomic OR), and marks uncertain
+// ones; then the wave writes the keys and queues the uncertain (row, table).
+template <int DT, int KS>
+__global__ void __launch_bounds__(256) keys_mfma_kernel(
+    Rows r, uint32_t L, uint32_t k, const uint8_t *Ah, const float *anorm, const float *xnorm,
+    const int32_t *B, int32_t w, uint32_t tshift, float gam, uint64_t *keys, uint2 *fix,
+    unsigned long long *nfix)
+{
+    typedef sjk::Mma<DT> M;
+    typedef typename M::acc_t acc_t;
+    __shared__ unsigned long long skey[4][32 * 64];
+    __shared__ unsigned long long sflag[4][32];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int h = lane >> 5, c32 = lane & 31;
+    const uint32_t row0 = (blockIdx.x * 4 + wave) * 32;
+    const uint32_t nf = L * k;
+    const uint32_t beta = 64 / k;
+    const uint64_t low = beta >= 64 ? ~0ull : (1ull << beta) - 1;
+    unsigned long long *kk = skey[wave];
+    for (uint32_t i = lane; i < 32 * L; i += 64)
+        kk[i] = 0ull;
+    if (lane < 32)
+        sflag[wave][lane] = 0ull;
+    i32x4 af[KS];
+    const uint32_t arow = row0 + c32;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const uint32_t off = 32 * ks + 16 * h;
+        af[ks] = arow < r.n && off < r.row_bytes
+                     ? *(const i32x4 *)(r.X + (size_t)arow * r.row_bytes + off)
+                     : i32x4{0, 0, 0, 0};
+    }
+    float xn[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        const uint32_t R = row0 + 8 * (q >> 2) + 4 * h + (q & 3);
+        xn[q] = R < r.n ? xnorm[R] : 0.0f;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (uint32_t f0 = 0; f0 < nf; f0 += 32) {
+        const uint32_t f = f0 + c32;
+        acc_t acc = acc_t{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const uint32_t off = 32 * ks + 16 * h;
+            const i32x4 b = f < nf && off < r.row_bytes
+                                ? *(const i32x4 *)(Ah + (size_t)f * r.row_bytes + off)
+                                : i32x4{0, 0, 0, 0};
+            acc = M::mma(af[ks], b, acc);
+        }
+        if (f >= nf)
+            continue;
+        const uint32_t t = f / k, u = f - t * k;
+        const float na = anorm[f];
+        const double bf = w > 0 ? (double)B[f] : 0.0;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int Rl = 8 * (q >> 2) + 4 * h + (q & 3);
+            const float z = acc[q];
+            const float e = gam * na * xn[q];
+            uint64_t contrib;
+            bool sure;
+            if (w == 0) {
+                sure = __builtin_fabsf(z) > e;
+                contrib = (uint64_t)(z >= 0.0f) << u;
+            } else {
+                const double lo = floor(((double)z - (double)e + bf) / (double)w);
+                const double hi = floor(((double)z + (double)e + bf) / (double)w);
+                sure = lo == hi;
+                contrib = ((uint64_t)(int64_t)lo & low) << (beta * u);
+            }
+            if (sure)
+                atomicOr(&kk[Rl * L + t], (unsigned long long)contrib);
+            else
+                atomicOr(&sflag[wave][Rl], 1ull << t);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    for (uint32_t i = lane; i < 32 * L; i += 64) {
+        const uint32_t Rl = i / L, t = i - Rl * L;
+        const uint32_t R = row0 + Rl;
+        if (R >= r.n)
+            continue;
+        keys[(size_t)t * r.n + R] = kk[i] | (tshift ? (uint64_t)t << tshift : 0ull);
+        if ((sflag[wave][Rl] >> t) & 1) {
+            const unsigned long long slot = atomicAdd(nfix, 1ull);
+            fix[slot] = make_uint2(R, t);
+        }
+    }
+}
+
+// The queued (row, table) keys, recomputed exactly as keys_kernel does (one
+// thread per entry, the row read from global memory; grid-stride over the
+// queue's length, read from device memory).
+template <int DT>
+__global__ void __launch_bounds__(256) fix_kernel(Rows r, uint32_t d, uint32_t k,
+                                                  const typename Chunk<DT>::a_t *A,
+                                                  const int32_t *B, int32_t w, uint32_t tshift,
+                                                  const uint2 *fix,
+                                                  const unsigned long long *nfix, uint64_t *keys)
+{
+    typedef Chunk<DT> C;
+    typedef typename C::acc_t acc_t;
+    const uint64_t n_fix = *nfix;
+    const uint32_t dp = padded_d<DT>(d), nch = dp / C::E;
+    const uint32_t beta = k ? 64 / k : 64;
+    const uint64_t low = beta >= 64 ? ~0ull : (1ull << beta) - 1;
+    for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < n_fix;
+         i += (uint64_t)gridDim.x * 256) {
+        const uint2 e = fix[i];
+        const uint32_t row = e.x, t = e.y;
+        const uint8_t *x = r.X + (size_t)row * r.row_bytes;
+        uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
+        for (uint32_t u = 0; u < k; ++u) {
+            const typename C::a_t *a = A + (size_t)(t * k + u) * dp;
+            acc_t z = acc_t(0);
+            for (uint32_t c = 0; c < nch; ++c) {
+                const i32x4 v = *(const i32x4 *)(x + 16 * c);
+#pragma unroll
+                for (int m = 0; m < C::E; ++m)
+                    z += acc_t(a[c * C::E + m]) * C::at(v, m);
+            }
+            fold_value(key, z, u, beta, low, B, t * k + u, w);
+        }
+        keys[(size_t)t * r.n + row] = key;
+    }
+}
+
 // v[i] = i mod n for i < total (the row of entry i of table-major arrays).
 __global__ void iota_kernel(uint32_t *v, uint32_t n, uint32_t total)
 {
@@ -598,6 +792,82 @@ hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_
     default:
         return launch_keys_t<DT_I8>(r, d, L, k, Aw, B, w, tshift, keys, s);
     }
+}
+
+bool keys_fast_applies(int dtype, uint32_t row_bytes, uint32_t L, uint32_t k, int32_t w)
+{
+    return (dtype == DT_F16 || dtype == DT_BF16) && row_bytes <= 512 && k >= 1 &&
+           (uint64_t)L * k <= HF_MAX && L <= 64 && (w == 0 || k >= 2);
+}
+
+size_t keys_fast_bytes(uint32_t n_max, uint32_t L, uint32_t k, uint32_t row_bytes)
+{
+    // fp16 / bf16 projection rows, their norms, row norms, the fix queue
+    return (size_t)L * k * row_bytes + 256 + (size_t)L * k * 4 + 256 + (size_t)n_max * 4 + 256 +
+           (size_t)L * n_max * 8;
+}
+
+template <int DT, int KS>
+static void launch_mfma_t(const Rows &r, uint32_t L, uint32_t k, const uint8_t *Ah,
+                          const float *an, const float *xn, const int32_t *B, int32_t w,
+                          uint32_t tshift, float gam, uint64_t *keys, uint2 *fix,
+                          unsigned long long *nfix, hipStream_t s)
+{
+    hipLaunchKernelGGL((keys_mfma_kernel<DT, KS>), dim3((r.n + 127) / 128), dim3(256), 0, s, r,
+                       L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix);
+}
+
+template <int DT>
+static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
+                              const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
+                              uint32_t tshift, uint64_t *keys, uint8_t *ws, bool widen,
+                              unsigned long long *nfix, hipStream_t s)
+{
+    const uint32_t nf = L * k;
+    uint8_t *Ah = ws;
+    float *an = (float *)(ws + (((size_t)nf * r.row_bytes + 255) & ~(size_t)255));
+    float *xn = (float *)((uint8_t *)an + (((size_t)nf * 4 + 255) & ~(size_t)255));
+    uint2 *fix = (uint2 *)((uint8_t *)xn + (((size_t)r.n * 4 + 255) & ~(size_t)255));
+    if (widen) {
+        const uint32_t rl = r.row_bytes / 2;
+        const uint64_t n_out = (uint64_t)nf * rl;
+        hipLaunchKernelGGL(widen_h_kernel<DT>, dim3((unsigned)((n_out + 255) / 256)), dim3(256),
+                           0, s, A, (uint16_t *)Ah, d, rl, n_out);
+        hipLaunchKernelGGL(anorm_kernel, dim3((nf + 255) / 256), dim3(256), 0, s, A, d, nf, an);
+    }
+    hipLaunchKernelGGL(xnorm_kernel<DT>, dim3((r.n + 255) / 256), dim3(256), 0, s, r, d, xn);
+    // twice the fp32 and double summation bounds for d terms
+    const double dd = d ? (double)d : 1.0;
+    const double g24 = dd * 0x1p-24 / (1.0 - dd * 0x1p-24);
+    const double g53 = dd * 0x1p-53 / (1.0 - dd * 0x1p-53);
+    const float gam = (float)(2.0 * (g24 + g53) * (1.0 + 0x1p-10));
+    const uint32_t ks = (r.row_bytes + 31) / 32;
+    if (ks <= 2)
+        launch_mfma_t<DT, 2>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+    else if (ks <= 4)
+        launch_mfma_t<DT, 4>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+    else if (ks <= 8)
+        launch_mfma_t<DT, 8>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+    else
+        launch_mfma_t<DT, 16>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+    hipLaunchKernelGGL(fix_kernel<DT>, dim3(512), dim3(256), 0, s, r, d, k,
+                       (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, fix,
+                       (const unsigned long long *)nfix, keys);
+    return hipGetLastError();
+}
+
+hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
+                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
+                            uint32_t tshift, uint64_t *keys, void *ws, bool widen,
+                            unsigned long long *nfix, hipStream_t s)
+{
+    if (r.n == 0)
+        return hipSuccess;
+    if (dtype == DT_F16)
+        return keys_fast_t<DT_F16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+                                   nfix, s);
+    return keys_fast_t<DT_BF16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+                                nfix, s);
 }
 
 hipError_t launch_widen(int dtype, const int8_t *A, uint32_t n_fn, uint32_t d, void *out,

@@ -115,9 +115,12 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_head = take((size_t)bp_cap * 16);
     const size_t off_bnq = take((size_t)bp_cap * 4);
     const size_t off_t0 = take((size_t)bp_cap * 8);
-    const size_t off_cnt = take(4 * 8);
+    const size_t off_cnt = take(6 * 8);
     const size_t off_temp = take(temp_bytes);
     const size_t off_aw = take(a_bytes);
+    // keys on the matrix cores where they apply
+    const bool fast = sjl::keys_fast_applies(dtype, (uint32_t)krow, L, k, w);
+    const size_t off_ws = fast ? take(sjl::keys_fast_bytes((uint32_t)n_max, L, k, (uint32_t)krow)) : 0;
     if ((st = grow_scratch(c, need)) != SJ_OK)
         return st;
     uint8_t *scr = (uint8_t *)c->scratch;
@@ -127,7 +130,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     sjl::Rows rp{aligned ? (const uint8_t *)P : scr + off_rp, n_p, (uint32_t)krow};
     sjl::Rows rq{aligned ? (const uint8_t *)Q : scr + off_rq, n_q, (uint32_t)krow};
     unsigned long long *cnt = (unsigned long long *)(scr + off_cnt);
-    SJ_HIP(hipMemsetAsync(cnt, 0, 4 * 8, s));
+    SJ_HIP(hipMemsetAsync(cnt, 0, 6 * 8, s));
     SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
     SJ_HIP(hipEventRecord(c->ev[0], s));
     if (!aligned) {
@@ -144,9 +147,17 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     }
     uint64_t *keys_p = (uint64_t *)(scr + off_kp), *keys_q = (uint64_t *)(scr + off_kq);
     SJ_HIP(sjl::launch_widen(dtype, A, L * k, d, scr + off_aw, s));
-    SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, scr + off_aw, B, w, tshift, keys_p, s));
-    if (!self)
-        SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, tshift, keys_q, s));
+    if (fast) {
+        SJ_HIP(sjl::launch_keys_fast(dtype, rp, d, L, k, A, scr + off_aw, B, w, tshift, keys_p,
+                                     scr + off_ws, true, cnt + 3, s));
+        if (!self)
+            SJ_HIP(sjl::launch_keys_fast(dtype, rq, d, L, k, A, scr + off_aw, B, w, tshift,
+                                         keys_q, scr + off_ws, false, cnt + 4, s));
+    } else {
+        SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, scr + off_aw, B, w, tshift, keys_p, s));
+        if (!self)
+            SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, tshift, keys_q, s));
+    }
     SJ_HIP(hipEventRecord(c->ev[1], s));
     uint64_t *sorted_p = (uint64_t *)(scr + off_sp), *sorted_q = (uint64_t *)(scr + off_sq);
     uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
