@@ -2,13 +2,15 @@
 pair set, on seeded inputs and seeded LSH draws.
 
 The bucket keys are integers computed exactly (or in double precision in the
-same order) on both sides, so the candidate sets agree exactly; the exact
-test then follows the all-pairs join's rules: identical sets for
-integer-valued inputs, identical outside the boundary band for real-valued
-ones.  Cases cover both hash families, every dtype, both metrics, ragged
-sizes against the 64-row tiles, buckets spanning several tiles, unaligned
-rows, the self-join, k = 0 (the exact join), the first-table rule (no
-duplicates), the candidate count, overflow and argument errors.
+same order) on both sides -- the GPU's matrix-core hash keeps only the
+decisions its fp32 sums make certain and recomputes the rest that way -- so
+the candidate sets agree exactly; the exact test then follows the all-pairs
+join's rules: identical sets for integer-valued inputs, identical outside the
+boundary band for real-valued ones.  Cases cover both hash families, every
+dtype, both metrics, ragged sizes against the 128-row tiles, buckets
+spanning several tiles, unaligned rows, the self-join, k = 0 (the exact
+join), the first-table rule (no duplicates), decisions the fp32 hash cannot
+take, the candidate count, overflow and argument errors.
 """
 import sys
 
@@ -191,3 +193,31 @@ def test_lsh_cosine_workload_recall():
     say("pairs", len(g), "exact", exact.total, "candidates", cand, "band", info)
     assert cand < wl.n_p * wl.n_q // 8
     assert len(ref) >= 0.9 * exact.total
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("wid", [0, 5])
+def test_lsh_uncertain_decisions_are_exact(dtype, wid):
+    """Rows built so that many projections are exactly zero (sign hashes) or
+    land exactly on a bucket boundary (width 5): the matrix-core hash cannot
+    decide those from its fp32 sums and recomputes them exactly; the pairs must
+    still be the oracle's, and the same integer points stored as int8 (which
+    take the exact int32 hash throughout) must give the same pairs."""
+    import paper_2006_12608_amd as sj
+    import torch
+    rng = np.random.default_rng(91 + wid)
+    d, L, k = 32, 6, 4
+    h = workloads.lsh_params(92, L=L, k=k, d=d, w=wid)
+    h.A[:, 16:] = 0                       # projections see only the first 16 coordinates
+    x = rng.integers(-3, 4, size=(400, d))
+    x[:150, :16] = 0                      # ... which are zero for 150 rows: z = 0 exactly
+    y = rng.integers(-3, 4, size=(380, d))
+    y[:120, :16] = 0
+    y[200:260] = x[200:260]
+    w = workloads.Workload("zeros", "ip", dtype, workloads.encode(x, dtype),
+                           workloads.encode(y, dtype), 10.0, np.zeros((0, 2), np.int64))
+    g, ref, exact, cand, _ = run_lsh(w, h)
+    wi = workloads.Workload("zeros-i8", "ip", "i8", workloads.encode(x, "i8"),
+                            workloads.encode(y, "i8"), 10.0, np.zeros((0, 2), np.int64))
+    gi, *_ = run_lsh(wi, h)
+    assert np.array_equal(keys(g), keys(gi))
