@@ -546,7 +546,7 @@ __device__ __forceinline__ bool matches(typename sjk::Mma<DT>::val_t acc,
 // test, drops pairs that share a bucket in an earlier table (so every pair is
 // reported once) and appends the rest with one atomic per wave and block.
 template <int DT, int MET>
-__global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
+__global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
 {
     typedef sjk::Mma<DT> M;
     typedef typename M::acc_t acc_t;
@@ -606,15 +606,6 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
             }
         }
         __syncthreads();
-        const uint8_t *pa[LPT], *pb[LPT];
-        bool va[LPT], vb[LPT];
-#pragma unroll
-        for (int e = 0; e < LPT; ++e) {
-            pa[e] = g.P.X + (size_t)sIP[lr + 32 * e] * rb;
-            pb[e] = g.Q.X + (size_t)sIQ[lr + 32 * e] * rb;
-            va[e] = lr + 32 * e < rows_p;
-            vb[e] = lr + 32 * e < rows_q;
-        }
 
         acc_t acc[2][2];
 #pragma unroll
@@ -622,20 +613,21 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
                 acc[a][b] = acc_t{};
-        // the next chunk's loads are issued before this chunk's MFMAs
-        i32x4 la[LPT], lb[LPT];
-        auto fetch = [&](uint32_t kc) {
+        // rows are addressed through the tile's indices in LDS at every load
+        // (no per-thread row pointers: fewer registers, four waves per SIMD)
+        for (uint32_t kc = 0; kc < rb; kc += 128) {
             const uint32_t off = kc + 16 * lc;
             const i32x4 z = {0, 0, 0, 0};
             const bool in = off < rb;
+            i32x4 la[LPT], lb[LPT];
 #pragma unroll
             for (int e = 0; e < LPT; ++e) {
-                la[e] = va[e] && in ? *(const i32x4 *)(pa[e] + off) : z;
-                lb[e] = vb[e] && in ? *(const i32x4 *)(pb[e] + off) : z;
+                const uint32_t rr = lr + 32 * e;
+                la[e] = rr < rows_p && in
+                            ? *(const i32x4 *)(g.P.X + (size_t)sIP[rr] * rb + off) : z;
+                lb[e] = rr < rows_q && in
+                            ? *(const i32x4 *)(g.Q.X + (size_t)sIQ[rr] * rb + off) : z;
             }
-        };
-        fetch(0);
-        for (uint32_t kc = 0; kc < rb; kc += 128) {
             if (kc)
                 __syncthreads();   // the previous chunk's fragments are read
 #pragma unroll
@@ -644,8 +636,6 @@ __global__ void __launch_bounds__(256) join_kernel(JoinArgs g)
                 sB[(lr + 32 * e) * CS + lc] = lb[e];
             }
             __syncthreads();
-            if (kc + 128 < rb)
-                fetch(kc + 128);
             const uint32_t nks = min(4u, (rb - kc + 31) / 32);
 #pragma unroll
             for (uint32_t ks = 0; ks < 4; ++ks)
