@@ -64,15 +64,19 @@ constexpr int TILE_BITS = 38;
 
 // Bucket pairs: for every table and every key present in both P and Q, one
 // record (t, first sorted position in P, P rows, first sorted position in Q)
-// plus its Q rows and its first tile; records are numbered by one packed
-// atomic (slot << TILE_BITS | tiles), so first tiles increase with the slot.
-// counters[0] = packed count, [1] = tiles, [2] = pair evaluations.
+// plus its Q rows and its first tile within its table.  Table t keeps its
+// records in its own region [t tcap, (t + 1) tcap) and its own counters (a
+// cache line each, CSTRIDE words apart, so the tables' atomics do not
+// contend): counters[t CSTRIDE] = records << TILE_BITS | tiles (one packed
+// atomic numbers the records, so first tiles increase with the record), and
+// counters[t CSTRIDE + 1] = pair evaluations.
+constexpr int CSTRIDE = 16;
 struct BucketPairs {
     uint4 *head;          // {t, p0, np, q0}
     uint32_t *nq;
     unsigned long long *tile0;
-    unsigned long long *counters;
-    uint32_t cap;         // records the arrays hold
+    unsigned long long *counters;   // L * CSTRIDE words
+    uint32_t tcap;        // records per table region
 };
 
 hipError_t launch_bucket_pairs(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
@@ -86,8 +90,10 @@ struct JoinArgs {
     const uint4 *head;
     const uint32_t *nq;
     const unsigned long long *tile0;
-    uint32_t n_bp;
+    uint32_t tcap;                        // records per table region
     uint64_t n_tiles;
+    uint64_t tbase[65];                   // first tile of each table (tbase[L] = n_tiles)
+    uint32_t nrec[64];                    // records of each table
     float thr_f;                          // as sjk::JoinArgs
     int32_t thr_i;
     const void *norm_p, *norm_q;

@@ -505,15 +505,16 @@ __global__ void __launch_bounds__(256) bucket_pairs_kernel(const uint64_t *sorte
         return;
     const uint32_t np = pe - p, nq = qe - q0;
     const uint64_t tiles = (uint64_t)((np + TILE - 1) / TILE) * ((nq + TILE - 1) / TILE);
+    unsigned long long *cnt = bp.counters + (size_t)t * CSTRIDE;
     const unsigned long long old =
-        atomicAdd(&bp.counters[0], (1ull << TILE_BITS) | (unsigned long long)tiles);
-    atomicAdd(&bp.counters[1], (unsigned long long)tiles);
-    atomicAdd(&bp.counters[2], (unsigned long long)np * nq);
+        atomicAdd(&cnt[0], (1ull << TILE_BITS) | (unsigned long long)tiles);
+    atomicAdd(&cnt[1], (unsigned long long)np * nq);
     const uint64_t slot = old >> TILE_BITS;
-    if (slot < bp.cap) {
-        bp.head[slot] = make_uint4(t, p, np, q0);
-        bp.nq[slot] = nq;
-        bp.tile0[slot] = old & ((1ull << TILE_BITS) - 1);
+    if (slot < bp.tcap) {
+        const size_t at = (size_t)t * bp.tcap + slot;
+        bp.head[at] = make_uint4(t, p, np, q0);
+        bp.nq[at] = nq;
+        bp.tile0[at] = old & ((1ull << TILE_BITS) - 1);
     }
 }
 
@@ -568,28 +569,41 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
     const uint64_t T1 = min(T0 + per, g.n_tiles);
     if (T0 >= T1)
         return;   // the whole workgroup: no barrier is skipped by part of it
+    // the table of the first tile (tables without records have no tiles),
+    // then its record by binary search over the table's first tiles
+    uint32_t tab = 0;
+    while (tab + 1 < g.L && g.tbase[tab + 1] <= T0)
+        ++tab;
     uint32_t slot = 0;
     {
-        uint32_t hi = g.n_bp;
+        const uint64_t Tl = T0 - g.tbase[tab];
+        const unsigned long long *t0 = g.tile0 + (size_t)tab * g.tcap;
+        uint32_t hi = g.nrec[tab];
         while (hi - slot > 1) {
             const uint32_t mid = (slot + hi) >> 1;
-            if (g.tile0[mid] <= T0)
+            if (t0[mid] <= Tl)
                 slot = mid;
             else
                 hi = mid;
         }
     }
-    uint64_t local = T0 - g.tile0[slot];
+    uint64_t local = T0 - g.tbase[tab] - g.tile0[(size_t)tab * g.tcap + slot];
     for (uint64_t T = T0; T < T1; ++T) {
-        const uint4 h = g.head[slot];
-        const uint32_t t = h.x, nq = g.nq[slot];
+        const size_t rec = (size_t)tab * g.tcap + slot;
+        const uint4 h = g.head[rec];
+        const uint32_t t = h.x, nq = g.nq[rec];
         const uint32_t ntq = (nq + TILE - 1) / TILE;
         const uint32_t ntp = (h.z + TILE - 1) / TILE;
         const uint32_t tp = (uint32_t)(local / ntq), tq = (uint32_t)(local % ntq);
         const uint32_t rows_p = min(h.z - tp * TILE, TILE), rows_q = min(nq - tq * TILE, TILE);
-        if (++local == (uint64_t)ntp * ntq) {   // the next tile starts the next pair
-            ++slot;
+        if (++local == (uint64_t)ntp * ntq) {   // the next tile starts the next record
             local = 0;
+            if (++slot == g.nrec[tab]) {         // ... of the next table with records
+                slot = 0;
+                ++tab;
+                while (tab < g.L && g.nrec[tab] == 0)
+                    ++tab;
+            }
         }
 
         __syncthreads();   // the previous tile's reads of sIP/sIQ/sA/sB are done

@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "sj.h"
 #include "sj_host.h"
@@ -86,7 +87,20 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const bool joint = bits + sjl::table_bits(L) <= 64;
     const uint32_t tshift = joint && L > 1 ? bits : 0;
     const uint32_t sbits = joint ? bits + sjl::table_bits(L) : bits;
-    const uint64_t bp_cap = (uint64_t)L * (n_p < n_q ? n_p : n_q);
+    // records: a region of min(n_p, n_q) per table (a table has at most that
+    // many keys shared by P and Q)
+    const uint64_t tcap = n_p < n_q ? n_p : n_q;
+    const uint64_t bp_cap = (uint64_t)L * tcap;
+    // a table's tiles, sum over its buckets of ceil(p_b / T) ceil(q_b / T),
+    // are at most n_p n_q / T^2 + (n_p + n_q) / T + min(n_p, n_q): they must
+    // fit the packed counter's low TILE_BITS bits
+    {
+        const double T = sjl::TILE;
+        const double most = (double)n_p * n_q / (T * T) + ((double)n_p + n_q) / T + (double)tcap;
+        if (most >= (double)(1ull << sjl::TILE_BITS))
+            return fail(SJ_E_UNSUPPORTED, "n_p = %u, n_q = %u: a table could hold more than 2^%d "
+                        "candidate tiles", n_p, n_q, sjl::TILE_BITS);
+    }
     size_t temp_bytes = sjl::sort_temp_bytes(joint ? L * n_p : n_p, sbits);
     const size_t tq = sjl::sort_temp_bytes(joint ? L * n_q : n_q, sbits);
     temp_bytes = temp_bytes > tq ? temp_bytes : tq;
@@ -116,6 +130,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_bnq = take((size_t)bp_cap * 4);
     const size_t off_t0 = take((size_t)bp_cap * 8);
     const size_t off_cnt = take(6 * 8);
+    const size_t off_tcnt = take((size_t)L * sjl::CSTRIDE * 8);
     const size_t off_temp = take(temp_bytes);
     const size_t off_aw = take(a_bytes);
     // keys on the matrix cores where they apply
@@ -131,6 +146,8 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     sjl::Rows rq{aligned ? (const uint8_t *)Q : scr + off_rq, n_q, (uint32_t)krow};
     unsigned long long *cnt = (unsigned long long *)(scr + off_cnt);
     SJ_HIP(hipMemsetAsync(cnt, 0, 6 * 8, s));
+    unsigned long long *tcnt = (unsigned long long *)(scr + off_tcnt);
+    SJ_HIP(hipMemsetAsync(tcnt, 0, (size_t)L * sjl::CSTRIDE * 8, s));
     SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
     SJ_HIP(hipEventRecord(c->ev[0], s));
     if (!aligned) {
@@ -168,18 +185,24 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
         SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, joint,
                                 scr + off_temp, temp_bytes, s));
     sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
-                        (unsigned long long *)(scr + off_t0), cnt, (uint32_t)bp_cap};
+                        (unsigned long long *)(scr + off_t0), tcnt, (uint32_t)tcap};
     SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));
     SJ_HIP(hipEventRecord(c->ev[2], s));
-    SJ_HIP(hipMemcpyAsync(c->h_small + 1, cnt, 3 * 8, hipMemcpyDeviceToHost, s));
+    std::vector<unsigned long long> hc((size_t)L * sjl::CSTRIDE);
+    SJ_HIP(hipMemcpyAsync(hc.data(), tcnt, hc.size() * 8, hipMemcpyDeviceToHost, s));
     SJ_HIP(hipStreamSynchronize(s));
-    const uint64_t n_bp = c->h_small[1] >> sjl::TILE_BITS;
-    const uint64_t n_tiles = c->h_small[2], cand = c->h_small[3];
-    if (n_tiles >> sjl::TILE_BITS)
-        return fail(SJ_E_UNSUPPORTED, "%llu candidate tiles are more than 2^%d",
-                    (unsigned long long)n_tiles, sjl::TILE_BITS);
 
     sjl::JoinArgs g = {};
+    uint64_t n_tiles = 0, cand = 0;
+    for (uint32_t t = 0; t < L; ++t) {
+        const unsigned long long packed = hc[(size_t)t * sjl::CSTRIDE];
+        g.tbase[t] = n_tiles;
+        g.nrec[t] = (uint32_t)(packed >> sjl::TILE_BITS);
+        n_tiles += packed & ((1ull << sjl::TILE_BITS) - 1);
+        cand += hc[(size_t)t * sjl::CSTRIDE + 1];
+    }
+    g.tbase[L] = n_tiles;
+
     g.P = rp;
     g.Q = rq;
     g.L = L;
@@ -190,7 +213,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     g.head = bp.head;
     g.nq = bp.nq;
     g.tile0 = bp.tile0;
-    g.n_bp = (uint32_t)n_bp;
+    g.tcap = (uint32_t)tcap;
     g.n_tiles = n_tiles;
     if (dtype == SJ_I8) {
         if (!l2) {
