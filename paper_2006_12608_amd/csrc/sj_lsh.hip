@@ -261,8 +261,8 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
 // (any summation order; gamma(d) = d u / (1 - d u)), so when |z| exceeds twice
 // the sum of both bounds the sign is the double sum's, and when the interval
 // z +- that margin maps to one bucket the quantised value is.  A (row, table)
-// with any uncertain function is queued and its key recomputed with the exact
-// double evaluation (fix_kernel), so the keys equal keys_kernel's.
+// with uncertain functions is queued with their mask, and fix_kernel computes
+// those with the exact double evaluation, so the keys equal keys_kernel's.
 constexpr int HF_MAX = 256;
 
 template <int DT>
@@ -315,17 +315,18 @@ __global__ void xnorm_kernel(Rows r, uint32_t d, float *out)
 // A wave takes 32 rows (A-fragments of KS k-steps in registers) and sweeps the
 // L k functions in MFMA blocks of 32; each lane folds its function's value
 // into the (row, table) key in LDS (64-bit atomic OR), and marks uncertain
-// ones; then the wave writes the keys and queues the uncertain (row, table).
+// ones; then the wave writes the keys and queues each (row, table) with its
+// mask of uncertain functions (one queue atomic per wave).
 template <int DT, int KS>
 __global__ void __launch_bounds__(256) keys_mfma_kernel(
     Rows r, uint32_t L, uint32_t k, const uint8_t *Ah, const float *anorm, const float *xnorm,
-    const int32_t *B, int32_t w, uint32_t tshift, float gam, uint64_t *keys, uint2 *fix,
+    const int32_t *B, int32_t w, uint32_t tshift, float gam, uint64_t *keys, uint4 *fix,
     unsigned long long *nfix)
 {
     typedef sjk::Mma<DT> M;
     typedef typename M::acc_t acc_t;
     __shared__ unsigned long long skey[4][32 * 64];
-    __shared__ unsigned long long sflag[4][32];
+    __shared__ unsigned long long sunc[4][32][HF_MAX / 64];   // uncertain (row, function)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int h = lane >> 5, c32 = lane & 31;
     const uint32_t row0 = (blockIdx.x * 4 + wave) * 32;
@@ -335,8 +336,8 @@ __global__ void __launch_bounds__(256) keys_mfma_kernel(
     unsigned long long *kk = skey[wave];
     for (uint32_t i = lane; i < 32 * L; i += 64)
         kk[i] = 0ull;
-    if (lane < 32)
-        sflag[wave][lane] = 0ull;
+    for (uint32_t i = lane; i < 32 * (HF_MAX / 64); i += 64)
+        sunc[wave][i / (HF_MAX / 64)][i % (HF_MAX / 64)] = 0ull;
     i32x4 af[KS];
     const uint32_t arow = row0 + c32;
 #pragma unroll
@@ -388,33 +389,71 @@ __global__ void __launch_bounds__(256) keys_mfma_kernel(
             if (sure)
                 atomicOr(&kk[Rl * L + t], (unsigned long long)contrib);
             else
-                atomicOr(&sflag[wave][Rl], 1ull << t);
+                atomicOr(&sunc[wave][Rl][f >> 6], 1ull << (f & 63));
         }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    for (uint32_t i = lane; i < 32 * L; i += 64) {
-        const uint32_t Rl = i / L, t = i - Rl * L;
-        const uint32_t R = row0 + Rl;
-        if (R >= r.n)
-            continue;
-        keys[(size_t)t * r.n + R] = kk[i] | (tshift ? (uint64_t)t << tshift : 0ull);
-        if ((sflag[wave][Rl] >> t) & 1) {
-            const unsigned long long slot = atomicAdd(nfix, 1ull);
-            fix[slot] = make_uint2(R, t);
+    // the uncertain functions of (row Rl, table t): bits t k .. t k + k - 1 of
+    // the row's function mask
+    auto umask = [&](uint32_t Rl, uint32_t t) -> uint64_t {
+        const uint32_t b0 = t * k;
+        const unsigned long long *m = sunc[wave][Rl];
+        uint64_t v = m[b0 >> 6] >> (b0 & 63);
+        if ((b0 & 63) != 0 && (b0 >> 6) + 1 < HF_MAX / 64)
+            v |= m[(b0 >> 6) + 1] << (64 - (b0 & 63));
+        return k >= 64 ? v : v & ((1ull << k) - 1);
+    };
+    // keys (certain bits), then the queue entries of the wave with one atomic
+    uint32_t total = 0;
+    for (uint32_t i0 = 0; i0 < 32 * L; i0 += 64) {
+        const uint32_t i = i0 + lane;
+        bool q = false;
+        if (i < 32 * L) {
+            const uint32_t Rl = i / L, t = i - Rl * L;
+            const uint32_t R = row0 + Rl;
+            if (R < r.n) {
+                keys[(size_t)t * r.n + R] = kk[i] | (tshift ? (uint64_t)t << tshift : 0ull);
+                q = umask(Rl, t) != 0;
+            }
         }
+        total += (uint32_t)__popcll(__ballot(q));
+    }
+    if (total == 0)
+        return;
+    unsigned long long base = 0;
+    if (lane == 0)
+        base = atomicAdd(nfix, (unsigned long long)total);
+    base = sjk::first_lane_u64(base);
+    for (uint32_t i0 = 0; i0 < 32 * L; i0 += 64) {
+        const uint32_t i = i0 + lane;
+        uint64_t m = 0;
+        uint32_t Rl = 0, t = 0;
+        if (i < 32 * L) {
+            Rl = i / L;
+            t = i - Rl * L;
+            if (row0 + Rl < r.n)
+                m = umask(Rl, t);
+        }
+        const uint64_t bits = __ballot(m != 0);
+        if (m != 0)
+            fix[base + sjk::lanes_below(bits)] =
+                make_uint4(row0 + Rl, t, (uint32_t)m, (uint32_t)(m >> 32));
+        base += (uint32_t)__popcll(bits);
     }
 }
 
-// The queued (row, table) keys, recomputed exactly as keys_kernel does (one
-// thread per entry, the row read from global memory; grid-stride over the
-// queue's length, read from device memory).
+// The queued (row, table) keys: the functions the matrix-core pass could not
+// decide, recomputed exactly as keys_kernel does (the row read from global
+// memory), OR-ed into the key (whose bits for them are still zero); one
+// thread per entry, grid-stride over the queue's length read from device
+// memory.
 template <int DT>
 __global__ void __launch_bounds__(256) fix_kernel(Rows r, uint32_t d, uint32_t k,
                                                   const typename Chunk<DT>::a_t *A,
-                                                  const int32_t *B, int32_t w, uint32_t tshift,
-                                                  const uint2 *fix,
+                                                  const int32_t *B, int32_t w,
+                                                  const uint4 *fix,
                                                   const unsigned long long *nfix, uint64_t *keys)
 {
     typedef Chunk<DT> C;
@@ -425,22 +464,25 @@ __global__ void __launch_bounds__(256) fix_kernel(Rows r, uint32_t d, uint32_t k
     const uint64_t low = beta >= 64 ? ~0ull : (1ull << beta) - 1;
     for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < n_fix;
          i += (uint64_t)gridDim.x * 256) {
-        const uint2 e = fix[i];
+        const uint4 e = fix[i];
         const uint32_t row = e.x, t = e.y;
+        uint64_t m = (uint64_t)e.z | ((uint64_t)e.w << 32);
         const uint8_t *x = r.X + (size_t)row * r.row_bytes;
-        uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
-        for (uint32_t u = 0; u < k; ++u) {
+        uint64_t key = 0;
+        while (m) {
+            const uint32_t u = (uint32_t)__builtin_ctzll(m);
+            m &= m - 1;
             const typename C::a_t *a = A + (size_t)(t * k + u) * dp;
             acc_t z = acc_t(0);
             for (uint32_t c = 0; c < nch; ++c) {
                 const i32x4 v = *(const i32x4 *)(x + 16 * c);
 #pragma unroll
-                for (int m = 0; m < C::E; ++m)
-                    z += acc_t(a[c * C::E + m]) * C::at(v, m);
+                for (int q = 0; q < C::E; ++q)
+                    z += acc_t(a[c * C::E + q]) * C::at(v, q);
             }
             fold_value(key, z, u, beta, low, B, t * k + u, w);
         }
-        keys[(size_t)t * r.n + row] = key;
+        keys[(size_t)t * r.n + row] |= key;
     }
 }
 
@@ -808,13 +850,13 @@ size_t keys_fast_bytes(uint32_t n_max, uint32_t L, uint32_t k, uint32_t row_byte
 {
     // fp16 / bf16 projection rows, their norms, row norms, the fix queue
     return (size_t)L * k * row_bytes + 256 + (size_t)L * k * 4 + 256 + (size_t)n_max * 4 + 256 +
-           (size_t)L * n_max * 8;
+           (size_t)L * n_max * 16;
 }
 
 template <int DT, int KS>
 static void launch_mfma_t(const Rows &r, uint32_t L, uint32_t k, const uint8_t *Ah,
                           const float *an, const float *xn, const int32_t *B, int32_t w,
-                          uint32_t tshift, float gam, uint64_t *keys, uint2 *fix,
+                          uint32_t tshift, float gam, uint64_t *keys, uint4 *fix,
                           unsigned long long *nfix, hipStream_t s)
 {
     hipLaunchKernelGGL((keys_mfma_kernel<DT, KS>), dim3((r.n + 127) / 128), dim3(256), 0, s, r,
@@ -831,7 +873,7 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
     uint8_t *Ah = ws;
     float *an = (float *)(ws + (((size_t)nf * r.row_bytes + 255) & ~(size_t)255));
     float *xn = (float *)((uint8_t *)an + (((size_t)nf * 4 + 255) & ~(size_t)255));
-    uint2 *fix = (uint2 *)((uint8_t *)xn + (((size_t)r.n * 4 + 255) & ~(size_t)255));
+    uint4 *fix = (uint4 *)((uint8_t *)xn + (((size_t)r.n * 4 + 255) & ~(size_t)255));
     if (widen) {
         const uint32_t rl = r.row_bytes / 2;
         const uint64_t n_out = (uint64_t)nf * rl;
@@ -855,7 +897,7 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
     else
         launch_mfma_t<DT, 16>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
     hipLaunchKernelGGL(fix_kernel<DT>, dim3(512), dim3(256), 0, s, r, d, k,
-                       (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, fix,
+                       (const typename Chunk<DT>::a_t *)Aw, B, w, fix,
                        (const unsigned long long *)nfix, keys);
     return hipGetLastError();
 }
