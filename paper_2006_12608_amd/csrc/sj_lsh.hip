@@ -263,7 +263,7 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
 // z +- that margin maps to one bucket the quantised value is.  A (row, table)
 // with uncertain functions is queued with their mask, and fix_kernel computes
 // those with the exact double evaluation, so the keys equal keys_kernel's.
-constexpr int HF_MAX = 256;
+constexpr int HF_MAX = 512;
 
 template <int DT>
 __global__ void widen_h_kernel(const int8_t *A, uint16_t *Ah, uint32_t d, uint32_t rl,

@@ -221,3 +221,13 @@ def test_lsh_uncertain_decisions_are_exact(dtype, wid):
                             workloads.encode(y, "i8"), 10.0, np.zeros((0, 2), np.int64))
     gi, *_ = run_lsh(wi, h)
     assert np.array_equal(keys(g), keys(gi))
+
+
+def test_lsh_many_functions_matrix_core_hash():
+    """24 tables of 12 signs (288 functions: the matrix-core hash's function
+    masks span several 64-bit words, and tables straddle them) on real-valued
+    unit rows: parity with the oracle outside the band."""
+    wl = workloads.make_config("cos_f16_262144x256", n=1200)
+    h = workloads.lsh_params(78, L=24, k=12, d=wl.d)
+    g, ref, exact, cand, info = run_lsh(wl, h)
+    assert len(ref) > 0
