@@ -160,3 +160,16 @@ def test_jl_full_size_sampled_rows():
     # the JL property on unit rows: norms within 1 +- 0.5 for nearly all rows
     nrm = np.linalg.norm(Y, axis=1)
     assert (np.abs(nrm - 1) <= 0.5).mean() > 0.99
+
+
+@pytest.mark.parametrize("dtype,n,d,shapes", [
+    ("f16", 1, 6, [(3, 6, 1)]),                      # one row, one level
+    ("bf16", 129, 15, [(2, 5, 3), (7, 6, 1)]),       # odd sizes: no 4-entry loads
+    ("i8", 65, 200, [(130, 200, 1)]),                 # more than 128 output columns
+])
+def test_jl_edge_shapes(dtype, n, d, shapes):
+    rng = np.random.default_rng(n + d)
+    As = [rng.integers(-3, 4, size=(k, c)).astype(np.float64) for (k, c, r) in shapes]
+    X = workloads.encode(rng.integers(-4, 5, size=(n, d)), dtype)
+    Y = run(X, dtype, shapes, As)
+    assert np.array_equal(Y, jl.transform(values(dtype, X), shapes, As))

@@ -231,3 +231,15 @@ def test_lsh_many_functions_matrix_core_hash():
     h = workloads.lsh_params(78, L=24, k=12, d=wl.d)
     g, ref, exact, cand, info = run_lsh(wl, h)
     assert len(ref) > 0
+
+
+@pytest.mark.parametrize("dtype,n_p,n_q,d,L,k,wid,metric,thr", [
+    ("f16", 1, 1, 7, 2, 3, 0, "ip", -1000.0),    # one point each, odd d (repacked rows)
+    ("bf16", 1, 300, 9, 3, 64, 0, "ip", 5.0),    # 64 sign bits per table (one bit each)
+    ("i8", 257, 1, 5, 4, 2, 3, "l2", 40.0),      # quantised with a tiny bucket width
+    ("f16", 130, 129, 1, 2, 5, 0, "ip", 2.0),    # d = 1: every projection is a multiple of x
+])
+def test_lsh_edge_shapes(dtype, n_p, n_q, d, L, k, wid, metric, thr):
+    w = case(60 + d + n_p, n_p, n_q, d, dtype, metric, thr, -3, 3)
+    h = workloads.lsh_params(61 + k, L=L, k=k, d=d, w=wid)
+    run_lsh(w, h)
