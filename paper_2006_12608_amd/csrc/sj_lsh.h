@@ -33,8 +33,8 @@ hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_
                        const void *Aw, const int32_t *B, int32_t w, uint32_t tshift,
                        uint64_t *keys, hipStream_t s);
 
-// The same keys with the projections on the matrix cores (fp16 / bf16 rows of
-// at most 512 bytes, L k <= 512, k >= 2 for quantised hashes:
+// The same keys with the projections on the matrix cores (rows of at most
+// 512 bytes, L k <= 512, k >= 2 for quantised hashes:
 // keys_fast_applies): decisions the fp32 sums make certain are kept, the
 // other (row, table) keys are recomputed exactly.  `ws` is workspace of
 // keys_fast_bytes(n_max, L, k, row_bytes) bytes whose first part (the fp16 /

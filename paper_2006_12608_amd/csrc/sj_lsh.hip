@@ -252,9 +252,10 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
 
 // ------------------------------------------------ keys on the matrix cores
 //
-// For fp16 / bf16 rows of at most 512 bytes and at most HF_MAX functions in
-// all: the projections z_f(x) of 32 rows by 32 functions come from one MFMA
-// block (fp16 / bf16 products are exact in fp32, the sums are rounded).  A
+// For rows of at most 512 bytes and at most HF_MAX functions in all: the
+// projections z_f(x) of 32 rows by 32 functions come from one MFMA block
+// (int8: exact int32 sums, so every decision is taken here; fp16 / bf16:
+// products exact in fp32, sums rounded).  A
 // decision (sign, or floor((z + B) / w)) is taken from the fp32 value only when
 // it is certain: the fp32 sum and the double sum in ascending m both differ
 // from the exact sum by at most gamma(d) sum_m |A_m x_m| <= gamma(d) ||A|| ||x||
@@ -277,6 +278,18 @@ __global__ void widen_h_kernel(const int8_t *A, uint16_t *Ah, uint32_t d, uint32
             Ah[i] = __builtin_bit_cast(uint16_t, (_Float16)a);
         else
             Ah[i] = (uint16_t)(__builtin_bit_cast(uint32_t, a) >> 16);
+    }
+}
+
+// int8 projection rows copied into rows of rb bytes (zero padded): the int8
+// matrix cores' operand layout.
+__global__ void pad_b_kernel(const int8_t *A, int8_t *Ab, uint32_t d, uint32_t rb,
+                             uint64_t n_out)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n_out) {
+        const uint64_t f = i / rb, m = i - f * rb;
+        Ab[i] = m < d ? A[f * d + m] : (int8_t)0;
     }
 }
 
@@ -347,11 +360,13 @@ __global__ void __launch_bounds__(256) keys_mfma_kernel(
                      ? *(const i32x4 *)(r.X + (size_t)arow * r.row_bytes + off)
                      : i32x4{0, 0, 0, 0};
     }
-    float xn[16];
+    float xn[16] = {};
+    if constexpr (DT != DT_I8) {
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-        const uint32_t R = row0 + 8 * (q >> 2) + 4 * h + (q & 3);
-        xn[q] = R < r.n ? xnorm[R] : 0.0f;
+        for (int q = 0; q < 16; ++q) {
+            const uint32_t R = row0 + 8 * (q >> 2) + 4 * h + (q & 3);
+            xn[q] = R < r.n ? xnorm[R] : 0.0f;
+        }
     }
     __builtin_amdgcn_wave_barrier();
     for (uint32_t f0 = 0; f0 < nf; f0 += 32) {
@@ -368,23 +383,35 @@ __global__ void __launch_bounds__(256) keys_mfma_kernel(
         if (f >= nf)
             continue;
         const uint32_t t = f / k, u = f - t * k;
-        const float na = anorm[f];
+        const float na = DT == DT_I8 ? 0.0f : anorm[f];
         const double bf = w > 0 ? (double)B[f] : 0.0;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
             const int Rl = 8 * (q >> 2) + 4 * h + (q & 3);
-            const float z = acc[q];
-            const float e = gam * na * xn[q];
             uint64_t contrib;
             bool sure;
-            if (w == 0) {
-                sure = __builtin_fabsf(z) > e;
-                contrib = (uint64_t)(z >= 0.0f) << u;
+            if constexpr (DT == DT_I8) {
+                // int8 products summed exactly in int32: every decision is the
+                // exact one (and the double evaluation's, which is exact too)
+                const int32_t z = acc[q];
+                sure = true;
+                if (w == 0)
+                    contrib = (uint64_t)(z >= 0) << u;
+                else
+                    contrib = ((uint64_t)(int64_t)floor(((double)z + bf) / (double)w) & low)
+                              << (beta * u);
             } else {
-                const double lo = floor(((double)z - (double)e + bf) / (double)w);
-                const double hi = floor(((double)z + (double)e + bf) / (double)w);
-                sure = lo == hi;
-                contrib = ((uint64_t)(int64_t)lo & low) << (beta * u);
+                const float z = acc[q];
+                const float e = gam * na * xn[q];
+                if (w == 0) {
+                    sure = __builtin_fabsf(z) > e;
+                    contrib = (uint64_t)(z >= 0.0f) << u;
+                } else {
+                    const double lo = floor(((double)z - (double)e + bf) / (double)w);
+                    const double hi = floor(((double)z + (double)e + bf) / (double)w);
+                    sure = lo == hi;
+                    contrib = ((uint64_t)(int64_t)lo & low) << (beta * u);
+                }
             }
             if (sure)
                 atomicOr(&kk[Rl * L + t], (unsigned long long)contrib);
@@ -842,7 +869,7 @@ hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_
 
 bool keys_fast_applies(int dtype, uint32_t row_bytes, uint32_t L, uint32_t k, int32_t w)
 {
-    return (dtype == DT_F16 || dtype == DT_BF16) && row_bytes <= 512 && k >= 1 &&
+    return row_bytes <= 512 && k >= 1 &&
            (uint64_t)L * k <= HF_MAX && L <= 64 && (w == 0 || k >= 2);
 }
 
@@ -874,14 +901,24 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
     float *an = (float *)(ws + (((size_t)nf * r.row_bytes + 255) & ~(size_t)255));
     float *xn = (float *)((uint8_t *)an + (((size_t)nf * 4 + 255) & ~(size_t)255));
     uint4 *fix = (uint4 *)((uint8_t *)xn + (((size_t)r.n * 4 + 255) & ~(size_t)255));
-    if (widen) {
-        const uint32_t rl = r.row_bytes / 2;
-        const uint64_t n_out = (uint64_t)nf * rl;
-        hipLaunchKernelGGL(widen_h_kernel<DT>, dim3((unsigned)((n_out + 255) / 256)), dim3(256),
-                           0, s, A, (uint16_t *)Ah, d, rl, n_out);
-        hipLaunchKernelGGL(anorm_kernel, dim3((nf + 255) / 256), dim3(256), 0, s, A, d, nf, an);
+    if constexpr (DT == DT_I8) {
+        // the projection rows as int8 operand rows; sums exact: no norms, no queue
+        if (widen) {
+            const uint64_t n_out = (uint64_t)nf * r.row_bytes;
+            hipLaunchKernelGGL(pad_b_kernel, dim3((unsigned)((n_out + 255) / 256)), dim3(256), 0,
+                               s, A, (int8_t *)Ah, d, r.row_bytes, n_out);
+        }
+    } else {
+        if (widen) {
+            const uint32_t rl = r.row_bytes / 2;
+            const uint64_t n_out = (uint64_t)nf * rl;
+            hipLaunchKernelGGL(widen_h_kernel<DT>, dim3((unsigned)((n_out + 255) / 256)),
+                               dim3(256), 0, s, A, (uint16_t *)Ah, d, rl, n_out);
+            hipLaunchKernelGGL(anorm_kernel, dim3((nf + 255) / 256), dim3(256), 0, s, A, d, nf,
+                               an);
+        }
+        hipLaunchKernelGGL(xnorm_kernel<DT>, dim3((r.n + 255) / 256), dim3(256), 0, s, r, d, xn);
     }
-    hipLaunchKernelGGL(xnorm_kernel<DT>, dim3((r.n + 255) / 256), dim3(256), 0, s, r, d, xn);
     // twice the fp32 and double summation bounds for d terms
     const double dd = d ? (double)d : 1.0;
     const double g24 = dd * 0x1p-24 / (1.0 - dd * 0x1p-24);
@@ -896,9 +933,10 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
         launch_mfma_t<DT, 8>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
     else
         launch_mfma_t<DT, 16>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
-    hipLaunchKernelGGL(fix_kernel<DT>, dim3(512), dim3(256), 0, s, r, d, k,
-                       (const typename Chunk<DT>::a_t *)Aw, B, w, fix,
-                       (const unsigned long long *)nfix, keys);
+    if constexpr (DT != DT_I8)
+        hipLaunchKernelGGL(fix_kernel<DT>, dim3(512), dim3(256), 0, s, r, d, k,
+                           (const typename Chunk<DT>::a_t *)Aw, B, w, fix,
+                           (const unsigned long long *)nfix, keys);
     return hipGetLastError();
 }
 
@@ -912,6 +950,9 @@ hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, ui
     if (dtype == DT_F16)
         return keys_fast_t<DT_F16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
                                    nfix, s);
+    if (dtype == DT_I8)
+        return keys_fast_t<DT_I8>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+                                  nfix, s);
     return keys_fast_t<DT_BF16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
                                 nfix, s);
 }
