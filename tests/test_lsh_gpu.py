@@ -119,7 +119,7 @@ def test_lsh_parity_real_cosine(dtype):
 
 
 def test_lsh_buckets_span_tiles_and_ragged():
-    """k = 1: two big buckets per table, each hundreds of rows (several 64-row
+    """k = 1: two big buckets per table, each hundreds of rows (several 128-row
     tiles plus ragged tails on both sides)."""
     w = case(41, 517, 389, 33, "i8", "ip", 15.0, -6, 6)   # 33-byte rows: repacked
     h = workloads.lsh_params(42, L=3, k=1, d=33)
