@@ -67,19 +67,24 @@ def _code_only(src: str) -> str:
 JOIN_SOURCES = ("sj_api", "sj_aux", "sj_internal", "sj_join")
 
 
-def kernel_source_hash() -> str:
-    """Hash of the join's code (comments and layout ignored), to tell
+# Sources of the TCU JL transform (its own counter record).
+JL_SOURCES = ("sj_jl", "sj_host")
+
+
+def kernel_source_hash(prefixes=JOIN_SOURCES) -> str:
+    """Hash of the code of the source files whose names start with one of
+    `prefixes` (comments and layout ignored; default: the join's), to tell
     whether a stored counter record was taken on the current kernels."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2006_12608_amd", "csrc")
     for f in sorted(os.listdir(d)):
-        if f.endswith((".h", ".hip", ".cpp")) and f.startswith(JOIN_SOURCES):
+        if f.endswith((".h", ".hip", ".cpp")) and f.startswith(prefixes):
             h.update(f.encode())
             h.update(_code_only(open(os.path.join(d, f)).read()).encode())
     return h.hexdigest()[:16]
 
 
-def traffic_for(key: str):
+def traffic_for(key: str, prefixes=JOIN_SOURCES):
     """HBM bytes per launch from the committed rocprofv3 counter summary (key:
     the workload name for its join or first-pass kernel, "<workload>:emit" for
     its emit-from-bits kernel), if it was taken on the current kernel sources;
@@ -91,7 +96,7 @@ def traffic_for(key: str):
         rec = json.load(open(p)).get(key)
     except (ValueError, OSError):
         return None
-    if not rec or rec.get("kernel_sha") != kernel_source_hash():
+    if not rec or rec.get("kernel_sha") != kernel_source_hash(prefixes):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -225,7 +230,8 @@ def bench_jl(args, w, Pd, ctx):
         "flop": flop,
         "roofline": {"bound": "hbm", "kernel": "jl_level (all levels)", "kernel_ms": kms,
                      "achieved": nbytes / (kms / 1e3) / 1e9, "peak": 8000.0, "unit": "GB/s",
-                     "frac": nbytes / (kms / 1e3) / 1e9 / 8000.0, "traffic": None,
+                     "frac": nbytes / (kms / 1e3) / 1e9 / 8000.0,
+                     "traffic": traffic_for(f"jl:{args.workload}:{args.jl}", JL_SOURCES),
                      "algorithmic_bytes": nbytes},
     }), flush=True)
 
