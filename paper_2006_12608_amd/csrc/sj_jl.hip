@@ -120,8 +120,9 @@ __global__ void __launch_bounds__(256) jl_level(const void *X, uint64_t rows, ui
                     sx[r * XS + e] = row < rows && k < K ? load_elem<SRC>(X, row * K + k) : 0.0f;
                 }
             }
-#pragma unroll
-            for (int q = tid; q < 32 * NCB * KC; q += 256) {
+            // only the column blocks this group uses (whole blocks of 32 rows)
+            const uint32_t arows = min((N - cb0 + 31) / 32 * 32, 32u * NCB);
+            for (uint32_t q = tid; q < arows * KC; q += 256) {
                 const int r = q / KC, e = q % KC;
                 const uint32_t col = cb0 + r, k = k0 + e;
                 sa[r * XS + e] = col < N && k < K ? A[(uint64_t)col * K + k] : 0.0f;
