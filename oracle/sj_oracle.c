@@ -318,8 +318,12 @@ int or_lsh_keys(int dtype, const void *X, int64_t n, int64_t d, int64_t L, int64
         return -1;
     const int beta = k > 0 ? (int)(64 / k) : 64;
     const uint64_t low = beta >= 64 ? ~(uint64_t)0 : (((uint64_t)1 << beta) - 1);
-    for (int64_t t = 0; t < L; ++t)
-        for (int64_t i = 0; i < n; ++i) {
+    /* OpenMP only splits the independent rows */
+#ifdef _OPENMP
+#pragma omp parallel for schedule(static)
+#endif
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t t = 0; t < L; ++t) {
             uint64_t key = 0;
             for (int64_t u = 0; u < k; ++u) {
                 const int64_t f = t * k + u;

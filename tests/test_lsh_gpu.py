@@ -243,3 +243,35 @@ def test_lsh_edge_shapes(dtype, n_p, n_q, d, L, k, wid, metric, thr):
     w = case(60 + d + n_p, n_p, n_q, d, dtype, metric, thr, -3, 3)
     h = workloads.lsh_params(61 + k, L=L, k=k, d=d, w=wid)
     run_lsh(w, h)
+
+
+def test_lsh_full_size_sampled_rows():
+    """The full cosine workload (262144 x 256 fp16) with the benchmark's LSH
+    parameters (16 tables of 10 signs, its seed): the oracle computes every
+    row's keys and, for sampled rows of P, the exact matches; the LSH join's
+    pairs of those rows must be exactly the matches that share a key with them
+    in some table (outside the boundary band)."""
+    import paper_2006_12608_amd as sj
+    wl = workloads.make_config("cos_f16_262144x256")
+    h = workloads.lsh_params(1300 + workloads.NAMES.index("cos_f16_262144x256"), L=16, k=10,
+                             d=wl.d)
+    Pd, Qd = to_device(wl.P, wl.dtype), to_device(wl.Q, wl.dtype)
+    A, _ = lsh_device(h)
+    say("lsh full", wl.name)
+    got, cand = sj.join_lsh(Pd, Qd, wl.threshold, "ip", L=h.L, k=h.k, A=A)
+    g = sorted_pairs(got)
+    rng = np.random.default_rng(4321)
+    rows = np.sort(np.concatenate([rng.choice(wl.n_p, size=16, replace=False),
+                                   wl.planted[:16, 0]]))
+    rows = np.unique(rows)
+    kq = oracle.lsh_keys(wl.dtype, wl.Q, h.L, h.k, h.A)
+    kp = oracle.lsh_keys(wl.dtype, np.ascontiguousarray(wl.P[rows]), h.L, h.k, h.A)
+    ex = oracle.join("ip", wl.dtype, wl.P, wl.Q, wl.threshold, rows=rows,
+                     band=1e-3 * wl.threshold)
+    pos = {int(r): t for t, r in enumerate(rows)}
+    keep = np.array([bool((kp[:, pos[int(i)]] == kq[:, int(j)]).any()) for i, j in ex.pairs],
+                    dtype=bool) if ex.total else np.zeros(0, bool)
+    ref = oracle.JoinResult(ex.pairs[keep], int(keep.sum()), ex.band_pairs, ex.band_match)
+    info = compare(g[np.isin(g[:, 0], rows)], ref, True)
+    say("rows", rows.size, "pairs", ref.total, "band", info)
+    assert ref.total >= 16
