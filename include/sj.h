@@ -169,7 +169,9 @@ int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, co
  * join), L * max(n_p, n_q) < 2^26; other arguments, outputs and errors as
  * sj_join_ip.  *n_cand (host, may be NULL) receives the number of pair
  * evaluations made (the sum over tables and shared buckets of |P bucket| x
- * |Q bucket|).  Device scratch grows to about L * (n_p + n_q) * 64 bytes. */
+ * |Q bucket|).  Device scratch grows to about L * (n_p + n_q) * 64 bytes,
+ * plus L * max(n_p, n_q) * 32 when a key's bits and the table index together
+ * exceed 64 (the sort by key, then by table, keeps its own buffers). */
 int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
                 uint32_t n_q, uint32_t d, double thr, uint32_t L, uint32_t k, const int8_t *A,
                 const int32_t *B, int32_t w, uint32_t *pairs, uint64_t cap, uint64_t *n_out,

@@ -50,12 +50,17 @@ hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, ui
 // Sorts each table's keys with the row indices as values (n rows per table):
 // sorted[t * n + p], perm[t * n + p] = the p-th smallest key of table t and its
 // row.  joint: the keys carry their table above `bits` and one sort of all
-// L n entries does it.  `iota` holds L n entries; `temp` must hold
-// sort_temp_bytes(joint ? L n : n, joint ? bits + table_bits(L) : bits) bytes.
+// L n entries does it (`iota` holds L n entries; `temp` must hold
+// sort_temp_bytes(L n, bits + table_bits(L)) bytes); otherwise all entries
+// are sorted by key and then stably by table (`temp`:
+// sort_temp_bytes_split(L n, bits, table_bits(L)) bytes, `work`:
+// split_work_bytes(L n) bytes).
 size_t sort_temp_bytes(uint32_t n, uint32_t bits);
+size_t sort_temp_bytes_split(uint32_t total, uint32_t bits, uint32_t tbits);
+size_t split_work_bytes(uint32_t total);
 hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
                        uint32_t n, uint32_t L, uint32_t bits, bool joint, void *temp,
-                       size_t temp_bytes, hipStream_t s);
+                       size_t temp_bytes, void *work, hipStream_t s);
 
 // Tile edge of the bucket join (rows of P and of Q per workgroup tile).
 constexpr uint32_t TILE = 128;

@@ -983,29 +983,91 @@ size_t sort_temp_bytes(uint32_t n, uint32_t bits)
     return bytes;
 }
 
+size_t sort_temp_bytes_split(uint32_t total, uint32_t bits, uint32_t tbits)
+{
+    size_t a = 0, b = 0;
+    (void)hipcub::DeviceRadixSort::SortPairs(nullptr, a, (const uint64_t *)nullptr,
+                                             (uint64_t *)nullptr, (const uint32_t *)nullptr,
+                                             (uint32_t *)nullptr, total, 0, (int)bits);
+    (void)hipcub::DeviceRadixSort::SortPairs(nullptr, b, (const uint32_t *)nullptr,
+                                             (uint32_t *)nullptr, (const uint32_t *)nullptr,
+                                             (uint32_t *)nullptr, total, 0, (int)(tbits ? tbits : 1));
+    return a > b ? a : b;
+}
+
+size_t split_work_bytes(uint32_t total) { return (size_t)total * 32 + 1024; }
+
+// Table of each entry (entries are t n + row) and the identity permutation.
+__global__ void table_of_kernel(const uint32_t *ent, uint32_t n, uint32_t total, uint32_t *tkey,
+                                uint32_t *idx)
+{
+    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+    if (i < total) {
+        tkey[i] = ent[i] / n;
+        idx[i] = i;
+    }
+}
+
+// sorted[j] = K1[idx[j]], perm[j] = the row of entry E1[idx[j]].
+__global__ void gather_sorted_kernel(const uint64_t *K1, const uint32_t *E1, const uint32_t *idx,
+                                     uint32_t n, uint32_t total, uint64_t *sorted, uint32_t *perm)
+{
+    const uint32_t j = blockIdx.x * 256 + threadIdx.x;
+    if (j < total) {
+        const uint32_t q = idx[j];
+        sorted[j] = K1[q];
+        perm[j] = E1[q] % n;
+    }
+}
+
 hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
                        uint32_t n, uint32_t L, uint32_t bits, bool joint, void *temp,
-                       size_t temp_bytes, hipStream_t s)
+                       size_t temp_bytes, void *work, hipStream_t s)
 {
     if (n == 0)
         return hipSuccess;
-    const uint32_t total = joint ? n * L : n;
-    hipLaunchKernelGGL(iota_kernel, dim3((total + 255) / 256), dim3(256), 0, s, iota, n, total);
-    hipError_t e = hipGetLastError();
+    const uint32_t total = n * L;
+    const dim3 grid((total + 255) / 256);
     if (joint) {
         // keys carry their table above `bits`: one sort orders every table
         // within its own segment [t n, (t + 1) n)
+        hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, s, iota, n, total);
+        hipError_t e = hipGetLastError();
         size_t tb = temp_bytes;
         if (e == hipSuccess)
             e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys, sorted, iota, perm, total, 0,
                                                    (int)(bits + table_bits(L)), s);
         return e;
     }
-    for (uint32_t t = 0; t < L && e == hipSuccess; ++t) {
-        size_t tb = temp_bytes;
-        e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys + (size_t)t * n,
-                                               sorted + (size_t)t * n, iota,
-                                               perm + (size_t)t * n, n, 0, (int)bits, s);
+    // The table does not fit above the key: sort all entries by key, then
+    // stably by table (two least-significant-digit-first passes of one sort),
+    // instead of L separate sorts.
+    uint8_t *w = (uint8_t *)work;
+    uint64_t *K1 = (uint64_t *)w;
+    uint32_t *E0 = (uint32_t *)(w + (size_t)total * 8);
+    uint32_t *E1 = E0 + total;
+    uint32_t *tkey = E1 + total;
+    uint32_t *tout = tkey + total;
+    uint32_t *idx0 = tout + total;
+    uint32_t *idx2 = idx0 + total;
+    hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, s, E0, total, total);
+    hipError_t e = hipGetLastError();
+    size_t tb = temp_bytes;
+    if (e == hipSuccess)
+        e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys, K1, E0, E1, total, 0, (int)bits,
+                                               s);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(table_of_kernel, grid, dim3(256), 0, s, E1, n, total, tkey, idx0);
+        e = hipGetLastError();
+    }
+    tb = temp_bytes;
+    if (e == hipSuccess)
+        e = hipcub::DeviceRadixSort::SortPairs(temp, tb, tkey, tout, idx0, idx2, total, 0,
+                                               (int)(table_bits(L) ? table_bits(L) : 1), s);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(gather_sorted_kernel, grid, dim3(256), 0, s, K1, E1, idx2, n, total,
+                           sorted, perm);
+        e = hipGetLastError();
     }
     return e;
 }

@@ -101,8 +101,11 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
             return fail(SJ_E_UNSUPPORTED, "n_p = %u, n_q = %u: a table could hold more than 2^%d "
                         "candidate tiles", n_p, n_q, sjl::TILE_BITS);
     }
-    size_t temp_bytes = sjl::sort_temp_bytes(joint ? L * n_p : n_p, sbits);
-    const size_t tq = sjl::sort_temp_bytes(joint ? L * n_q : n_q, sbits);
+    size_t temp_bytes =
+        joint ? sjl::sort_temp_bytes(L * n_p, sbits)
+              : sjl::sort_temp_bytes_split(L * n_p, bits, sjl::table_bits(L));
+    const size_t tq = joint ? sjl::sort_temp_bytes(L * n_q, sbits)
+                            : sjl::sort_temp_bytes_split(L * n_q, bits, sjl::table_bits(L));
     temp_bytes = temp_bytes > tq ? temp_bytes : tq;
     const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
@@ -132,6 +135,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_cnt = take(6 * 8);
     const size_t off_tcnt = take((size_t)L * sjl::CSTRIDE * 8);
     const size_t off_temp = take(temp_bytes);
+    const size_t off_sortw = joint ? 0 : take(sjl::split_work_bytes((uint32_t)(L * n_max)));
     const size_t off_aw = take(a_bytes);
     // keys on the matrix cores where they apply
     const bool fast = sjl::keys_fast_applies(dtype, (uint32_t)krow, L, k, w);
@@ -180,10 +184,10 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
     uint32_t *iota = (uint32_t *)(scr + off_iota);
     SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, iota, n_p, L, bits, joint,
-                            scr + off_temp, temp_bytes, s));
+                            scr + off_temp, temp_bytes, scr + off_sortw, s));
     if (!self)
         SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, joint,
-                                scr + off_temp, temp_bytes, s));
+                                scr + off_temp, temp_bytes, scr + off_sortw, s));
     sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
                         (unsigned long long *)(scr + off_t0), tcnt, (uint32_t)tcap};
     SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));

@@ -126,6 +126,17 @@ def test_lsh_buckets_span_tiles_and_ragged():
     run_lsh(w, h)
 
 
+def test_lsh_quantised_wide_keys_many_rows():
+    """Seven quantised values of 9 bits and 8 tables (63 + 3 bits: the table
+    does not fit above the key, so the entries are sorted by key and then
+    stably by table) on 6000 int8 rows of the squared-L2 workload: the sorts
+    span many radix blocks."""
+    wl = workloads.make_config("l2_i8_1048576x64", n=6000)
+    h = workloads.lsh_params(1303, L=8, k=7, d=wl.d, w=2000)
+    g, ref, exact, cand, _ = run_lsh(wl, h)
+    assert 0 < len(ref) <= exact.total
+
+
 def test_lsh_k0_is_exact_join():
     import paper_2006_12608_amd as sj
     w = case(43, 200, 150, 64, "bf16", "ip", 12.0)
