@@ -163,7 +163,7 @@ int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, co
  *   B  device, L*k int32 offsets (read only when w > 0; may be NULL when w == 0);
  *   w  bucket width (0 = sign hashes).
  * Afterwards sj_get_stats reports kernel = 3, ms_norms = repacking, norms and
- * hashing, ms_scan = the per-table sorts and the bucket pairing, ms_join = the
+ * hashing, ms_scan = the sorts and the bucket pairing, ms_join = the
  * bucket join.
  * Limits: 1 <= L <= 64, 0 <= k <= 64 (k = 0: one bucket per table, the exact
  * join), L * max(n_p, n_q) < 2^26; other arguments, outputs and errors as

@@ -83,7 +83,8 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const bool self = P == Q && n_p == n_q;
     const bool l2 = metric == SJ_L2;
     const uint32_t bits = sjl::key_bits(k, w);
-    // one sort for all tables when the table number fits above the key
+    // one sort for all tables when the table number fits above the key, else a
+    // sort by key and a stable sort by table
     const bool joint = bits + sjl::table_bits(L) <= 64;
     const uint32_t tshift = joint && L > 1 ? bits : 0;
     const uint32_t sbits = joint ? bits + sjl::table_bits(L) : bits;
