@@ -103,3 +103,80 @@ def test_jl_norm_preservation():
     se = ratios.std() / np.sqrt(ratios.size)
     assert abs(ratios.mean() - 1) < 4 * se
     assert (np.abs(np.sqrt(ratios) - 1) <= 0.35).mean() >= 0.95
+
+
+def test_abs_bound_worked_example():
+    """|A_l| ... |A_1| |x| (the scale of the JL parity tolerance) on the
+    hand-worked example, whose second factor and inputs have negative entries:
+    a missing absolute value on x or on either factor changes a value."""
+    g = _golden()
+    shapes = [tuple(int(v) for v in s) for s in g["shapes"]]
+    As = [np.array(g["A1"]), np.array(g["A2"])]
+    B = jl.abs_bound(np.array(g["x"]), shapes, As)
+    assert np.array_equal(B, np.array(g["absbound"]))
+
+
+def _abs_bound_fractions(x, shapes, As):
+    """Lemma 3's levels applied block by block to |x| with |A_i|, in exact
+    rational arithmetic: level i splits its input into r_i blocks of c_i
+    entries and maps each block b to |A_i| b."""
+    from fractions import Fraction
+    v = [abs(Fraction(float(t))) for t in x]
+    for (k, c, r), A in zip(shapes, As):
+        out = []
+        for blk in range(r):
+            seg = v[blk * c:(blk + 1) * c]
+            for row in range(k):
+                out.append(sum(abs(Fraction(float(A[row][col]))) * seg[col] for col in range(c)))
+        v = out
+    return v
+
+
+@pytest.mark.parametrize("shapes", [[(3, 4, 3), (2, 9, 1)], [(4, 2, 4), (2, 4, 4), (3, 8, 1)]])
+def test_abs_bound_exact_rationals(shapes):
+    """abs_bound against an exact, level-by-level evaluation with Fractions on
+    random real inputs and factors of both signs (within the relative
+    rounding of the float64 evaluation, gamma(n) for sums of n nonnegative
+    terms, n at most the dense row length)."""
+    rng = np.random.default_rng(17 + len(shapes))
+    d = shapes[0][1] * shapes[0][2]
+    As = [rng.standard_normal((k, c)) for (k, c, r) in shapes]
+    X = rng.standard_normal((3, d))
+    B = jl.abs_bound(X, shapes, As)
+    u = 2.0 ** -53
+    tol = 4 * d * len(shapes) * u
+    for row in range(X.shape[0]):
+        exact = _abs_bound_fractions(X[row], shapes, As)
+        assert len(exact) == B.shape[1]
+        for got, want in zip(B[row], exact):
+            assert want > 0 and abs(got - float(want)) <= tol * float(want)
+
+
+def test_abs_bound_mutants_are_caught(monkeypatch):
+    """Plausible slips in abs_bound (no absolute value on x, none on a later
+    factor, |M| of the signed product instead of the product of |A_i|) each
+    fail one of the two pins above."""
+    orig_dense = jl.dense_matrix
+
+    def no_abs_x(X, shapes, As):
+        M = orig_dense(np.shape(X)[1], shapes, [np.abs(A) for A in As])
+        return np.asarray(X, np.float64) @ M.T
+
+    def no_abs_last(X, shapes, As):
+        M = orig_dense(np.shape(X)[1], shapes, [np.abs(A) for A in As[:-1]] + [As[-1]])
+        return np.abs(np.asarray(X, np.float64)) @ M.T
+
+    def abs_of_product(X, shapes, As):
+        M = np.abs(orig_dense(np.shape(X)[1], shapes, As))
+        return np.abs(np.asarray(X, np.float64)) @ M.T
+
+    for mutant in (no_abs_x, no_abs_last, abs_of_product):
+        monkeypatch.setattr(jl, "abs_bound", mutant)
+        failed = 0
+        for pin, args in ((test_abs_bound_worked_example, ()),
+                          (test_abs_bound_exact_rationals, ([(3, 4, 3), (2, 9, 1)],))):
+            try:
+                pin(*args)
+            except AssertionError:
+                failed += 1
+        assert failed >= 1, mutant.__name__
