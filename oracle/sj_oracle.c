@@ -265,10 +265,12 @@ int64_t or_count(int metric, int dtype, const void *P, int64_t n_p, const void *
     return total;
 }
 
-/* Scores of the listed (i, j) pairs (metric's score, not the match flag). */
+/* Scores of the listed (i, j) pairs (metric's score, not the match flag).
+ * OpenMP only splits the independent pairs between threads. */
 void or_scores(int metric, int dtype, const void *P, const void *Q, int64_t d,
                const int64_t *pairs, int64_t n_pairs, double *out)
 {
+#pragma omp parallel for schedule(static)
     for (int64_t t = 0; t < n_pairs; ++t) {
         int64_t i = pairs[2 * t], j = pairs[2 * t + 1];
         out[t] = metric == OR_IP ? or_score_ip(dtype, P, i, Q, j, d)

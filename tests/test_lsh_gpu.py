@@ -286,3 +286,51 @@ def test_lsh_full_size_sampled_rows():
     info = compare(g[np.isin(g[:, 0], rows)], ref, True)
     say("rows", rows.size, "pairs", ref.total, "band", info)
     assert ref.total >= 16
+
+
+def test_lsh_quantised_joint_sort_full_key():
+    """Six quantised values of 10 bits and 16 tables (60 key bits + 4 table
+    bits = 64: the table number sits in the top bits of one joint sort key,
+    the benchmark's configuration on the int8 squared-L2 workload) on 6000
+    rows of that workload: parity with the oracle's LSH join and its
+    candidate count."""
+    wl = workloads.make_config("l2_i8_1048576x64", n=6000)
+    h = workloads.lsh_params(1303, L=16, k=6, d=wl.d, w=2000)
+    g, ref, exact, cand, _ = run_lsh(wl, h)
+    assert 0 < len(ref) <= exact.total
+
+
+def test_lsh_full_size_quantised_sampled_rows():
+    """The full int8 squared-L2 workload (1048576 x 64) with the benchmark's
+    LSH parameters (16 tables of 6 quantised projections, width 2000, its
+    seed): the oracle computes every row's keys and, for sampled rows of P
+    (random ones and planted ones), the exact matches; the LSH join's pairs
+    of those rows must be exactly the matches that share a key with them in
+    some table.  Every reported pair must pass the exact test, and none may
+    repeat."""
+    import paper_2006_12608_amd as sj
+    name = "l2_i8_1048576x64"
+    wl = workloads.make_config(name)
+    h = workloads.lsh_params(1300 + workloads.NAMES.index(name), L=16, k=6, d=wl.d, w=2000)
+    Pd, Qd = to_device(wl.P, wl.dtype), to_device(wl.Q, wl.dtype)
+    A, B = lsh_device(h)
+    say("lsh full", wl.name, f"L={h.L} k={h.k} w={h.w}")
+    got, cand = sj.join_lsh(Pd, Qd, wl.threshold, "l2", L=h.L, k=h.k, A=A, B=B, w=h.w)
+    g = sorted_pairs(got)
+    assert np.unique(keys(g)).size == g.shape[0]
+    sc = oracle.scores("l2", wl.dtype, wl.P, wl.Q, g.astype(np.int64))
+    assert np.all(sc <= wl.threshold)
+    rng = np.random.default_rng(4322)
+    rows = np.unique(np.concatenate([rng.choice(wl.n_p, size=24, replace=False),
+                                     wl.planted[:40, 0], wl.planted[-8:, 0]]))
+    kq = oracle.lsh_keys(wl.dtype, wl.Q, h.L, h.k, h.A, h.B, h.w)
+    kp = oracle.lsh_keys(wl.dtype, np.ascontiguousarray(wl.P[rows]), h.L, h.k, h.A, h.B, h.w)
+    ex = oracle.join("l2", wl.dtype, wl.P, wl.Q, wl.threshold, rows=rows)
+    pos = {int(r): t for t, r in enumerate(rows)}
+    keep = np.array([bool((kp[:, pos[int(i)]] == kq[:, int(j)]).any()) for i, j in ex.pairs],
+                    dtype=bool)
+    ref = oracle.JoinResult(ex.pairs[keep], int(keep.sum()), ex.band_pairs, ex.band_match)
+    compare(g[np.isin(g[:, 0], rows)], ref, False)
+    say("rows", rows.size, "exact", ex.total, "found", ref.total, "candidates", cand,
+        "pairs", g.shape[0])
+    assert ref.total >= 30

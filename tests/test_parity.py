@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_util import compare, gpu_join, sorted_pairs, to_device
+from gpu_util import compare, gpu_join, keys, sorted_pairs, to_device
 from pins import values
 
 pytestmark = pytest.mark.gpu
@@ -316,39 +316,80 @@ def test_self_join_same_pointer_all_variants():
             assert s == {(j, i) for (i, j) in s}
 
 
-# ------------------------------------------------ full-size, sampled rows
+# --------------------------------------------------- full-size workloads
 
 def _sample_rows(n, k, seed):
     rng = np.random.default_rng(seed)
     return np.sort(rng.choice(n, size=k, replace=False))
 
 
-@pytest.mark.parametrize("k,n_rows,two_pass", [("ip_bf16_65536x128", 48, False),
-                                                ("cos_f16_262144x256", 12, False),
-                                                ("l2_i8_1048576x64", 12, False),
-                                                ("ip_bf16_clustered_131072x1024", 8, True)])
-def test_full_size_sampled_rows(k, n_rows, two_pass):
+def _keys_torch(pairs):
+    import torch
+    return pairs[:, 0].to(torch.int64) * (1 << 32) + pairs[:, 1].to(torch.int64)
+
+
+# (workload, sampled rows of P for the false-negative check, two-pass,
+#  emitted pairs rescored: "all", or the size of a random sample)
+FULL = [("ip_bf16_65536x128", 128, False, "all"),
+        ("cos_f16_262144x256", 32, False, "all"),
+        ("l2_i8_1048576x64", 64, False, "all"),
+        ("ip_bf16_clustered_131072x1024", 16, True, 1_000_000)]
+
+
+@pytest.mark.parametrize("k,n_rows,two_pass,rescore", FULL)
+def test_full_size(k, n_rows, two_pass, rescore):
     """The full workload on the GPU in the launch configuration the benchmark
-    uses; the oracle recomputes a sample of P's rows against all of Q."""
+    uses, checked three ways.
+    No false positive anywhere: the oracle rescores every emitted pair (on the
+    clustered workload, whose 5.2e8 pairs are too many for the oracle's loops,
+    a random sample of 10^6 of them) and each one must pass the exact test
+    (real-valued inputs: or lie inside the boundary band).
+    No false negative: every planted pair is in the output and no decoy is
+    (the int8 workload's 1000 pairs at exactly r^2 = 2000 among the planted,
+    its 1000 decoys at 2001), and for a random sample of P's rows the
+    oracle's matches against all of Q equal the GPU's.
+    No duplicates, and the output size equals sj_count's total."""
     import torch
     import paper_2006_12608_amd as sj
     w = workloads.make_config(k)
     Pd, Qd = to_device(w.P, w.dtype), to_device(w.Q, w.dtype)
-    rows = _sample_rows(w.n_p, n_rows, 77 + workloads.NAMES.index(k))
-    if w.planted.size:   # include some planted rows
-        rows = np.unique(np.concatenate([rows, w.planted[:4, 0]]))
-    say("full size", w.name, "rows", rows.size, "two_pass", two_pass)
+    say("full size", w.name, "two_pass", two_pass, "rescore", rescore)
     total = sj.count(Pd, Qd, w.threshold, w.metric)
     out = torch.empty((total, 2), dtype=torch.int32, device="cuda")
     f = sj.join_ip if w.metric == "ip" else sj.join_l2
     pairs = f(Pd, Qd, w.threshold, cap=total, out=out, two_pass=two_pass)
     assert pairs.shape[0] == total
-    sel = torch.isin(pairs[:, 0], torch.from_numpy(rows.astype(np.int32)).cuda())
-    g = sorted_pairs(pairs[sel])
     band = 1e-3 * abs(w.threshold) if w.real_valued else 0.0
+    kd = _keys_torch(pairs)
+    if rescore == "all":
+        gk = np.sort(kd.cpu().numpy().astype(np.uint64))
+        assert np.unique(gk).size == gk.size, "duplicate pairs in the GPU output"
+        sel = np.stack([(gk >> np.uint64(32)).astype(np.int64),
+                        (gk & np.uint64(0xFFFFFFFF)).astype(np.int64)], 1)
+    else:
+        assert torch.unique(kd).numel() == total, "duplicate pairs in the GPU output"
+        rng = np.random.default_rng(91)
+        idx = torch.from_numpy(rng.choice(total, size=min(rescore, total), replace=False)).cuda()
+        sel = pairs[idx].cpu().numpy().view(np.uint32).astype(np.int64)
+        gk = None
+    del kd
+    sc = oracle.scores(w.metric, w.dtype, w.P, w.Q, sel)
+    ok = sc >= w.threshold - band if w.metric == "ip" else sc <= w.threshold + band
+    in_band = int(np.sum(np.abs(sc - w.threshold) <= band)) if band else 0
+    say("rescored", sel.shape[0], "pairs; failing", int((~ok).sum()), "in band", in_band)
+    assert ok.all(), f"false positives: {sel[~ok][:5].tolist()} scores {sc[~ok][:5].tolist()}"
+    if w.planted.size:
+        pk = keys(w.planted)
+        assert np.isin(pk, gk).all(), "planted pairs missing"
+    if w.decoys.size:
+        assert not np.isin(keys(w.decoys), gk).any(), "decoys reported"
+        ties = oracle.scores(w.metric, w.dtype, w.P, w.Q, w.planted[-(w.decoys.shape[0]):])
+        assert np.all(ties == w.threshold)   # the exact ties are among the planted pairs
+    rows = _sample_rows(w.n_p, n_rows, 77 + workloads.NAMES.index(k))
+    if w.planted.size:   # include some planted rows
+        rows = np.unique(np.concatenate([rows, w.planted[:4, 0]]))
+    sel_rows = torch.isin(pairs[:, 0], torch.from_numpy(rows.astype(np.int32)).cuda())
+    g = sorted_pairs(pairs[sel_rows])
     ref = oracle.join(w.metric, w.dtype, w.P, w.Q, w.threshold, rows=rows, band=band)
     info = compare(g, ref, w.real_valued)
-    say("total", total, "sampled", ref.total, info)
-    if w.planted.size:
-        pl = w.planted[np.isin(w.planted[:, 0], rows)]
-        assert set(map(tuple, pl.tolist())) <= set(map(tuple, g.astype(np.int64).tolist()))
+    say("total", total, "rows", rows.size, "sampled matches", ref.total, info)
