@@ -42,7 +42,10 @@
  *
  * Sizes: n_p, n_q < 2^32; 0 <= d <= 65536 for fp16/bf16 and d <= 32768 for
  * int8 (larger d could overflow the int32 accumulators); n_p, n_q or d equal
- * to 0 are valid (d = 0 makes every score 0).
+ * to 0 are valid.  n_p = 0 or n_q = 0 gives no pairs.  d = 0 follows the
+ * join's definition rather than returning nothing: points of R^0 all
+ * coincide, every inner product and squared distance is 0, so every pair
+ * matches when s <= 0 (IP) or r2 >= 0 (L2) and none otherwise.
  */
 #ifndef SJ_H
 #define SJ_H
@@ -135,9 +138,13 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
                uint32_t d, double r2, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
                unsigned flags);
 
-/* Number of matches of the join with metric `metric` (SJ_IP: threshold s,
- * SJ_L2: threshold r2), stored in *count (host); writes no pairs.  Runs the
- * counting pass and the scan of the count-then-emit protocol. */
+/* Size of the similarity join of Section 4 (the number of pairs (x, y), x in
+ * P, y in Q, within the threshold) with metric `metric` (SJ_IP: <P_i, Q_j> >=
+ * threshold, SJ_L2: ||P_i - Q_j||^2 <= threshold), stored in *count (host);
+ * writes no pairs.  Runs the counting pass and the scan of the count-then-emit
+ * protocol, with the arithmetic, threshold rounding and errors of
+ * sj_join_ip / sj_join_l2.  A caller sizes `pairs` with it before a
+ * count-then-emit call. */
 int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
              uint32_t n_q, uint32_t d, double threshold, uint64_t *count);
 

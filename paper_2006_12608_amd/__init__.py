@@ -2,8 +2,8 @@
 Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
 
 The raw C-ABI entry points are exposed under their C names (sj_create,
-sj_join_ip, sj_join_l2, sj_count, sj_join_lsh, sj_destroy, sj_get_stats,
-sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
+sj_join_ip, sj_join_l2, sj_count, sj_join_lsh, sj_jl,
+sj_destroy, sj_get_stats, sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
 `join_lsh` (the LSH-bucketed join of Theorem 3) are conveniences over PyTorch
 device tensors.  This module only marshals
 arguments: every step of the join runs in the library's HIP kernels.  Import
@@ -196,6 +196,9 @@ def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
     import torch
     _check_pair(P, Q)
     ctx = ctx or context(P.device.index)
+    if two_pass is None:
+        # no capacity given: count-then-emit sizes the output exactly
+        two_pass = cap is None and out is None
     flags = ((SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
              | (SJ_FLAG_RECOMPUTE if recompute else 0))
     if cap is None and out is None:
@@ -213,16 +216,18 @@ def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
     return out[:n]
 
 
-def join_ip(P, Q, s: float, cap: int | None = None, two_pass: bool = False, timing: bool = False,
-            ctx=None, out=None, recompute: bool = False):
+def join_ip(P, Q, s: float, cap: int | None = None, two_pass: bool | None = None,
+            timing: bool = False, ctx=None, out=None, recompute: bool = False):
     """All (i, j) with <P_i, Q_j> >= s as an (n, 2) int32 tensor of uint32
-    indices.  With cap=None the exact size is counted first.  two_pass selects
-    count-then-emit; recompute makes its second pass repeat the product even
-    where the first pass's match bits would be kept."""
+    indices.  With cap=None (and no `out`) the output is sized by sj_count and
+    filled by count-then-emit (deterministic order) unless two_pass=False asks
+    for the single pass; with a capacity the single pass runs unless
+    two_pass=True.  recompute makes the second pass of count-then-emit repeat
+    the product even where the first pass's match bits would be kept."""
     return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out, recompute)
 
 
-def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool = False,
+def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool | None = None,
             timing: bool = False, ctx=None, out=None, recompute: bool = False):
     """All (i, j) with ||P_i - Q_j||^2 <= r2 (see join_ip)."""
     return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out, recompute)

@@ -32,6 +32,7 @@ def sorted_pairs(pairs) -> np.ndarray:
 
 
 def gpu_join(metric, Pd, Qd, thr, cap=None, two_pass=False, timing=False):
+    """The library's join; two_pass=False is the single pass (sized by sj_count)."""
     import paper_2006_12608_amd as sj
     f = sj.join_ip if metric == "ip" else sj.join_l2
     return f(Pd, Qd, thr, cap=cap, two_pass=two_pass, timing=timing)

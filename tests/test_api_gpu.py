@@ -119,3 +119,40 @@ def test_two_contexts_two_streams(env):
     with torch.cuda.stream(s1):
         c = sj.count(P, P, 20.0)
     assert c == ref
+
+
+def test_python_default_is_count_then_emit(env):
+    """join_ip / join_l2 without a capacity size the output with sj_count and
+    fill it by count-then-emit: the order is deterministic and equals an
+    explicit two-pass call's; with two_pass=False the same set comes from the
+    single pass."""
+    sj, ctx, torch = env
+    say("python default")
+    P = torch.randint(-4, 5, (700, 64), dtype=torch.int8, device="cuda")
+    Q = torch.randint(-4, 5, (650, 64), dtype=torch.int8, device="cuda")
+    for f, thr in ((sj.join_ip, 40.0), (sj.join_l2, 700.0)):
+        a = f(P, Q, thr, ctx=ctx)
+        b = f(P, Q, thr, ctx=ctx)
+        assert a.shape[0] > 0 and torch.equal(a, b)
+        c = f(P, Q, thr, cap=a.shape[0], two_pass=True, ctx=ctx)
+        assert torch.equal(a, c)
+        d = f(P, Q, thr, two_pass=False, ctx=ctx)
+        ka = (a[:, 0].long() << 32 | a[:, 1].long()).sort().values
+        kd = (d[:, 0].long() << 32 | d[:, 1].long()).sort().values
+        assert torch.equal(ka, kd)
+
+
+def test_zero_dimension_reading(env):
+    """d = 0: points of R^0 all coincide (every score is 0): every pair for
+    s <= 0 or r2 >= 0, none otherwise, in both modes and through sj_count."""
+    sj, ctx, torch = env
+    say("d = 0")
+    P0 = torch.zeros((7, 0), dtype=torch.bfloat16, device="cuda")
+    Q0 = torch.zeros((9, 0), dtype=torch.bfloat16, device="cuda")
+    for two_pass in (False, True):
+        assert sj.join_ip(P0, Q0, 0.0, two_pass=two_pass, ctx=ctx).shape[0] == 63
+        assert sj.join_ip(P0, Q0, 1e-30, two_pass=two_pass, ctx=ctx).shape[0] == 0
+        assert sj.join_l2(P0, Q0, 0.0, two_pass=two_pass, ctx=ctx).shape[0] == 63
+        assert sj.join_l2(P0, Q0, -1e-30, two_pass=two_pass, ctx=ctx).shape[0] == 0
+    assert sj.count(P0, Q0, -5.0, "ip", ctx=ctx) == 63
+    assert sj.count(P0, Q0, 3.0, "l2", ctx=ctx) == 63
