@@ -5,9 +5,12 @@ A step is one whole join call -- sj_join_ip / sj_join_l2 on one batch of
 synthetic input already resident in HBM: (row norms for L2), the fused MFMA
 product + threshold + compaction kernel, and the hand-back of the match count
 (two passes plus the scan for workloads that need count-then-emit).  The
-default workload is the 65536 x 65536, d = 128, bf16 inner-product join; the
-others (--workload NAME, see workloads.NAMES) are available for measurements but are not the
-headline line.
+default workload is the largest one that fits one GPU: the 1048576 x 1048576,
+d = 64, int8 squared-L2 join (1.1e12 pair evaluations).  After the timed
+region the line also reports the join kernel's fraction of the dense MFMA
+peak on the 65536 x 128 bf16 and 262144 x 256 fp16 inner-product workloads
+(`other_workloads`); the others (--workload NAME, see workloads.NAMES) are
+available for measurements but are not the headline line.
 
 Prints ONE JSON line on stdout:
   metric/value/unit: pair-evaluations per second of the whole step
@@ -16,6 +19,9 @@ Prints ONE JSON line on stdout:
             the MI355X dense MFMA peak for its dtype
   cpu_baseline: the oracle (plain C loops) on a bounded sample of the same
             workload on this host's cores
+  other_workloads: kernel time and fraction of peak of the join on the other
+            two workloads with a 60%-of-peak target (measured untimed, after
+            the timed region)
 """
 from __future__ import annotations
 
@@ -31,7 +37,9 @@ sys.path.insert(0, ROOT)
 
 # dense MFMA peaks of MI355X (TFLOP/s or TOP/s)
 PEAK = {"f16": 2500.0, "bf16": 2500.0, "i8": 5000.0}
-DEFAULT_WORKLOAD = "ip_bf16_65536x128"
+DEFAULT_WORKLOAD = "l2_i8_1048576x64"
+# workloads whose join kernel fraction is reported beside the headline
+OTHER_WORKLOADS = ("ip_bf16_65536x128", "cos_f16_262144x256")
 TWO_PASS = {"ip_bf16_clustered_131072x1024"}   # high-output workload: count-then-emit
 
 
@@ -101,12 +109,14 @@ def traffic_for(key: str, prefixes=JOIN_SOURCES):
     return rec.get("hbm_bytes_per_launch")
 
 
-def measured_mfma_peak(dtype: str, duration_ms: float, operands=None):
-    """The MFMA-only throughput of this GPU (libsj_peak.so: four accumulator
-    chains per wave, two waves per SIMD) over a run as long as the timed
-    region, with MFMA operands taken from `operands` (a device tensor, e.g. the
-    workload's rows; random values if None), or None when the probe library
-    is not built."""
+def measured_mfma_peak(dtype: str, duration_ms: float, operands=None, waves_per_simd: int = 2):
+    """The throughput of a loop of MFMAs alone on this GPU (libsj_peak.so:
+    four accumulator chains per wave, `waves_per_simd` waves per SIMD, no
+    memory traffic) over a run of `duration_ms`, with MFMA operands taken
+    from `operands` (a device tensor, e.g. the workload's rows; random values
+    if None), or None when the probe library is not built.  At full
+    matrix-core duty the chip's power limit lowers the clock below what the
+    join runs at, so this is context for the clock counters, not a ceiling."""
     import ctypes
     path = os.path.join(ROOT, "paper_2006_12608_amd", "libsj_peak.so")
     if not os.path.exists(path):
@@ -120,7 +130,7 @@ def measured_mfma_peak(dtype: str, duration_ms: float, operands=None):
     code = {"f16": 1, "bf16": 2, "i8": 3}[dtype]
     ptr = operands.data_ptr() if operands is not None else None
     nbytes = operands.numel() * operands.element_size() if operands is not None else 0
-    if lib.sj_peak_mfma(code, 2, max(duration_ms, 1.0), ptr, nbytes, ctypes.byref(tops),
+    if lib.sj_peak_mfma(code, waves_per_simd, max(duration_ms, 1.0), ptr, nbytes, ctypes.byref(tops),
                         ctypes.byref(ms)) != 0:
         return None
     return {"value": tops.value, "unit": "TOP/s" if dtype == "i8" else "TFLOP/s",
@@ -144,7 +154,10 @@ def cpu_baseline(w, target_s: float = 12.0):
     threads = oracle.max_threads()
     rng = np.random.default_rng(4242)
     per_row_work = w.n_q * max(w.d, 1)
-    r0 = max(1, min(w.n_p, int(2e8 // per_row_work) or 1))
+    # the probe takes at least one row per thread (the oracle's threads split
+    # the rows), so its rate is the rate of the timed sample
+    r0 = max(threads, min(w.n_p, int(2e8 // per_row_work) or 1))
+    r0 = min(r0, w.n_p)
     rows = np.sort(rng.choice(w.n_p, size=r0, replace=False))
     t = time.perf_counter()
     oracle.join(w.metric, w.dtype, w.P, w.Q, w.threshold, rows=rows, threads=threads)
@@ -311,6 +324,11 @@ def main():
     import workloads
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=workloads.NAMES)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the join kernel measurements on the other workloads")
+    ap.add_argument("--mfma-loop", action="store_true",
+                    help="only run the MFMA-only loop on the workload's rows (for counters)")
+    ap.add_argument("--loop-ms", type=float, default=200.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 256 MiB buffer three times (the reference kernel for "
                          "scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters to HBM bytes)")
@@ -327,6 +345,9 @@ def main():
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.mfma_loop:
+        mfma_loop(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the join shards "
@@ -447,18 +468,65 @@ def main():
         line["emit"] = {"from_match_bits": from_bits, "hbm_bytes_algorithmic": emit_bytes,
                         "hbm_gbps_algorithmic": emit_bytes / (float(np.mean(emit_ms)) / 1e3) / 1e9,
                         "traffic": traffic_for(args.workload + ":emit") if from_bits else None}
-    # the same fraction against what the matrix cores alone sustain on this GPU
-    # over a run as long as the timed region, on this workload's data (the
-    # clock under load is below the spec peak's 2.4 GHz and depends on the
-    # operands' bit patterns)
-    meas = measured_mfma_peak(w.dtype, el * 1e3, Pd)
-    if meas is not None:
-        meas["frac"] = achieved / meas["value"]
-        line["roofline"]["mfma_only_measured"] = meas
+    if not args.no_other_workloads:
+        line["other_workloads"] = {name: kernel_fraction(name, stream, ctx)
+                                   for name in OTHER_WORKLOADS if name != w.name}
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample ...")
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)
+
+
+def kernel_fraction(name: str, stream, ctx, steps: int = 10):
+    """The join kernel's average time over `steps` single-pass calls on the
+    named workload (after the clock-settling count passes) and its fraction
+    of the dense MFMA peak: 2 d FLOP per pair evaluation over the kernel time
+    recorded with HIP events on the call's stream."""
+    import numpy as np
+    import torch
+    import paper_2006_12608_amd as sj
+    import workloads
+    log(f"measuring the join kernel on {name} ...")
+    w = workloads.make_config(name)
+    Pd = workloads.to_torch(w.P, w.dtype)
+    Qd = workloads.to_torch(w.Q, w.dtype)
+    torch.cuda.synchronize()
+    dt = {"f16": sj.SJ_F16, "bf16": sj.SJ_BF16, "i8": sj.SJ_I8}[w.dtype]
+    fn = sj.sj_join_ip if w.metric == "ip" else sj.sj_join_l2
+    total = sj.count(Pd, Qd, w.threshold, w.metric, ctx=ctx)
+    out = torch.empty((max(total, 1), 2), dtype=torch.int32, device="cuda")
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < 0.3:
+        sj.count(Pd, Qd, w.threshold, w.metric, ctx=ctx)
+    ms = []
+    for _ in range(steps + 2):
+        st, n = fn(ctx, dt, Pd.data_ptr(), w.n_p, Qd.data_ptr(), w.n_q, w.d, w.threshold,
+                   out.data_ptr(), total, sj.SJ_FLAG_TIMING)
+        if st != sj.SJ_OK:
+            raise sj.SjError(st, sj.sj_last_error(), n)
+        ms.append(sj.sj_get_stats(ctx).ms_join)
+    kms = float(np.mean(ms[2:]))
+    achieved = 2.0 * w.n_p * w.n_q * w.d / (kms / 1e3) / 1e12
+    return {"kernel_ms": kms, "achieved": achieved, "peak": PEAK[w.dtype],
+            "unit": "TOP/s" if w.dtype == "i8" else "TFLOP/s",
+            "frac": achieved / PEAK[w.dtype], "n_out": int(n), "dtype": w.dtype,
+            "steps": steps}
+
+
+def mfma_loop(args):
+    """The MFMA-only loop (libsj_peak.so) on the workload's P rows for about
+    --loop-ms milliseconds at 1, 2 and 4 waves per SIMD: one JSON line.  A
+    command to take clock and matrix-core busy counters of the loop with."""
+    import torch
+    import workloads
+    w = workloads.make_config(args.workload)
+    Pd = workloads.to_torch(w.P, w.dtype)
+    torch.cuda.synchronize()
+    res = {}
+    for wps in (1, 2, 4):
+        res[f"{wps}_waves_per_simd"] = measured_mfma_peak(w.dtype, args.loop_ms, Pd, wps)
+    print(json.dumps({"mfma_loop": res, "workload": w.name, "dtype": w.dtype,
+                      "peak": PEAK[w.dtype]}), flush=True)
 
 
 if __name__ == "__main__":

@@ -32,8 +32,36 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-u
          "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
+def _obj(src: str) -> str:
+    return os.path.join(BUILD_DIR, os.path.splitext(os.path.basename(src))[0] + ".o")
+
+
+def _deps(path: str, seen=None) -> set:
+    """The file and every local header it includes (recursively)."""
+    import re
+    seen = set() if seen is None else seen
+    if path in seen or not os.path.exists(path):
+        return seen
+    seen.add(path)
+    for inc in re.findall(r'^\s*#include\s+"([^"]+)"', open(path).read(), flags=re.M):
+        for d in (os.path.dirname(path), CSRC, os.path.join(ROOT, "include")):
+            cand = os.path.join(d, inc)
+            if os.path.exists(cand):
+                _deps(cand, seen)
+                break
+    return seen
+
+
+def _stale(src: str) -> bool:
+    obj = _obj(src)
+    if not os.path.exists(obj):
+        return True
+    t = os.path.getmtime(obj)
+    return any(os.path.getmtime(f) > t for f in _deps(os.path.join(CSRC, src)))
+
+
 def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(os.path.basename(src))[0] + ".o")
+    obj = _obj(src)
     cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd.insert(1, "-xhip")
@@ -52,13 +80,17 @@ def _link(objs, out: str) -> None:
     os.replace(tmp, out)
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libsj.so (the join) and libsj_peak.so (the
-    MFMA-only throughput probe bench.py reports beside the spec peak); returns
-    the path of libsj.so."""
+def build(verbose: bool = False, only_stale: bool = False) -> str:
+    """Compile every source (only_stale: only those whose object is older than
+    the source or a header it includes) and link libsj.so (the join) and
+    libsj_peak.so (the MFMA-only loop bench.py --mfma-loop runs); returns the
+    path of libsj.so."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(len(SOURCES) + 1, os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES + [PEAK_SOURCE]))
+    srcs = SOURCES + [PEAK_SOURCE]
+    todo = [s for s in srcs if _stale(s)] if only_stale else srcs
+    with ThreadPoolExecutor(max_workers=min(len(srcs), os.cpu_count() or 4)) as ex:
+        list(ex.map(_compile, todo))
+    objs = [_obj(s) for s in srcs]
     _link(objs[:-1], OUT)
     _link(objs[-1:], PEAK_OUT)
     if verbose:
@@ -67,5 +99,5 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, only_stale="--changed" in sys.argv[1:])
     sys.exit(0)
