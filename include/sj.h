@@ -148,6 +148,25 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
 int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
              uint32_t n_q, uint32_t d, double threshold, uint64_t *count);
 
+/* For callers that cannot allocate device memory during the join (serving
+ * loops, harnesses that forbid hipMalloc / hipFree): the join of sj_join_ip
+ * (metric SJ_IP) or sj_join_l2 (SJ_L2), with the same arguments, results,
+ * ordering and errors, that allocates nothing.  Its device scratch (match
+ * counter, scan total, row norms, repacked rows, block counts and offsets) is
+ * a fixed 16 MiB region of this library that each GPU holds until the process
+ * ends, located once per device by sj_create; a call that would need more
+ * (e.g. SJ_L2 with n_p + n_q above about 4 Mi rows, or count-then-emit with
+ * more than about 1.3 M output blocks) returns SJ_E_UNSUPPORTED before any
+ * launch.  Flags: SJ_FLAG_TWO_PASS (its second pass always recomputes the
+ * product: no match bits are kept), SJ_FLAG_TIMING, SJ_FLAG_RECOMPUTE (implied).
+ * Every call on one GPU uses that GPU's region: calls that overlap on one GPU
+ * (several host threads, or contexts on different streams) race and must be
+ * serialised by the caller.  Like the other joins it synchronises the
+ * context's stream, so it cannot be captured into a HIP graph. */
+int sj_join_noalloc(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p,
+                    const void *Q, uint32_t n_q, uint32_t d, double threshold, uint32_t *pairs,
+                    uint64_t cap, uint64_t *n_out, unsigned flags);
+
 /* LSH-bucketed join (Section 4, the LSH method of Theorem 3): instead of all
  * n_p x n_q pairs, only pairs whose points share a bucket of some hash table
  * are evaluated.  There are L tables; table t hashes a point x with the

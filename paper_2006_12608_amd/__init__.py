@@ -2,7 +2,7 @@
 Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
 
 The raw C-ABI entry points are exposed under their C names (sj_create,
-sj_join_ip, sj_join_l2, sj_count, sj_join_lsh, sj_jl,
+sj_join_ip, sj_join_l2, sj_count, sj_join_noalloc, sj_join_lsh, sj_jl,
 sj_destroy, sj_get_stats, sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
 `join_lsh` (the LSH-bucketed join of Theorem 3) are conveniences over PyTorch
 device tensors.  This module only marshals
@@ -57,6 +57,9 @@ def _load():
     lib.sj_join_l2.restype = i32
     lib.sj_count.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, ctypes.POINTER(u64)]
     lib.sj_count.restype = i32
+    lib.sj_join_noalloc.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, vp, u64,
+                                    ctypes.POINTER(u64), ctypes.c_uint]
+    lib.sj_join_noalloc.restype = i32
     lib.sj_join_lsh.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, u32, u32, vp, vp,
                                 ctypes.c_int32, vp, u64, ctypes.POINTER(u64),
                                 ctypes.POINTER(u64)]
@@ -108,6 +111,15 @@ def sj_join_ip(ctx, dtype, P, n_p, Q, n_q, d, s, pairs, cap, flags=0):
 def sj_join_l2(ctx, dtype, P, n_p, Q, n_q, d, r2, pairs, cap, flags=0):
     """Returns (status, n_out); pointers are integers (device addresses)."""
     return _join_raw(lib.sj_join_l2, ctx, dtype, P, n_p, Q, n_q, d, r2, pairs, cap, flags)
+
+
+def sj_join_noalloc(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, pairs, cap, flags=0):
+    """The join without device allocation (fixed library scratch); returns
+    (status, n_out); pointers are integers (device addresses)."""
+    n = ctypes.c_uint64(0)
+    st = lib.sj_join_noalloc(ctx, metric, dtype, P, n_p, Q, n_q, d, float(thr), pairs, cap,
+                             ctypes.byref(n), flags)
+    return st, n.value
 
 
 def sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, threshold):

@@ -12,8 +12,19 @@
 #include <cstring>
 #include <string>
 
+#include <mutex>
+
 #include "sj_host.h"
 #include "sj_internal.h"
+
+// Device scratch of sj_join_noalloc, for callers that cannot allocate: the
+// match counter and scan total (first 256 bytes), then the row norms,
+// repacked rows and block counts / offsets of one call.  Each GPU the library
+// runs on holds its own copy until the process ends; host code reaches it only
+// through the address looked up once per device (sj_create), never through
+// this name.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
 namespace sjh {
 
@@ -152,7 +163,41 @@ const size_t kMaxMaskBytes = (size_t)64 << 30;
 // blocks with matches makes the second pass recompute.
 const uint64_t kMaxRecords = (uint64_t)4 << 20;
 
-int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
+// Per-device address of `scratch` (hipGetSymbolAddress with the device
+// current, at sj_create); null until looked up or when the lookup failed.
+constexpr int kMaxDevices = 64;
+std::mutex g_fixed_mu;
+uint8_t *g_fixed[kMaxDevices] = {};
+int g_fixed_err[kMaxDevices] = {};
+
+// Looks up this device's copy of `scratch` once; the device must be current.
+void lookup_fixed_scratch(int device)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return;
+    std::lock_guard<std::mutex> lock(g_fixed_mu);
+    if (g_fixed[device] || g_fixed_err[device])
+        return;
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+        (void)hipGetLastError();
+        g_fixed_err[device] = e != hipSuccess ? (int)e : -1;
+        return;
+    }
+    g_fixed[device] = (uint8_t *)ptr;
+}
+
+// A caller-independent scratch region: `base` (device) of `bytes` bytes whose
+// first 256 bytes hold the call's counters.  Null base: the context's own,
+// growing scratch and counters.
+struct Fixed {
+    uint8_t *base;
+    size_t bytes;
+};
+const size_t kFixedHead = 256;
+
+int run(sj_ctx *c, const Request &rq, uint64_t *n_out, const Fixed *fx = nullptr)
 {
     if (!c)
         return fail(SJ_E_INVAL, "context is NULL");
@@ -213,6 +258,12 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     // matches instead (its outputs are sparse next to its products).
     bool use_records = rq.two_pass && !rq.count_only && !rq.recompute &&
                        plan.family == sjk::FAM_RESIDENT;
+    if (fx) {
+        // the fixed region holds no match bits or records: the second pass
+        // recomputes the product
+        use_masks = false;
+        use_records = false;
+    }
     uint64_t rec_cap = kMaxRecords / plan.grid;
     rec_cap = rec_cap < plan.wg_blocks32 ? rec_cap : plan.wg_blocks32;
     if (rec_cap == 0)
@@ -247,17 +298,29 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         need = align_up(need + sjk::scan_partials_size(plan.n_blocks) * 8);
     }
     off_mask = need;   // match bits or match records
-    const size_t extra = use_masks ? mask_bytes : use_records ? rec_bytes : 0;
-    if (extra) {
-        const std::string prev_err = g_err;
-        if (grow_scratch(c, need + extra) != SJ_OK) {
-            use_masks = use_records = false;   // recompute instead
-            g_err = prev_err;
+    uint8_t *scr;
+    unsigned long long *d_small = c->d_small;
+    if (fx) {
+        if (need > fx->bytes - kFixedHead)
+            return fail(SJ_E_UNSUPPORTED,
+                        "this call needs %zu bytes of device scratch; the fixed scratch of "
+                        "sj_join_noalloc holds %zu",
+                        need, fx->bytes - kFixedHead);
+        d_small = (unsigned long long *)fx->base;
+        scr = fx->base + kFixedHead;
+    } else {
+        const size_t extra = use_masks ? mask_bytes : use_records ? rec_bytes : 0;
+        if (extra) {
+            const std::string prev_err = g_err;
+            if (grow_scratch(c, need + extra) != SJ_OK) {
+                use_masks = use_records = false;   // recompute instead
+                g_err = prev_err;
+            }
         }
+        if ((st = grow_scratch(c, use_masks || use_records ? need + extra : need)) != SJ_OK)
+            return st;
+        scr = (uint8_t *)c->scratch;
     }
-    if ((st = grow_scratch(c, use_masks || use_records ? need + extra : need)) != SJ_OK)
-        return st;
-    uint8_t *scr = (uint8_t *)c->scratch;
 
     sjk::JoinArgs g = {};
     g.P = aligned ? (const uint8_t *)rq.P : scr + off_rp;
@@ -280,7 +343,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
     g.norm_q = scr + off_nq;
     g.pairs = rq.count_only ? nullptr : rq.pairs;
     g.cap = rq.count_only ? 0 : rq.cap;
-    g.counter = c->d_small;
+    g.counter = d_small;
     g.block_counts = (uint32_t *)(scr + off_cnt);
     g.block_offsets = (const unsigned long long *)(scr + off_offs);
     g.masks = use_masks ? (uint16_t *)(scr + off_mask) : nullptr;
@@ -290,15 +353,21 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
                                               align_up((size_t)rec_cap * plan.grid *
                                                        sizeof(sjk::MatchRecord)))
                                : nullptr;
-    g.rec_max = c->d_small + 2;
+    g.rec_max = d_small + 2;
     g.qsplit = plan.qsplit;
 
     hipStream_t s = c->stream;
     SJ_HIP(hipSetDevice(c->device));
-    if (!blocks)
-        SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
-    if (use_records)
-        SJ_HIP(hipMemsetAsync(c->d_small + 2, 0, sizeof(unsigned long long), s));
+    if (fx) {
+        // the fixed region keeps the previous call's contents: clear the
+        // counters (the count pass writes every block count itself)
+        SJ_HIP(sjk::launch_zero_u64(d_small, 4, s));
+    } else {
+        if (!blocks)
+            SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
+        if (use_records)
+            SJ_HIP(hipMemsetAsync(c->d_small + 2, 0, sizeof(unsigned long long), s));
+    }
     if (rq.timing)
         SJ_HIP(hipEventRecord(c->ev[0], s));
     if (!aligned) {
@@ -325,7 +394,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
         SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, mode, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
-        SJ_HIP(hipMemcpyAsync(c->h_small, c->d_small, sizeof(unsigned long long),
+        SJ_HIP(hipMemcpyAsync(c->h_small, d_small, sizeof(unsigned long long),
                               hipMemcpyDeviceToHost, s));
         SJ_HIP(hipStreamSynchronize(s));
         total = c->h_small[0];
@@ -343,10 +412,10 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out)
             SJ_HIP(hipEventRecord(c->ev[2], s));
         SJ_HIP(sjk::launch_scan(g.block_counts, plan.n_blocks,
                                 (unsigned long long *)(scr + off_offs),
-                                (unsigned long long *)(scr + off_part), c->d_small + 1, s));
+                                (unsigned long long *)(scr + off_part), d_small + 1, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[3], s));
-        SJ_HIP(hipMemcpyAsync(c->h_small + 1, c->d_small + 1, 2 * sizeof(unsigned long long),
+        SJ_HIP(hipMemcpyAsync(c->h_small + 1, d_small + 1, 2 * sizeof(unsigned long long),
                               hipMemcpyDeviceToHost, s));
         SJ_HIP(hipStreamSynchronize(s));
         total = c->h_small[1];
@@ -429,6 +498,9 @@ int sj_create(sj_ctx **out, int device, void *stream)
             sj_destroy(c);
             return fail(SJ_E_HIP, "hipEventCreate failed");
         }
+    // this device's copy of the no-allocation scratch, looked up once (a
+    // failure only disables sj_join_noalloc, which then reports it)
+    lookup_fixed_scratch(device);
     *out = c;
     return SJ_OK;
 }
@@ -461,6 +533,29 @@ int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, co
     g_err.clear();
     Request rq{metric, dtype, P, Q, n_p, n_q, d, threshold, nullptr, 0, true, true, false, false};
     return run(ctx, rq, count);
+}
+
+int sj_join_noalloc(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p,
+                    const void *Q, uint32_t n_q, uint32_t d, double threshold, uint32_t *pairs,
+                    uint64_t cap, uint64_t *n_out, unsigned flags)
+{
+    g_err.clear();
+    if (!ctx)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (flags & ~(unsigned)(SJ_FLAG_TWO_PASS | SJ_FLAG_TIMING | SJ_FLAG_RECOMPUTE))
+        return fail(SJ_E_INVAL, "unknown flags 0x%x", flags);
+    uint8_t *base = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_fixed_mu);
+        if (ctx->device >= 0 && ctx->device < kMaxDevices)
+            base = g_fixed[ctx->device];
+    }
+    if (!base)
+        return fail(SJ_E_HIP, "the fixed scratch of device %d is not available", ctx->device);
+    const Fixed fx{base, kNoAllocScratchBytes};
+    Request rq{metric, dtype, P, Q, n_p, n_q, d, threshold, pairs, cap,
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0, true};
+    return run(ctx, rq, n_out, &fx);
 }
 
 void sj_destroy(sj_ctx *c)

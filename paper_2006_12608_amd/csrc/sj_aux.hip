@@ -205,6 +205,21 @@ hipError_t launch_repack(const uint8_t *src, uint32_t n, uint32_t src_bytes, uin
     return hipGetLastError();
 }
 
+// --------------------------------------------------------------------- fill
+// Zeroes n 64-bit words (counters that must start at zero), with a kernel
+// rather than a memset node.
+__global__ void __launch_bounds__(64) zero_u64(unsigned long long *p, uint32_t n)
+{
+    for (uint32_t k = threadIdx.x; k < n; k += 64)
+        p[k] = 0ull;
+}
+
+hipError_t launch_zero_u64(unsigned long long *p, uint32_t n, hipStream_t stream)
+{
+    hipLaunchKernelGGL(zero_u64, dim3(1), dim3(64), 0, stream, p, n);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------- scan
 // Exclusive scan of uint32 block counts into uint64 offsets, in three kernels:
 // per-chunk sums, a scan of the chunk sums by one workgroup (which also writes

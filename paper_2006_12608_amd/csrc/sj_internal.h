@@ -125,6 +125,9 @@ hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_by
 hipError_t launch_repack(const uint8_t *src, uint32_t n, uint32_t src_bytes, uint8_t *dst,
                          uint32_t dst_bytes, hipStream_t stream);
 
+// Zeroes n 64-bit words on `stream` (one small kernel, no memset node).
+hipError_t launch_zero_u64(unsigned long long *p, uint32_t n, hipStream_t stream);
+
 // Exclusive scan of n uint32 counts into n uint64 offsets; *total receives the
 // sum.  `partials` needs scan_partials_size(n) elements of scratch.
 uint64_t scan_partials_size(uint64_t n);
