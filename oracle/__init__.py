@@ -12,6 +12,10 @@ from .oracle import (  # noqa: F401
     max_threads,
     lsh_keys,
     lsh_join,
+    round_to,
+    normalize,
+    hamming,
+    hamming_join,
     JoinResult,
 )
 from . import jl  # noqa: F401,E402

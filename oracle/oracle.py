@@ -61,6 +61,16 @@ def load(path: str | None = None):
     lib.or_lsh_join.restype = i64
     lib.or_max_threads.argtypes = []
     lib.or_max_threads.restype = i32
+    lib.or_round_f16.argtypes = [dbl]
+    lib.or_round_f16.restype = ctypes.c_uint16
+    lib.or_round_bf16.argtypes = [dbl]
+    lib.or_round_bf16.restype = ctypes.c_uint16
+    lib.or_normalize.argtypes = [i32, vp, i64, i64, i32, vp]
+    lib.or_normalize.restype = i32
+    lib.or_hamming.argtypes = [vp, i64, vp, i64, i64]
+    lib.or_hamming.restype = i64
+    lib.or_join_hamming.argtypes = [vp, i64, vp, i64, i64, dbl, vp, i64, i32]
+    lib.or_join_hamming.restype = i64
     if path is None:
         _lib = lib
     return lib
@@ -202,6 +212,65 @@ def lsh_join(metric: str, dtype: str, P: np.ndarray, Q: np.ndarray, thr: float, 
                               int(w), _ptr(out), cap, threads or 0)
         if tot < 0:
             raise RuntimeError(f"oracle lsh_join failed ({tot})")
+        if tot <= cap:
+            return out[:tot].copy()
+        cap = int(tot)
+
+
+# ------------------------------------------- Section 4's ip-distance front ends
+
+def round_to(out_dtype: str, v: float, lib=None) -> int:
+    """The nearest binary16 ("f16") or bfloat16 ("bf16") bit pattern of the
+    double v, ties to even."""
+    lib = lib or load()
+    return int(lib.or_round_f16(float(v)) if out_dtype == "f16" else lib.or_round_bf16(float(v)))
+
+
+def normalize(dtype: str, X: np.ndarray, lib=None) -> np.ndarray:
+    """Every row divided by its Euclidean norm (double, ascending k) and
+    rounded to the nearest value of the output type, ties to even: the
+    storage array of f = g = x / ||x||, Section 4's cosine ip-distance.  The
+    output type is the input's for fp16/bf16 and fp16 for int8; zero rows stay
+    zero."""
+    lib = lib or load()
+    _check(X, X, dtype)
+    out_dtype = "bf16" if dtype == "bf16" else "f16"
+    out = np.zeros(X.shape, np.uint16)
+    st = lib.or_normalize(_DT[dtype], _ptr(X), X.shape[0], X.shape[1], _DT[out_dtype], _ptr(out))
+    if st != 0:
+        raise RuntimeError(f"oracle normalize failed ({st})")
+    return out.view(np.float16) if out_dtype == "f16" else out
+
+
+def _check_bits(X: np.ndarray, d: int):
+    if X.dtype != np.uint8 or X.ndim != 2 or not X.flags.c_contiguous or \
+            X.shape[1] != (d + 7) // 8:
+        raise ValueError(f"expected a C-contiguous (n, {(d + 7) // 8}) uint8 array of bit rows")
+
+
+def hamming(P: np.ndarray, i: int, Q: np.ndarray, j: int, d: int, lib=None) -> int:
+    """Number of the d coordinates in which bit rows P_i and Q_j differ
+    (coordinate m is bit m % 8 of byte m / 8)."""
+    lib = lib or load()
+    _check_bits(P, d)
+    _check_bits(Q, d)
+    return int(lib.or_hamming(_ptr(P), i, _ptr(Q), j, d))
+
+
+def hamming_join(P: np.ndarray, Q: np.ndarray, d: int, r: float, threads: int | None = None,
+                 lib=None) -> np.ndarray:
+    """All (i, j) with Hamming(P_i, Q_j) <= r, as an (m, 2) uint32 array in
+    (i, j) order (rows of d bits, ceil(d / 8) bytes each)."""
+    lib = lib or load()
+    _check_bits(P, d)
+    _check_bits(Q, d)
+    cap = 1 << 16
+    while True:
+        out = np.zeros((cap, 2), np.uint32)
+        tot = lib.or_join_hamming(_ptr(P), P.shape[0], _ptr(Q), Q.shape[0], d, float(r),
+                                  _ptr(out), cap, threads or 0)
+        if tot < 0:
+            raise RuntimeError(f"oracle hamming_join failed ({tot})")
         if tot <= cap:
             return out[:tot].copy()
         cap = int(tot)

@@ -278,6 +278,158 @@ void or_scores(int metric, int dtype, const void *P, const void *Q, int64_t d,
     }
 }
 
+/*
+ * Section 4's ip-distance front ends, written from their definitions.
+ *
+ * Cosine similarity is the inner product of f(x) = g(x) = x / ||x||.
+ * or_normalize writes every row of X (n x d, dtype) divided by its Euclidean
+ * norm and rounded to the nearest value of the output type (binary16 for
+ * out_dtype OR_F16, bfloat16 for OR_BF16), ties to even.  ||x|| is the square
+ * root of the sum of the squares in double, ascending k (every square of a
+ * decoded element is exact in double); each quotient is one double division.
+ * A row whose norm is 0 is written as +0 throughout (its cosine with anything
+ * is taken as 0).
+ */
+
+/* Round |v| (finite, >= 0) to a multiple of 2^scale_exp: the integer nearest
+ * to |v| / 2^scale_exp, ties to the even integer. */
+static double round_half_even_scaled(double a, int scale_exp)
+{
+    double q = ldexp(a, -scale_exp);   /* exact: a power-of-two scaling */
+    double f = floor(q);
+    double diff = q - f;              /* exact: q has few integer bits */
+    if (diff > 0.5 || (diff == 0.5 && fmod(f, 2.0) != 0.0))
+        f += 1.0;
+    return f;
+}
+
+/* Nearest binary16 of v, ties to even: 11-bit significands, normal exponents
+ * -14..15 (spacing 2^(e-10) in [2^e, 2^(e+1))), subnormal spacing 2^-24,
+ * infinity above the largest finite value 65504. */
+static uint16_t round_to_f16(double v)
+{
+    uint16_t sign = signbit(v) ? 0x8000 : 0;
+    double a = fabs(v);
+    if (a == 0.0)
+        return sign;
+    int ex;
+    frexp(a, &ex);
+    int e = ex - 1;                   /* 2^e <= a < 2^(e+1) */
+    if (e > 15)
+        return sign | 0x7c00;
+    if (e < -14) {                    /* subnormal range: spacing 2^-24 */
+        double m = round_half_even_scaled(a, -24);   /* 0 .. 1024 */
+        return sign | (uint16_t)m;    /* 1024 is the smallest normal, 0x0400 */
+    }
+    double m = round_half_even_scaled(a, e - 10);    /* 1024 .. 2048 */
+    /* m = 2048 carries into the exponent; at e = 15 that is 0x7c00, infinity */
+    uint32_t bits = ((uint32_t)(e + 15) << 10) + (uint32_t)m - 1024u;
+    return sign | (uint16_t)bits;
+}
+
+/* Nearest bfloat16 of v, ties to even: 8-bit significands, normal exponents
+ * -126..127 (spacing 2^(e-7)), subnormal spacing 2^-133. */
+static uint16_t round_to_bf16(double v)
+{
+    uint16_t sign = signbit(v) ? 0x8000 : 0;
+    double a = fabs(v);
+    if (a == 0.0)
+        return sign;
+    int ex;
+    frexp(a, &ex);
+    int e = ex - 1;
+    if (e > 127)
+        return sign | 0x7f80;
+    if (e < -126) {
+        double m = round_half_even_scaled(a, -133);  /* 0 .. 128 */
+        return sign | (uint16_t)m;
+    }
+    double m = round_half_even_scaled(a, e - 7);     /* 128 .. 256 */
+    /* m = 256 carries into the exponent; at e = 127 that is 0x7f80, infinity */
+    uint32_t bits = ((uint32_t)(e + 127) << 7) + (uint32_t)m - 128u;
+    return sign | (uint16_t)bits;
+}
+
+/* Exposed for the pins: the rounding of one double to binary16 / bfloat16. */
+uint16_t or_round_f16(double v) { return round_to_f16(v); }
+uint16_t or_round_bf16(double v) { return round_to_bf16(v); }
+
+int or_normalize(int dtype, const void *X, int64_t n, int64_t d, int out_dtype, uint16_t *out)
+{
+    if (n < 0 || d < 0 || (dtype != OR_F16 && dtype != OR_BF16 && dtype != OR_I8) ||
+        (out_dtype != OR_F16 && out_dtype != OR_BF16))
+        return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        double s = 0.0;
+        for (int64_t k = 0; k < d; ++k) {
+            double x = elem(dtype, X, i * d + k);
+            s += x * x;
+        }
+        double norm = sqrt(s);
+        for (int64_t k = 0; k < d; ++k) {
+            if (norm == 0.0) {
+                out[i * d + k] = 0;
+                continue;
+            }
+            double y = elem(dtype, X, i * d + k) / norm;
+            out[i * d + k] = out_dtype == OR_F16 ? round_to_f16(y) : round_to_bf16(y);
+        }
+    }
+    return 0;
+}
+
+/*
+ * Hamming distance (Section 4's example with f(x) = (x, 1 - x), g(y) = (1 - y, y)
+ * on {0, 1}^d): the number of coordinates in which two bit rows differ.  A row
+ * holds d bits, coordinate m in bit m % 8 of byte m / 8, ceil(d / 8) bytes per
+ * row (bits past d are ignored).
+ */
+static int bit_at(const uint8_t *X, int64_t row, int64_t stride, int64_t m)
+{
+    return (X[row * stride + m / 8] >> (m % 8)) & 1;
+}
+
+int64_t or_hamming(const uint8_t *P, int64_t i, const uint8_t *Q, int64_t j, int64_t d)
+{
+    int64_t stride = (d + 7) / 8, h = 0;
+    for (int64_t m = 0; m < d; ++m)
+        h += bit_at(P, i, stride, m) != bit_at(Q, j, stride, m);
+    return h;
+}
+
+/* All (i, j) with Hamming(P_i, Q_j) <= r, lexicographic; at most cap written;
+ * returns the total, -1 on bad arguments, -2 out of memory. */
+int64_t or_join_hamming(const uint8_t *P, int64_t n_p, const uint8_t *Q, int64_t n_q, int64_t d,
+                        double r, uint32_t *out_pairs, int64_t cap, int threads)
+{
+    if (n_p < 0 || n_q < 0 || d < 0)
+        return -1;
+    row_out *ro = (row_out *)calloc((size_t)(n_p ? n_p : 1), sizeof(row_out));
+    if (!ro)
+        return -2;
+    int failed = 0;
+#ifdef _OPENMP
+    int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
+#endif
+    for (int64_t i = 0; i < n_p; ++i)
+        for (int64_t j = 0; j < n_q; ++j)
+            if ((double)or_hamming(P, i, Q, j, d) <= r &&
+                push_u32(&ro[i].pairs, &ro[i].n, &ro[i].cap, (uint32_t)j))
+                failed = 1;
+    int64_t total = 0;
+    for (int64_t i = 0; i < n_p; ++i) {
+        for (int64_t t = 0; t < ro[i].n; ++t, ++total)
+            if (total < cap) {
+                out_pairs[2 * total] = (uint32_t)i;
+                out_pairs[2 * total + 1] = ro[i].pairs[t];
+            }
+        free(ro[i].pairs);
+    }
+    free(ro);
+    return failed ? -2 : total;
+}
+
 /* Threads the OpenMP runtime would use by default (1 without OpenMP). */
 int or_max_threads(void)
 {

@@ -576,4 +576,170 @@ def pin_lsh_quantised_collision_probability(lib):
         assert abs(rate - p) < 0.012, (w, delta_norm2, rate, p)
 
 
+
+# ------------------------------------- Section 4's ip-distance front ends
+
+def _finite_table(dtype):
+    """Every finite nonnegative binary16 / bfloat16 pattern in increasing order,
+    with its exact value (decoded by the pins' own decoder)."""
+    top = 0x7C00 if dtype == "f16" else 0x7F80
+    bits = np.arange(top, dtype=np.uint16)
+    vals = bits.view(np.float16).astype(np.float64) if dtype == "f16" else \
+        values("bf16", bits.reshape(1, -1)).ravel()
+    return bits, vals
+
+
+def _nearest_by_search(dtype, v, bits, vals):
+    """Round-to-nearest-even by its definition: the closest finite value (the
+    two neighbours' distances are exact differences of nearby doubles), ties
+    to the even pattern; beyond the midpoint above the largest finite value,
+    infinity."""
+    a = abs(v)
+    sign = 0x8000 if math.copysign(1.0, v) < 0 else 0
+    inf = 0x7C00 if dtype == "f16" else 0x7F80
+    k = int(np.searchsorted(vals, a))
+    if k < len(vals) and vals[k] == a:
+        return sign | int(bits[k])
+    if k == len(vals):
+        ulp = vals[-1] - vals[-2]
+        mid = vals[-1] + ulp / 2
+        return sign | (inf if a >= mid else int(bits[-1]))
+    lo, hi = k - 1, k
+    dl, dh = a - vals[lo], vals[hi] - a
+    if dl < dh:
+        return sign | int(bits[lo])
+    if dh < dl:
+        return sign | int(bits[hi])
+    return sign | int(bits[lo] if bits[lo] % 2 == 0 else bits[hi])
+
+
+def pin_round_to_nearest_even(lib):
+    """The oracle's double -> binary16 / bfloat16 rounding against a search of
+    all finite patterns: random values in every binade (subnormals included),
+    every kind of exact midpoint (ties), zeros, the overflow threshold;
+    binary16 also against numpy's conversion."""
+    rng = np.random.default_rng(31)
+    for dtype in ("f16", "bf16"):
+        bits, vals = _finite_table(dtype)
+        ks = rng.choice(len(vals) - 1, 2500, replace=False)
+        ks = np.concatenate([ks, np.arange(8), len(vals) - 2 - np.arange(4)])
+        mids = (vals[ks] + vals[ks + 1]) / 2
+        inside = vals[ks] + (vals[ks + 1] - vals[ks]) * rng.random(ks.size)
+        ulp_top = vals[-1] - vals[-2]
+        edge = [0.0, -0.0, vals[-1] + ulp_top / 2, vals[-1] + ulp_top / 2 * (1 - 2 ** -30),
+                vals[-1] * 4, vals[1] / 2, vals[1] / 3]
+        tests = np.concatenate([mids, inside, -mids[:300], -inside[:300], np.array(edge)])
+        for v in tests:
+            want = _nearest_by_search(dtype, float(v), bits, vals)
+            got = oracle.round_to(dtype, float(v), lib=lib)
+            assert got == want, (dtype, float(v), hex(got), hex(want))
+            if dtype == "f16":
+                with np.errstate(over="ignore"):
+                    ref = int(np.float16(v).view(np.uint16))
+                assert got == ref, (float(v), hex(got))
+
+
+def _bits_of(dtype, v):
+    return int(np.float16(v).view(np.uint16)) if dtype == "f16" else \
+        _nearest_by_search("bf16", v, *_finite_table("bf16"))
+
+
+def pin_normalize_exact_cases(lib):
+    """Rows whose normalisation is known exactly: scaled one-hot rows give +-1
+    at the hot coordinate and 0 elsewhere; (3, 4) gives the roundings of 3/5
+    and 4/5, (1, 2, 2) those of 1/3 and 2/3, (2, 3, 6) those of 2/7, 3/7 and
+    6/7 (Pythagorean quadruples: the norm is an integer); a zero row stays zero.
+    Output type: fp16 for fp16 and int8 inputs, bf16 for bf16."""
+    for dtype in DT:
+        out_dt = "bf16" if dtype == "bf16" else "f16"
+        X = np.array([[0, -5, 0, 0, 0, 0, 0], [3, 4, 0, 0, 0, 0, 0], [1, 2, 2, 0, 0, 0, 0],
+                      [0, 0, 0, 0, 0, 0, 0], [-2, 3, -6, 0, 0, 0, 0], [0, 0, 0, 0, 0, 0, 7]])
+        got = oracle.normalize(dtype, encode(X, dtype), lib=lib)
+        got = got.view(np.uint16)
+        want = np.zeros(X.shape, np.uint16)
+        for i, norm in enumerate((5, 5, 3, 0, 7, 7)):
+            for k in range(X.shape[1]):
+                if X[i, k] != 0:
+                    want[i, k] = _bits_of(out_dt, X[i, k] / norm)
+        assert np.array_equal(got, want), (dtype, got, want)
+
+
+def pin_normalize_within_half_ulp(lib):
+    """Random rows of every input type: each normalised value lies within half
+    an output ulp of the exact x_k / ||x|| (exact rational sum of squares,
+    50-digit square root; slack 2^-50 relative for the double norm and
+    quotient), the output is invariant under scaling the row by powers of two
+    and equivariant under permuting its coordinates."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 50
+    rng = np.random.default_rng(32)
+    for dtype in DT:
+        out_dt = "bf16" if dtype == "bf16" else "f16"
+        if dtype == "i8":
+            X = encode(rng.integers(-120, 121, size=(40, 37)), dtype)
+        else:
+            X = encode(rng.standard_normal((40, 37)) * np.exp(rng.uniform(-3, 3, (40, 1))), dtype)
+        x = values(dtype, X)
+        Y = oracle.normalize(dtype, X, lib=lib)
+        y = values(out_dt, Y.view(np.uint16)) if out_dt == "bf16" else Y.astype(np.float64)
+        for i in range(x.shape[0]):
+            S = sum(Fraction(float(t)) ** 2 for t in x[i])
+            norm = Decimal(S.numerator).sqrt() / Decimal(S.denominator).sqrt()
+            for k in range(x.shape[1]):
+                q = Decimal(float(x[i, k])) / norm
+                yk = float(y[i, k])
+                a = abs(yk) if yk != 0 else abs(float(q))
+                e = math.frexp(a)[1] - 1 if a > 0 else -200
+                p = 11 if out_dt == "f16" else 8
+                emin = -14 if out_dt == "f16" else -126
+                ulp = 2.0 ** (max(e, emin) - (p - 1))
+                err = abs(Decimal(yk) - q)
+                assert err <= Decimal(ulp / 2) + abs(q) * Decimal(2.0 ** -50), \
+                    (dtype, i, k, yk, float(q))
+        # scaling by 2 (fp16 / bf16 rows stay exact) and a permutation
+        if dtype != "i8":
+            X2 = encode(x * 2.0, dtype)
+            assert np.array_equal(oracle.normalize(dtype, X2, lib=lib).view(np.uint16),
+                                  Y.view(np.uint16))
+        perm = rng.permutation(x.shape[1])
+        Yp = oracle.normalize(dtype, np.ascontiguousarray(X[:, perm]), lib=lib)
+        # the sum of squares runs in a different order: allow the rare
+        # one-ulp change of the norm, compare within one output ulp
+        a = Y.view(np.uint16)[:, perm].astype(np.int64)
+        b = Yp.view(np.uint16).astype(np.int64)
+        assert np.abs(a - b).max() <= 1
+
+
+def _bitrows(B):
+    """Pack (n, d) 0/1 rows: coordinate m in bit m % 8 of byte m / 8."""
+    return np.packbits(np.asarray(B, dtype=np.uint8), axis=1, bitorder="little")
+
+
+def pin_hamming_join_definition(lib):
+    """The Hamming join: on all of {0,1}^d joined with itself the count within
+    r is 2^d sum_{h <= r} C(d, h); on random rows (with random garbage in the
+    padding bits past d) each distance equals numpy's unpackbits and xor
+    count, and the join equals the squared-L2 join of the unpacked 0/1 rows."""
+    for d in (5, 9):
+        cube = np.array([[(v >> m) & 1 for m in range(d)] for v in range(1 << d)])
+        Bc = _bitrows(cube)
+        for r in (-1, 0, 1, 2.5, d):
+            want = (1 << d) * sum(math.comb(d, h) for h in range(d + 1) if h <= r)
+            assert len(oracle.hamming_join(Bc, Bc.copy(), d, r, lib=lib)) == want, (d, r)
+    rng = np.random.default_rng(33)
+    d = 45
+    bp, bq = rng.integers(0, 2, size=(30, d)), rng.integers(0, 2, size=(26, d))
+    Bp, Bq = _bitrows(bp), _bitrows(bq)
+    Bp[:, -1] |= rng.integers(0, 256, size=30).astype(np.uint8) & 0xE0   # bits 45..47
+    Bq[:, -1] |= rng.integers(0, 256, size=26).astype(np.uint8) & 0xE0
+    up = np.unpackbits(Bp, axis=1, bitorder="little")[:, :d]
+    uq = np.unpackbits(Bq, axis=1, bitorder="little")[:, :d]
+    for i in range(0, 30, 7):
+        for j in range(26):
+            assert oracle.hamming(Bp, i, Bq, j, d, lib=lib) == int((up[i] ^ uq[j]).sum())
+    for r in (5, 18, 22.7):
+        got = oracle.hamming_join(Bp, Bq, d, r, lib=lib)
+        l2 = oracle.join("l2", "i8", encode(bp, "i8"), encode(bq, "i8"), float(r), lib=lib)
+        assert pairset(got) == pairset(l2.pairs) and len(got) == l2.total
+
 PINS = {name[4:]: fn for name, fn in sorted(globals().items()) if name.startswith("pin_")}

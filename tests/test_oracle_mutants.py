@@ -60,6 +60,26 @@ MUTANTS = {
                               "for (int64_t t = 0; t + 1 < L && !collide; ++t)")],
     "lsh_no_exact_test": [("if (matches(metric, sc, thr) &&\n                    push_u32(&ro[i]",
                            "if (push_u32(&ro[i]")],
+    # Section 4's front ends: rounding to binary16 / bfloat16, normalisation,
+    # Hamming distance
+    "round_ties_away": [("if (diff > 0.5 || (diff == 0.5 && fmod(f, 2.0) != 0.0))",
+                         "if (diff >= 0.5)")],
+    "round_truncates": [("        f += 1.0;\n    return f;", "        f += 0.0;\n    return f;")],
+    "f16_round_subnormal_spacing": [("round_half_even_scaled(a, -24)",
+                                     "round_half_even_scaled(a, -25)")],
+    "bf16_round_precision": [("round_half_even_scaled(a, e - 7)",
+                              "round_half_even_scaled(a, e - 8)")],
+    "f16_round_no_infinity": [("    if (e > 15)\n        return sign | 0x7c00;", "")],
+    "normalize_no_sqrt": [("double norm = sqrt(s);", "double norm = s;")],
+    "normalize_drops_last_square": [("        for (int64_t k = 0; k < d; ++k) {\n"
+                                     "            double x = elem(dtype, X, i * d + k);",
+                                     "        for (int64_t k = 0; k + 1 < d; ++k) {\n"
+                                     "            double x = elem(dtype, X, i * d + k);")],
+    "hamming_skips_last_bit": [("    for (int64_t m = 0; m < d; ++m)\n        h += bit_at",
+                                "    for (int64_t m = 0; m + 1 < d; ++m)\n        h += bit_at")],
+    "hamming_strict": [("(double)or_hamming(P, i, Q, j, d) <= r", "(double)or_hamming(P, i, Q, j, d) < r")],
+    "hamming_bit_order": [("return (X[row * stride + m / 8] >> (m % 8)) & 1;",
+                           "return (X[row * stride + m / 8] >> (7 - m % 8)) & 1;")],
 }
 
 
