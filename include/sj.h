@@ -97,7 +97,14 @@ enum sj_flags {
     SJ_FLAG_TIMING = 2u,
     /* With SJ_FLAG_TWO_PASS: always recompute the product in the second pass
      * (no match bits, no scratch beyond the block counts and offsets). */
-    SJ_FLAG_RECOMPUTE = 4u
+    SJ_FLAG_RECOMPUTE = 4u,
+    /* sj_join_ip only: Section 4's cosine ip-distance, f = g = x / ||x||.  P and
+     * Q are first normalised as sj_normalize does (into device memory the
+     * context owns: 2 (n_p + n_q) d bytes, n_q d fewer when P == Q) and the
+     * join is the inner product of the normalised rows, >= s, with the
+     * arithmetic of the fp16 (fp16 and int8 inputs) or bf16 (bf16 inputs)
+     * join. */
+    SJ_FLAG_COSINE = 8u
 };
 
 /* Diagnostics of the last sj_join_ip / sj_join_l2 / sj_count call. */
@@ -147,6 +154,33 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
  * count-then-emit call. */
 int sj_count(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
              uint32_t n_q, uint32_t d, double threshold, uint64_t *count);
+
+/* Section 4's cosine ip-distance front end: Y = every row of X divided by its
+ * Euclidean norm, f(x) = x / ||x||.  X is n x d (dtype, row-major, device);
+ * Y (device, n x d 16-bit values) receives binary16 rows for SJ_F16 and SJ_I8
+ * inputs and bfloat16 rows for SJ_BF16.  ||x|| is the square root of the sum
+ * of the squares of the exactly decoded elements, summed in double in
+ * ascending k; each x_k / ||x|| is one double division, rounded to the
+ * nearest output value, ties to even.  A row whose norm is 0 is written as
+ * zeros.  Device scratch: n doubles.  Errors as sj_join_ip (16-bit rows must
+ * be 2-byte aligned). */
+int sj_normalize(sj_ctx *ctx, int dtype, const void *X, uint32_t n, uint32_t d, void *Y);
+
+/* Section 4's Hamming ip-distance: every (i, j) whose bit rows P_i and Q_j
+ * differ in at most r of their d coordinates.  P (n_p rows) and Q (n_q rows)
+ * are device bit rows of ceil(d / 8) bytes each, coordinate m in bit m % 8 of
+ * byte m / 8 (bits past d are ignored).  As the paper does, the rows are
+ * mapped to f(x) = (x, 1 - x) and g(y) = (1 - y, y) (int8 rows of 2 d values
+ * in device memory the context owns, (n_p + n_q) * 2 d bytes rounded up to 16
+ * per row), so that f(x).g(y) is the Hamming distance, and the pairs come from
+ * the int8 matrix-core join of f(P) with -g(Q) at threshold -r
+ * (f(x).(-g(y)) >= -r).  With P == Q and n_p == n_q the single pass computes
+ * the upper triangle only and mirrors its pairs.  Limits: d <= 16384.
+ * Outputs, flags (SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING, SJ_FLAG_RECOMPUTE) and
+ * errors as sj_join_ip; d = 0 gives every pair when r >= 0. */
+int sj_join_hamming(sj_ctx *ctx, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+                    uint32_t d, double r, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+                    unsigned flags);
 
 /* For callers that cannot allocate device memory during the join (serving
  * loops, harnesses that forbid hipMalloc / hipFree): the join of sj_join_ip
@@ -202,6 +236,35 @@ int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p,
                 uint32_t n_q, uint32_t d, double thr, uint32_t L, uint32_t k, const int8_t *A,
                 const int32_t *B, int32_t w, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
                 uint64_t *n_cand);
+
+/* Collision probability of one function of the LSH families of sj_join_lsh
+ * for two points at distance `dist`: w == 0 (random-hyperplane signs): dist
+ * is the angle between the vectors, in [0, pi], and the probability is
+ * 1 - dist / pi; w > 0 (quantised projections floor((<a, x> + b) / w) with
+ * a ~ N(0, sigma^2 I), b uniform in [0, w)): dist is the Euclidean distance
+ * and the probability is 1 - 2 Phi(-w / u) - 2 u / (sqrt(2 pi) w)
+ * (1 - exp(-w^2 / (2 u^2))) with u = sigma dist.  NaN for arguments outside
+ * these ranges.  Host only. */
+double sj_lsh_collision(int32_t w, double sigma, double dist);
+
+/* Section 4's choice of the LSH join's parameters (host only), for one
+ * function's collision probabilities p1 at the join's threshold distance and
+ * p2 at a far distance (0 < p2 < p1 < 1), n points per side and the matrix
+ * cores' tile edge `tile` standing for the paper's sqrt(m) (a TCU(m, tau)
+ * with tau = m, so that Section 4's p2 = m^(3/2) / (tau n) is tile / n):
+ *   *k      = the least k with p2^k <= tile / n (each point meets at most one
+ *             tile of far points per table in expectation; 0 when n <= tile),
+ *   *L_inst = ceil(1 / p1^k) tables: one instance finds a pair at the
+ *             threshold with probability 1 - (1 - p1^k)^L_inst >= 1 - 1/e,
+ *   *reps   = ceil(ln(1 / (1 - recall))) independent instances, merged, find
+ *             it with probability >= 1 - e^-reps >= recall (Section 4's
+ *             O(log n) instances for a high-probability guarantee).
+ * sj_join_lsh with L = L_inst * reps tables (independent draws) and k runs the
+ * merged instances in one call: its first-table rule reports every pair that
+ * collides in any table once.  Returns SJ_E_INVAL for arguments out of range,
+ * SJ_E_UNSUPPORTED when k would exceed 64. */
+int sj_lsh_plan(double p1, double p2, uint64_t n, uint32_t tile, double recall, uint32_t *k,
+                uint32_t *L_inst, uint32_t *reps);
 
 /* TCU Johnson-Lindenstrauss transform (Lemma 3 / Theorem 2): the reduced
  * rows Y_j = M X_j of the n rows of X (n x d, row-major, dtype as the joins,

@@ -2,8 +2,9 @@
 Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
 
 The raw C-ABI entry points are exposed under their C names (sj_create,
-sj_join_ip, sj_join_l2, sj_count, sj_join_noalloc, sj_join_lsh, sj_jl,
-sj_destroy, sj_get_stats, sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
+sj_join_ip, sj_join_l2, sj_count, sj_join_noalloc, sj_normalize,
+sj_join_hamming, sj_join_lsh, sj_lsh_collision, sj_lsh_plan, sj_jl, sj_destroy,
+sj_get_stats, sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
 `join_lsh` (the LSH-bucketed join of Theorem 3) are conveniences over PyTorch
 device tensors.  This module only marshals
 arguments: every step of the join runs in the library's HIP kernels.  Import
@@ -20,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libsj.so")
 SJ_F16, SJ_BF16, SJ_I8 = 1, 2, 3
 SJ_IP, SJ_L2 = 0, 1
 SJ_OK, SJ_E_INVAL, SJ_E_OVERFLOW, SJ_E_NOMEM, SJ_E_HIP, SJ_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING, SJ_FLAG_RECOMPUTE = 1, 2, 4
+SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING, SJ_FLAG_RECOMPUTE, SJ_FLAG_COSINE = 1, 2, 4, 8
 
 STATUS_NAMES = {0: "SJ_OK", -1: "SJ_E_INVAL", -2: "SJ_E_OVERFLOW", -3: "SJ_E_NOMEM",
                 -4: "SJ_E_HIP", -5: "SJ_E_UNSUPPORTED"}
@@ -60,10 +61,20 @@ def _load():
     lib.sj_join_noalloc.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, vp, u64,
                                     ctypes.POINTER(u64), ctypes.c_uint]
     lib.sj_join_noalloc.restype = i32
+    lib.sj_normalize.argtypes = [vp, i32, vp, u32, u32, vp]
+    lib.sj_normalize.restype = i32
+    lib.sj_join_hamming.argtypes = [vp, vp, u32, vp, u32, u32, dbl, vp, u64,
+                                    ctypes.POINTER(u64), ctypes.c_uint]
+    lib.sj_join_hamming.restype = i32
     lib.sj_join_lsh.argtypes = [vp, i32, i32, vp, u32, vp, u32, u32, dbl, u32, u32, vp, vp,
                                 ctypes.c_int32, vp, u64, ctypes.POINTER(u64),
                                 ctypes.POINTER(u64)]
     lib.sj_join_lsh.restype = i32
+    lib.sj_lsh_collision.argtypes = [ctypes.c_int32, dbl, dbl]
+    lib.sj_lsh_collision.restype = dbl
+    lib.sj_lsh_plan.argtypes = [dbl, dbl, u64, u32, dbl, ctypes.POINTER(u32), ctypes.POINTER(u32),
+                                ctypes.POINTER(u32)]
+    lib.sj_lsh_plan.restype = i32
     lib.sj_jl.argtypes = [vp, i32, vp, u32, u32, u32, vp, vp, vp]
     lib.sj_jl.restype = i32
     lib.sj_destroy.argtypes = [vp]
@@ -122,6 +133,19 @@ def sj_join_noalloc(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, pairs, cap, flag
     return st, n.value
 
 
+def sj_normalize(ctx, dtype, X, n, d, Y):
+    """Returns the status; pointers are integers (device addresses)."""
+    return lib.sj_normalize(ctx, dtype, X, n, d, Y)
+
+
+def sj_join_hamming(ctx, P, n_p, Q, n_q, d, r, pairs, cap, flags=0):
+    """Returns (status, n_out); P and Q are device bit rows (ceil(d / 8) bytes)."""
+    n = ctypes.c_uint64(0)
+    st = lib.sj_join_hamming(ctx, P, n_p, Q, n_q, d, float(r), pairs, cap, ctypes.byref(n),
+                             flags)
+    return st, n.value
+
+
 def sj_count(ctx, metric, dtype, P, n_p, Q, n_q, d, threshold):
     """Returns (status, count)."""
     n = ctypes.c_uint64(0)
@@ -136,6 +160,18 @@ def sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, L, k, A, B, w, pairs
     st = lib.sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, float(thr), L, k, A, B, int(w),
                          pairs, cap, ctypes.byref(n), ctypes.byref(nc))
     return st, n.value, nc.value
+
+
+def sj_lsh_collision(w: int, sigma: float, dist: float) -> float:
+    return lib.sj_lsh_collision(int(w), float(sigma), float(dist))
+
+
+def sj_lsh_plan(p1: float, p2: float, n: int, tile: int, recall: float):
+    """Returns (status, k, L_inst, reps)."""
+    k, L, r = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    st = lib.sj_lsh_plan(float(p1), float(p2), int(n), int(tile), float(recall), ctypes.byref(k),
+                         ctypes.byref(L), ctypes.byref(r))
+    return st, k.value, L.value, r.value
 
 
 def sj_jl(ctx, dtype, X, n, d, levels, shape, A, Y):
@@ -204,7 +240,28 @@ def count(P, Q, threshold: float, metric: str = "ip", ctx=None) -> int:
     return n
 
 
-def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
+def _sized_call(call, flags, cap, out, device):
+    """Runs call(pairs_ptr, cap, flags) -> (status, n); with neither a
+    capacity nor an output buffer, a first count-then-emit call with no room
+    sizes the output (it stops after the count) and a second one fills it."""
+    import torch
+    if cap is None and out is None:
+        st, n = call(None, 0, flags | SJ_FLAG_TWO_PASS)
+        if st not in (SJ_OK, SJ_E_OVERFLOW):
+            raise SjError(st, sj_last_error(), n)
+        cap = n
+    if out is None:
+        out = torch.empty((max(int(cap), 1), 2), dtype=torch.int32, device=device)
+        cap = int(cap)
+    else:
+        cap = out.shape[0] if cap is None else int(cap)
+    st, n = call(out.data_ptr() if cap else None, cap, flags)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error(), n)
+    return out[:n]
+
+
+def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False, cosine=False):
     import torch
     _check_pair(P, Q)
     ctx = ctx or context(P.device.index)
@@ -212,7 +269,12 @@ def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
         # no capacity given: count-then-emit sizes the output exactly
         two_pass = cap is None and out is None
     flags = ((SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
-             | (SJ_FLAG_RECOMPUTE if recompute else 0))
+             | (SJ_FLAG_RECOMPUTE if recompute else 0) | (SJ_FLAG_COSINE if cosine else 0))
+    if cosine:
+        def call(ptr, c, f):
+            return sj_join_ip(ctx, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(),
+                              Q.shape[0], P.shape[1], thr, ptr, c, f)
+        return _sized_call(call, flags, cap, out, P.device)
     if cap is None and out is None:
         cap = count(P, Q, thr, metric, ctx)
     if out is None:
@@ -229,20 +291,61 @@ def _join(metric, P, Q, thr, cap, two_pass, timing, ctx, out, recompute=False):
 
 
 def join_ip(P, Q, s: float, cap: int | None = None, two_pass: bool | None = None,
-            timing: bool = False, ctx=None, out=None, recompute: bool = False):
+            timing: bool = False, ctx=None, out=None, recompute: bool = False,
+            cosine: bool = False):
     """All (i, j) with <P_i, Q_j> >= s as an (n, 2) int32 tensor of uint32
     indices.  With cap=None (and no `out`) the output is sized by sj_count and
     filled by count-then-emit (deterministic order) unless two_pass=False asks
     for the single pass; with a capacity the single pass runs unless
     two_pass=True.  recompute makes the second pass of count-then-emit repeat
-    the product even where the first pass's match bits would be kept."""
-    return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out, recompute)
+    the product even where the first pass's match bits would be kept.
+    cosine=True normalises the rows in the library first (SJ_FLAG_COSINE)."""
+    return _join("ip", P, Q, s, cap, two_pass, timing, ctx, out, recompute, cosine)
 
 
 def join_l2(P, Q, r2: float, cap: int | None = None, two_pass: bool | None = None,
             timing: bool = False, ctx=None, out=None, recompute: bool = False):
     """All (i, j) with ||P_i - Q_j||^2 <= r2 (see join_ip)."""
     return _join("l2", P, Q, r2, cap, two_pass, timing, ctx, out, recompute)
+
+
+def normalize(X, ctx=None):
+    """Section 4's cosine front end (sj_normalize): the rows of X (float16,
+    bfloat16 or int8 device tensor) divided by their norms, rounded to
+    float16 (bfloat16 for bfloat16 input)."""
+    import torch
+    if X.dim() != 2 or not X.is_cuda or not X.is_contiguous():
+        raise ValueError("X must be a contiguous 2-D device tensor")
+    ctx = ctx or context(X.device.index)
+    Y = torch.empty(X.shape, dtype=torch.bfloat16 if X.dtype == torch.bfloat16 else torch.float16,
+                    device=X.device)
+    st = sj_normalize(ctx, dtype_code(X), X.data_ptr(), X.shape[0], X.shape[1], Y.data_ptr())
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return Y
+
+
+def join_hamming(P, Q, d: int, r: float, cap: int | None = None, two_pass: bool | None = None,
+                 timing: bool = False, ctx=None, out=None):
+    """Section 4's Hamming join (sj_join_hamming): all (i, j) whose d-bit rows
+    differ in at most r coordinates.  P and Q are (n, ceil(d / 8)) uint8
+    device tensors of bit rows (coordinate m in bit m % 8 of byte m / 8).
+    Sizing and modes as join_ip."""
+    import torch
+    for X in (P, Q):
+        if X.dtype != torch.uint8 or X.dim() != 2 or X.shape[1] != (d + 7) // 8 or \
+                not X.is_cuda or not X.is_contiguous():
+            raise ValueError(f"bit rows must be contiguous (n, {(d + 7) // 8}) uint8 device "
+                             "tensors")
+    ctx = ctx or context(P.device.index)
+    if two_pass is None:
+        two_pass = cap is None and out is None
+    flags = (SJ_FLAG_TWO_PASS if two_pass else 0) | (SJ_FLAG_TIMING if timing else 0)
+
+    def call(ptr, c, f):
+        return sj_join_hamming(ctx, P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0], d, r,
+                               ptr, c, f)
+    return _sized_call(call, flags, cap, out, P.device)
 
 
 def join_lsh(P, Q, thr: float, metric: str = "ip", *, L: int, k: int, A, B=None, w: int = 0,

@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["sj_api.cpp", "sj_aux.hip", "sj_join_f16.hip", "sj_join_bf16.hip", "sj_join_i8.hip",
-           "sj_lsh_api.cpp", "sj_lsh.hip", "sj_jl_api.cpp", "sj_jl.hip"]
+           "sj_lsh_api.cpp", "sj_lsh.hip", "sj_jl_api.cpp", "sj_jl.hip", "sj_front.hip", "sj_sort.hip"]
 PEAK_SOURCE = os.path.join("peak", "mfma_peak.hip")
 PEAK_OUT = os.path.join(HERE, "libsj_peak.so")
 # Packed-fp32 instructions are kept out of the generated code (they are not

@@ -128,6 +128,26 @@ int grow_scratch(sj_ctx *c, size_t bytes)
     return SJ_OK;
 }
 
+int grow_front(sj_ctx *c, size_t bytes)
+{
+    if (bytes <= c->front_bytes)
+        return SJ_OK;
+    if (c->front) {
+        (void)hipStreamSynchronize(c->stream);
+        (void)hipFree(c->front);
+        c->front = nullptr;
+        c->front_bytes = 0;
+    }
+    if (hipMalloc(&c->front, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        c->front = nullptr;
+        return fail(SJ_E_NOMEM, "cannot allocate %zu bytes of device memory for the rows of "
+                    "the front end", bytes);
+    }
+    c->front_bytes = bytes;
+    return SJ_OK;
+}
+
 double elapsed_ms(hipEvent_t a, hipEvent_t b)
 {
     float ms = 0.f;
@@ -152,6 +172,10 @@ struct Request {
     uint32_t *pairs;
     uint64_t cap;
     bool two_pass, count_only, timing, recompute;
+    // the score matrix is symmetric although P and Q are different buffers
+    // (the Hamming front end's f(x) and -g(x)): a single pass computes the
+    // upper triangle only and mirrors its pairs, as for P == Q
+    bool symmetric = false;
 };
 
 // Largest match-bit buffer the two-pass mode keeps (bytes); beyond it, or
@@ -389,8 +413,9 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out, const Fixed *fx = nullptr
     bool emit_from_bits = false;
     if (!blocks) {
         // a self-join computes the upper triangle only and mirrors its pairs
-        const int mode = self && plan.family == sjk::FAM_RESIDENT ? sjk::MODE_TRI
-                                                                  : sjk::MODE_SINGLE;
+        const bool tri = (self || rq.symmetric) && rq.n_p == rq.n_q;
+        const int mode = tri && plan.family == sjk::FAM_RESIDENT ? sjk::MODE_TRI
+                                                                 : sjk::MODE_SINGLE;
         SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, mode, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));
@@ -454,6 +479,51 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out, const Fixed *fx = nullptr
     return SJ_OK;
 }
 
+// Section 4's cosine ip-distance: P and Q normalised (f = g = x / ||x||) into
+// the front-end buffer, then the inner-product join of the normalised rows.
+int cosine_join(sj_ctx *c, Request rq, uint64_t *n_out)
+{
+    if (!c)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (!n_out)
+        return fail(SJ_E_INVAL, "result pointer is NULL");
+    *n_out = 0;
+    if (rq.dtype != SJ_F16 && rq.dtype != SJ_BF16 && rq.dtype != SJ_I8)
+        return fail(SJ_E_INVAL, "unknown dtype %d", rq.dtype);
+    if (rq.d > 65536)
+        return fail(SJ_E_UNSUPPORTED, "d = %u is above the limit", rq.d);
+    const size_t es = esize(rq.dtype);
+    int st;
+    if ((st = check_device_ptr(c, rq.P, (size_t)rq.n_p * rq.d * es, "P")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(c, rq.Q, (size_t)rq.n_q * rq.d * es, "Q")) != SJ_OK)
+        return st;
+    if (es == 2 && (((uintptr_t)rq.P | (uintptr_t)rq.Q) & 1))
+        return fail(SJ_E_INVAL, "fp16 / bf16 rows must be 2-byte aligned");
+    if (rq.n_p == 0 || rq.n_q == 0 || rq.d == 0) {
+        // nothing to normalise: the join's own handling of empty inputs and
+        // of d = 0 (every score 0) applies
+        rq.dtype = rq.dtype == SJ_BF16 ? SJ_BF16 : SJ_F16;
+        return run(c, rq, n_out);
+    }
+    const bool self = rq.P == rq.Q && rq.n_p == rq.n_q;
+    const size_t bp = align_up((size_t)rq.n_p * rq.d * 2);
+    const size_t bq = self ? 0 : align_up((size_t)rq.n_q * rq.d * 2);
+    const size_t bn = (size_t)(rq.n_p > rq.n_q ? rq.n_p : rq.n_q) * sizeof(double);
+    if ((st = grow_front(c, bp + bq + bn)) != SJ_OK)
+        return st;
+    uint8_t *f = (uint8_t *)c->front;
+    double *norm = (double *)(f + bp + bq);
+    SJ_HIP(hipSetDevice(c->device));
+    SJ_HIP(sjk::launch_normalize(rq.dtype, rq.P, rq.n_p, rq.d, norm, f, c->stream));
+    if (!self)
+        SJ_HIP(sjk::launch_normalize(rq.dtype, rq.Q, rq.n_q, rq.d, norm, f + bp, c->stream));
+    rq.P = f;
+    rq.Q = self ? f : f + bp;
+    rq.dtype = rq.dtype == SJ_BF16 ? SJ_BF16 : SJ_F16;
+    return run(c, rq, n_out);
+}
+
 }  // namespace
 
 extern "C" {
@@ -513,6 +583,79 @@ int sj_join_ip(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
     Request rq{SJ_IP, dtype, P, Q, n_p, n_q, d, s, pairs, cap,
                (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
                (flags & SJ_FLAG_RECOMPUTE) != 0};
+    if (flags & SJ_FLAG_COSINE)
+        return cosine_join(ctx, rq, n_out);
+    return run(ctx, rq, n_out);
+}
+
+int sj_normalize(sj_ctx *ctx, int dtype, const void *X, uint32_t n, uint32_t d, void *Y)
+{
+    g_err.clear();
+    if (!ctx)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (dtype != SJ_F16 && dtype != SJ_BF16 && dtype != SJ_I8)
+        return fail(SJ_E_INVAL, "unknown dtype %d", dtype);
+    if (d > 65536)
+        return fail(SJ_E_UNSUPPORTED, "d = %u is above the limit", d);
+    const size_t es = esize(dtype);
+    int st;
+    if ((st = check_device_ptr(ctx, X, (size_t)n * d * es, "X")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(ctx, Y, (size_t)n * d * 2, "Y")) != SJ_OK)
+        return st;
+    if (((uintptr_t)Y & 1) || (es == 2 && ((uintptr_t)X & 1)))
+        return fail(SJ_E_INVAL, "16-bit rows must be 2-byte aligned");
+    ctx->stats = sj_stats{};
+    if (n == 0 || d == 0)
+        return SJ_OK;
+    if ((st = grow_scratch(ctx, (size_t)n * sizeof(double))) != SJ_OK)
+        return st;
+    SJ_HIP(hipSetDevice(ctx->device));
+    SJ_HIP(sjk::launch_normalize(dtype, X, n, d, (double *)ctx->scratch, Y, ctx->stream));
+    SJ_HIP(hipStreamSynchronize(ctx->stream));
+    return SJ_OK;
+}
+
+int sj_join_hamming(sj_ctx *ctx, const void *P, uint32_t n_p, const void *Q, uint32_t n_q,
+                    uint32_t d, double r, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
+                    unsigned flags)
+{
+    g_err.clear();
+    if (!ctx)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (!n_out)
+        return fail(SJ_E_INVAL, "result pointer is NULL");
+    *n_out = 0;
+    if (std::isnan(r))
+        return fail(SJ_E_INVAL, "radius is NaN");
+    if (flags & ~(unsigned)(SJ_FLAG_TWO_PASS | SJ_FLAG_TIMING | SJ_FLAG_RECOMPUTE))
+        return fail(SJ_E_INVAL, "unknown flags 0x%x", flags);
+    if (d > 16384)
+        return fail(SJ_E_UNSUPPORTED, "d = %u bits is above the limit of 16384", d);
+    const size_t in_row = (d + 7) / 8;
+    int st;
+    if ((st = check_device_ptr(ctx, P, (size_t)n_p * in_row, "P")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(ctx, Q, (size_t)n_q * in_row, "Q")) != SJ_OK)
+        return st;
+    Request rq{SJ_IP, SJ_I8, P, Q, n_p, n_q, 0, -r, pairs, cap,
+               (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
+               (flags & SJ_FLAG_RECOMPUTE) != 0};
+    if (n_p == 0 || n_q == 0 || d == 0)
+        return run(ctx, rq, n_out);   // no pairs, or every distance 0 (d = 0)
+    // f(x) and -g(y) as int8 rows of 2 d values, padded with zeros to 16 bytes
+    const uint32_t rb = (uint32_t)((2 * (size_t)d + 15) & ~(size_t)15);
+    const size_t bp = align_up((size_t)n_p * rb), bq = align_up((size_t)n_q * rb);
+    if ((st = grow_front(ctx, bp + bq)) != SJ_OK)
+        return st;
+    uint8_t *f = (uint8_t *)ctx->front;
+    SJ_HIP(hipSetDevice(ctx->device));
+    SJ_HIP(sjk::launch_unpack_hamming((const uint8_t *)P, n_p, d, rb, 0, f, ctx->stream));
+    SJ_HIP(sjk::launch_unpack_hamming((const uint8_t *)Q, n_q, d, rb, 1, f + bp, ctx->stream));
+    rq.P = f;
+    rq.Q = f + bp;
+    rq.d = rb;
+    rq.symmetric = P == Q && n_p == n_q;
     return run(ctx, rq, n_out);
 }
 
@@ -570,6 +713,8 @@ void sj_destroy(sj_ctx *c)
             (void)hipEventDestroy(ev);
     if (c->scratch)
         (void)hipFree(c->scratch);
+    if (c->front)
+        (void)hipFree(c->front);
     if (c->d_small)
         (void)hipFree(c->d_small);
     if (c->h_small)

@@ -20,6 +20,8 @@ struct sj_ctx {
     unsigned long long *h_small = nullptr;  // pinned host copy of d_small
     void *scratch = nullptr;
     size_t scratch_bytes = 0;
+    void *front = nullptr;        // rows made by the front ends (normalised or
+    size_t front_bytes = 0;       // unpacked), kept apart from the join's scratch
     hipEvent_t ev[6] = {};
     sj_stats stats = {};
 };
@@ -53,6 +55,9 @@ float float_at_or_below(double r);
 
 // Grows the context's scratch to at least `bytes` (contents not kept).
 int grow_scratch(sj_ctx *c, size_t bytes);
+
+// Grows the context's front-end buffer to at least `bytes` (contents not kept).
+int grow_front(sj_ctx *c, size_t bytes);
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 

@@ -125,6 +125,20 @@ hipError_t launch_norms(int dtype, const uint8_t *X, uint32_t n, uint32_t row_by
 hipError_t launch_repack(const uint8_t *src, uint32_t n, uint32_t src_bytes, uint8_t *dst,
                          uint32_t dst_bytes, hipStream_t stream);
 
+// Section 4's cosine front end: Y (n x d, 16-bit) = every row of X (n x d of
+// dtype, row-major) divided by its Euclidean norm (double, ascending k) and
+// rounded to the nearest binary16 (fp16 and int8 inputs) or bfloat16 (bf16
+// inputs), ties to even; zero rows give zeros.  `norm` is n doubles of scratch.
+hipError_t launch_normalize(int dtype, const void *X, uint32_t n, uint32_t d, double *norm,
+                            void *Y, hipStream_t stream);
+
+// Section 4's Hamming front end: bit rows (ceil(d / 8) bytes, coordinate m in
+// bit m % 8 of byte m / 8) to int8 rows of out_bytes bytes (a multiple of 16,
+// at least 2 d): side 0 writes f(x) = (x, 1 - x), side 1 writes -g(y) =
+// (y - 1, -y), zero past 2 d; <f(x), -g(y)> = -Hamming(x, y).
+hipError_t launch_unpack_hamming(const uint8_t *bits, uint32_t n, uint32_t d, uint32_t out_bytes,
+                                 int side, uint8_t *out, hipStream_t stream);
+
 // Zeroes n 64-bit words on `stream` (one small kernel, no memset node).
 hipError_t launch_zero_u64(unsigned long long *p, uint32_t n, hipStream_t stream);
 

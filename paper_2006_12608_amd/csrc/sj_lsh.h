@@ -18,19 +18,16 @@ struct Rows {
 // Sign hashes (w == 0) are stored compressed, bit u = v_{t k + u}; quantised
 // hashes (w > 0) as the concatenation of their values' low floor(64 / k) bits.
 // Either way two rows share a bucket of table t exactly when their keys are
-// equal.  key_bits(k, w) is the number of low bits a key can occupy; with
-// tshift > 0 the key also carries t << tshift (tshift = key_bits, when
-// key_bits + table_bits(L) <= 64, so that one sort orders every table).
+// equal.  key_bits(k, w) is the number of low bits a key can occupy.
 // The projection entries come widened by launch_widen (widened_bytes(...)
 // bytes: int32 for int8 rows, double otherwise; each row padded with zeros
 // to a whole number of 16-byte chunks of the input rows).
 uint32_t key_bits(uint32_t k, int32_t w);
-uint32_t table_bits(uint32_t L);
 size_t widened_bytes(int dtype, uint32_t L, uint32_t k, uint32_t d);
 hipError_t launch_widen(int dtype, const int8_t *A, uint32_t n_fn, uint32_t d, void *out,
                         hipStream_t s);
 hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                       const void *Aw, const int32_t *B, int32_t w, uint32_t tshift,
+                       const void *Aw, const int32_t *B, int32_t w,
                        uint64_t *keys, hipStream_t s);
 
 // The same keys with the projections on the matrix cores (rows of at most
@@ -43,24 +40,17 @@ hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_
 bool keys_fast_applies(int dtype, uint32_t row_bytes, uint32_t L, uint32_t k, int32_t w);
 size_t keys_fast_bytes(uint32_t n_max, uint32_t L, uint32_t k, uint32_t row_bytes);
 hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
-                            uint32_t tshift, uint64_t *keys, void *ws, bool widen,
+                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w, uint64_t *keys, void *ws, bool widen,
                             unsigned long long *nfix, hipStream_t s);
 
 // Sorts each table's keys with the row indices as values (n rows per table):
 // sorted[t * n + p], perm[t * n + p] = the p-th smallest key of table t and its
-// row.  joint: the keys carry their table above `bits` and one sort of all
-// L n entries does it (`iota` holds L n entries; `temp` must hold
-// sort_temp_bytes(L n, bits + table_bits(L)) bytes); otherwise all entries
-// are sorted by key and then stably by table (`temp`:
-// sort_temp_bytes_split(L n, bits, table_bits(L)) bytes, `work`:
-// split_work_bytes(L n) bytes).
-size_t sort_temp_bytes(uint32_t n, uint32_t bits);
-size_t sort_temp_bytes_split(uint32_t total, uint32_t bits, uint32_t tbits);
-size_t split_work_bytes(uint32_t total);
-hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
-                       uint32_t n, uint32_t L, uint32_t bits, bool joint, void *temp,
-                       size_t temp_bytes, void *work, hipStream_t s);
+// row, rows of equal keys in increasing order (a stable radix sort over the
+// keys' low `bits` bits, tables as segments; sj_sort.hip).  `temp` must hold
+// sort_temp_bytes(n, L) bytes; `keys` is not modified.
+size_t sort_temp_bytes(uint32_t n, uint32_t L);
+hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t n,
+                       uint32_t L, uint32_t bits, void *temp, hipStream_t s);
 
 // Tile edge of the bucket join (rows of P and of Q per workgroup tile).
 constexpr uint32_t TILE = 128;

@@ -11,7 +11,6 @@
 // same fused threshold test and wave-ballot compaction as the all-pairs join.
 #include "sj_lsh.h"
 
-#include <hipcub/hipcub.hpp>
 
 #include "sj_internal.h"
 #include "sj_join_kernels.h"
@@ -144,14 +143,13 @@ __device__ __forceinline__ void fold_value(uint64_t &key, T z, uint32_t u, uint3
 // computes the keys of its row; wave v takes the tables v, v + 4, ...  Per
 // table: z_f = sum_m A[f][m] x_m in ascending m (exact products; for
 // fp16/bf16 a double sum in that order, for int8 an exact int32 sum), then the
-// function values and the key (see launch_keys); `tshift` > 0 also places the
-// table number above the key's bits (one sort for all tables).  Rows of at
+// function values and the key (see launch_keys).  Rows of at
 // most KSEG bytes are staged once for every table; longer rows once per table
 // and segment, with the partial sums kept for at most 16 functions per pass.
 template <int DT, bool LONG>
 __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t L, uint32_t k,
                                                    const typename Chunk<DT>::a_t *A,
-                                                   const int32_t *B, int32_t w, uint32_t tshift,
+                                                   const int32_t *B, int32_t w,
                                                    uint64_t *keys)
 {
     typedef Chunk<DT> C;
@@ -184,7 +182,7 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
         __syncthreads();
         const uint32_t nch = rb / 16;
         for (uint32_t t = wave; t < L; t += 4) {
-            uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
+            uint64_t key = 0ull;
             uint32_t u = 0;
             for (; u + 4 <= k; u += 4) {
                 acc_t z[4] = {};
@@ -216,7 +214,7 @@ __global__ void __launch_bounds__(256) keys_kernel(Rows r, uint32_t d, uint32_t 
     const uint32_t tl = (L + 3) / 4 * 4;
     for (uint32_t t0 = 0; t0 < tl; t0 += 4) {
         const uint32_t t = t0 + wave;
-        uint64_t key = tshift ? (uint64_t)t << tshift : 0ull;
+        uint64_t key = 0ull;
         for (uint32_t u = 0; u < k; u += 16) {
             acc_t z[16] = {};
             for (uint32_t seg0 = 0; seg0 < rb; seg0 += KSEG) {
@@ -333,7 +331,7 @@ __global__ void xnorm_kernel(Rows r, uint32_t d, float *out)
 template <int DT, int KS>
 __global__ void __launch_bounds__(256) keys_mfma_kernel(
     Rows r, uint32_t L, uint32_t k, const uint8_t *Ah, const float *anorm, const float *xnorm,
-    const int32_t *B, int32_t w, uint32_t tshift, float gam, uint64_t *keys, uint4 *fix,
+    const int32_t *B, int32_t w, float gam, uint64_t *keys, uint4 *fix,
     unsigned long long *nfix)
 {
     typedef sjk::Mma<DT> M;
@@ -441,7 +439,7 @@ __global__ void __launch_bounds__(256) keys_mfma_kernel(
             const uint32_t Rl = i / L, t = i - Rl * L;
             const uint32_t R = row0 + Rl;
             if (R < r.n) {
-                keys[(size_t)t * r.n + R] = kk[i] | (tshift ? (uint64_t)t << tshift : 0ull);
+                keys[(size_t)t * r.n + R] = kk[i];
                 q = umask(Rl, t) != 0;
             }
         }
@@ -511,14 +509,6 @@ __global__ void __launch_bounds__(256) fix_kernel(Rows r, uint32_t d, uint32_t k
         }
         keys[(size_t)t * r.n + row] |= key;
     }
-}
-
-// v[i] = i mod n for i < total (the row of entry i of table-major arrays).
-__global__ void iota_kernel(uint32_t *v, uint32_t n, uint32_t total)
-{
-    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < total)
-        v[i] = i % n;
 }
 
 // ------------------------------------------------------------ bucket pairs
@@ -802,17 +792,17 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
 
 template <int DT>
 hipError_t launch_keys_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k, const void *Aw,
-                         const int32_t *B, int32_t w, uint32_t tshift, uint64_t *keys,
+                         const int32_t *B, int32_t w, uint64_t *keys,
                          hipStream_t s)
 {
     const dim3 grid((r.n + KROWS - 1) / KROWS);
     const uint32_t rb = padded_d<DT>(d) * (DT == DT_I8 ? 1 : 2);
     if (rb <= KSEG)
         hipLaunchKernelGGL((keys_kernel<DT, false>), grid, dim3(256), 0, s, r, d, L, k,
-                           (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, keys);
+                           (const typename Chunk<DT>::a_t *)Aw, B, w, keys);
     else
         hipLaunchKernelGGL((keys_kernel<DT, true>), grid, dim3(256), 0, s, r, d, L, k,
-                           (const typename Chunk<DT>::a_t *)Aw, B, w, tshift, keys);
+                           (const typename Chunk<DT>::a_t *)Aw, B, w, keys);
     return hipGetLastError();
 }
 
@@ -837,14 +827,6 @@ uint32_t key_bits(uint32_t k, int32_t w)
     return b > 64 ? 64 : b;
 }
 
-uint32_t table_bits(uint32_t L)
-{
-    uint32_t b = 0;
-    while ((1u << b) < L)
-        ++b;
-    return b;
-}
-
 size_t widened_bytes(int dtype, uint32_t L, uint32_t k, uint32_t d)
 {
     return dtype == DT_I8 ? (size_t)L * k * padded_d<DT_I8>(d) * 4
@@ -852,18 +834,18 @@ size_t widened_bytes(int dtype, uint32_t L, uint32_t k, uint32_t d)
 }
 
 hipError_t launch_keys(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                       const void *Aw, const int32_t *B, int32_t w, uint32_t tshift,
+                       const void *Aw, const int32_t *B, int32_t w,
                        uint64_t *keys, hipStream_t s)
 {
     if (r.n == 0 || L == 0)
         return hipSuccess;
     switch (dtype) {
     case DT_F16:
-        return launch_keys_t<DT_F16>(r, d, L, k, Aw, B, w, tshift, keys, s);
+        return launch_keys_t<DT_F16>(r, d, L, k, Aw, B, w, keys, s);
     case DT_BF16:
-        return launch_keys_t<DT_BF16>(r, d, L, k, Aw, B, w, tshift, keys, s);
+        return launch_keys_t<DT_BF16>(r, d, L, k, Aw, B, w, keys, s);
     default:
-        return launch_keys_t<DT_I8>(r, d, L, k, Aw, B, w, tshift, keys, s);
+        return launch_keys_t<DT_I8>(r, d, L, k, Aw, B, w, keys, s);
     }
 }
 
@@ -882,18 +864,16 @@ size_t keys_fast_bytes(uint32_t n_max, uint32_t L, uint32_t k, uint32_t row_byte
 
 template <int DT, int KS>
 static void launch_mfma_t(const Rows &r, uint32_t L, uint32_t k, const uint8_t *Ah,
-                          const float *an, const float *xn, const int32_t *B, int32_t w,
-                          uint32_t tshift, float gam, uint64_t *keys, uint4 *fix,
+                          const float *an, const float *xn, const int32_t *B, int32_t w, float gam, uint64_t *keys, uint4 *fix,
                           unsigned long long *nfix, hipStream_t s)
 {
     hipLaunchKernelGGL((keys_mfma_kernel<DT, KS>), dim3((r.n + 127) / 128), dim3(256), 0, s, r,
-                       L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix);
+                       L, k, Ah, an, xn, B, w, gam, keys, fix, nfix);
 }
 
 template <int DT>
 static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                              const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
-                              uint32_t tshift, uint64_t *keys, uint8_t *ws, bool widen,
+                              const int8_t *A, const void *Aw, const int32_t *B, int32_t w, uint64_t *keys, uint8_t *ws, bool widen,
                               unsigned long long *nfix, hipStream_t s)
 {
     const uint32_t nf = L * k;
@@ -926,13 +906,13 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
     const float gam = (float)(2.0 * (g24 + g53) * (1.0 + 0x1p-10));
     const uint32_t ks = (r.row_bytes + 31) / 32;
     if (ks <= 2)
-        launch_mfma_t<DT, 2>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+        launch_mfma_t<DT, 2>(r, L, k, Ah, an, xn, B, w, gam, keys, fix, nfix, s);
     else if (ks <= 4)
-        launch_mfma_t<DT, 4>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+        launch_mfma_t<DT, 4>(r, L, k, Ah, an, xn, B, w, gam, keys, fix, nfix, s);
     else if (ks <= 8)
-        launch_mfma_t<DT, 8>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+        launch_mfma_t<DT, 8>(r, L, k, Ah, an, xn, B, w, gam, keys, fix, nfix, s);
     else
-        launch_mfma_t<DT, 16>(r, L, k, Ah, an, xn, B, w, tshift, gam, keys, fix, nfix, s);
+        launch_mfma_t<DT, 16>(r, L, k, Ah, an, xn, B, w, gam, keys, fix, nfix, s);
     if constexpr (DT != DT_I8)
         hipLaunchKernelGGL(fix_kernel<DT>, dim3(512), dim3(256), 0, s, r, d, k,
                            (const typename Chunk<DT>::a_t *)Aw, B, w, fix,
@@ -941,19 +921,18 @@ static hipError_t keys_fast_t(const Rows &r, uint32_t d, uint32_t L, uint32_t k,
 }
 
 hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, uint32_t k,
-                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w,
-                            uint32_t tshift, uint64_t *keys, void *ws, bool widen,
+                            const int8_t *A, const void *Aw, const int32_t *B, int32_t w, uint64_t *keys, void *ws, bool widen,
                             unsigned long long *nfix, hipStream_t s)
 {
     if (r.n == 0)
         return hipSuccess;
     if (dtype == DT_F16)
-        return keys_fast_t<DT_F16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+        return keys_fast_t<DT_F16>(r, d, L, k, A, Aw, B, w, keys, (uint8_t *)ws, widen,
                                    nfix, s);
     if (dtype == DT_I8)
-        return keys_fast_t<DT_I8>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+        return keys_fast_t<DT_I8>(r, d, L, k, A, Aw, B, w, keys, (uint8_t *)ws, widen,
                                   nfix, s);
-    return keys_fast_t<DT_BF16>(r, d, L, k, A, Aw, B, w, tshift, keys, (uint8_t *)ws, widen,
+    return keys_fast_t<DT_BF16>(r, d, L, k, A, Aw, B, w, keys, (uint8_t *)ws, widen,
                                 nfix, s);
 }
 
@@ -972,104 +951,6 @@ hipError_t launch_widen(int dtype, const int8_t *A, uint32_t n_fn, uint32_t d, v
         hipLaunchKernelGGL(widen_kernel<double>, grid, dim3(256), 0, s, A, (double *)out, d, dp,
                            n);
     return hipGetLastError();
-}
-
-size_t sort_temp_bytes(uint32_t n, uint32_t bits)
-{
-    size_t bytes = 0;
-    (void)hipcub::DeviceRadixSort::SortPairs(nullptr, bytes, (const uint64_t *)nullptr,
-                                             (uint64_t *)nullptr, (const uint32_t *)nullptr,
-                                             (uint32_t *)nullptr, n, 0, (int)bits);
-    return bytes;
-}
-
-size_t sort_temp_bytes_split(uint32_t total, uint32_t bits, uint32_t tbits)
-{
-    size_t a = 0, b = 0;
-    (void)hipcub::DeviceRadixSort::SortPairs(nullptr, a, (const uint64_t *)nullptr,
-                                             (uint64_t *)nullptr, (const uint32_t *)nullptr,
-                                             (uint32_t *)nullptr, total, 0, (int)bits);
-    (void)hipcub::DeviceRadixSort::SortPairs(nullptr, b, (const uint32_t *)nullptr,
-                                             (uint32_t *)nullptr, (const uint32_t *)nullptr,
-                                             (uint32_t *)nullptr, total, 0, (int)(tbits ? tbits : 1));
-    return a > b ? a : b;
-}
-
-size_t split_work_bytes(uint32_t total) { return (size_t)total * 32 + 1024; }
-
-// Table of each entry (entries are t n + row) and the identity permutation.
-__global__ void table_of_kernel(const uint32_t *ent, uint32_t n, uint32_t total, uint32_t *tkey,
-                                uint32_t *idx)
-{
-    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < total) {
-        tkey[i] = ent[i] / n;
-        idx[i] = i;
-    }
-}
-
-// sorted[j] = K1[idx[j]], perm[j] = the row of entry E1[idx[j]].
-__global__ void gather_sorted_kernel(const uint64_t *K1, const uint32_t *E1, const uint32_t *idx,
-                                     uint32_t n, uint32_t total, uint64_t *sorted, uint32_t *perm)
-{
-    const uint32_t j = blockIdx.x * 256 + threadIdx.x;
-    if (j < total) {
-        const uint32_t q = idx[j];
-        sorted[j] = K1[q];
-        perm[j] = E1[q] % n;
-    }
-}
-
-hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t *iota,
-                       uint32_t n, uint32_t L, uint32_t bits, bool joint, void *temp,
-                       size_t temp_bytes, void *work, hipStream_t s)
-{
-    if (n == 0)
-        return hipSuccess;
-    const uint32_t total = n * L;
-    const dim3 grid((total + 255) / 256);
-    if (joint) {
-        // keys carry their table above `bits`: one sort orders every table
-        // within its own segment [t n, (t + 1) n)
-        hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, s, iota, n, total);
-        hipError_t e = hipGetLastError();
-        size_t tb = temp_bytes;
-        if (e == hipSuccess)
-            e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys, sorted, iota, perm, total, 0,
-                                                   (int)(bits + table_bits(L)), s);
-        return e;
-    }
-    // The table does not fit above the key: sort all entries by key, then
-    // stably by table (two least-significant-digit-first passes of one sort),
-    // instead of L separate sorts.
-    uint8_t *w = (uint8_t *)work;
-    uint64_t *K1 = (uint64_t *)w;
-    uint32_t *E0 = (uint32_t *)(w + (size_t)total * 8);
-    uint32_t *E1 = E0 + total;
-    uint32_t *tkey = E1 + total;
-    uint32_t *tout = tkey + total;
-    uint32_t *idx0 = tout + total;
-    uint32_t *idx2 = idx0 + total;
-    hipLaunchKernelGGL(iota_kernel, grid, dim3(256), 0, s, E0, total, total);
-    hipError_t e = hipGetLastError();
-    size_t tb = temp_bytes;
-    if (e == hipSuccess)
-        e = hipcub::DeviceRadixSort::SortPairs(temp, tb, keys, K1, E0, E1, total, 0, (int)bits,
-                                               s);
-    if (e == hipSuccess) {
-        hipLaunchKernelGGL(table_of_kernel, grid, dim3(256), 0, s, E1, n, total, tkey, idx0);
-        e = hipGetLastError();
-    }
-    tb = temp_bytes;
-    if (e == hipSuccess)
-        e = hipcub::DeviceRadixSort::SortPairs(temp, tb, tkey, tout, idx0, idx2, total, 0,
-                                               (int)(table_bits(L) ? table_bits(L) : 1), s);
-    if (e == hipSuccess) {
-        hipLaunchKernelGGL(gather_sorted_kernel, grid, dim3(256), 0, s, K1, E1, idx2, n, total,
-                           sorted, perm);
-        e = hipGetLastError();
-    }
-    return e;
 }
 
 hipError_t launch_bucket_pairs(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,

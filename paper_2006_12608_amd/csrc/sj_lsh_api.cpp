@@ -83,11 +83,6 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const bool self = P == Q && n_p == n_q;
     const bool l2 = metric == SJ_L2;
     const uint32_t bits = sjl::key_bits(k, w);
-    // one sort for all tables when the table number fits above the key, else a
-    // sort by key and a stable sort by table
-    const bool joint = bits + sjl::table_bits(L) <= 64;
-    const uint32_t tshift = joint && L > 1 ? bits : 0;
-    const uint32_t sbits = joint ? bits + sjl::table_bits(L) : bits;
     // records: a region of min(n_p, n_q) per table (a table has at most that
     // many keys shared by P and Q)
     const uint64_t tcap = n_p < n_q ? n_p : n_q;
@@ -102,16 +97,12 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
             return fail(SJ_E_UNSUPPORTED, "n_p = %u, n_q = %u: a table could hold more than 2^%d "
                         "candidate tiles", n_p, n_q, sjl::TILE_BITS);
     }
-    size_t temp_bytes =
-        joint ? sjl::sort_temp_bytes(L * n_p, sbits)
-              : sjl::sort_temp_bytes_split(L * n_p, bits, sjl::table_bits(L));
-    const size_t tq = joint ? sjl::sort_temp_bytes(L * n_q, sbits)
-                            : sjl::sort_temp_bytes_split(L * n_q, bits, sjl::table_bits(L));
-    temp_bytes = temp_bytes > tq ? temp_bytes : tq;
+    // one sort workspace, used by P and then by Q
+    const size_t temp_bytes = sjl::sort_temp_bytes(n_max, L);
     const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
     // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
-    //          [sorted Q][perm P][perm Q][iota][bucket pairs][counters][sort temp]
+    //          [sorted Q][perm P][perm Q][bucket pairs][counters][sort temp]
     //          [widened projections]
     size_t need = 0;
     auto take = [&](size_t bytes) {
@@ -129,14 +120,12 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_sq = self ? off_sp : take((size_t)L * n_q * 8);
     const size_t off_pp = take((size_t)L * n_p * 4);
     const size_t off_pq = self ? off_pp : take((size_t)L * n_q * 4);
-    const size_t off_iota = take((size_t)L * n_max * 4);
     const size_t off_head = take((size_t)bp_cap * 16);
     const size_t off_bnq = take((size_t)bp_cap * 4);
     const size_t off_t0 = take((size_t)bp_cap * 8);
     const size_t off_cnt = take(6 * 8);
     const size_t off_tcnt = take((size_t)L * sjl::CSTRIDE * 8);
     const size_t off_temp = take(temp_bytes);
-    const size_t off_sortw = joint ? 0 : take(sjl::split_work_bytes((uint32_t)(L * n_max)));
     const size_t off_aw = take(a_bytes);
     // keys on the matrix cores where they apply
     const bool fast = sjl::keys_fast_applies(dtype, (uint32_t)krow, L, k, w);
@@ -170,25 +159,22 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     uint64_t *keys_p = (uint64_t *)(scr + off_kp), *keys_q = (uint64_t *)(scr + off_kq);
     SJ_HIP(sjl::launch_widen(dtype, A, L * k, d, scr + off_aw, s));
     if (fast) {
-        SJ_HIP(sjl::launch_keys_fast(dtype, rp, d, L, k, A, scr + off_aw, B, w, tshift, keys_p,
+        SJ_HIP(sjl::launch_keys_fast(dtype, rp, d, L, k, A, scr + off_aw, B, w, keys_p,
                                      scr + off_ws, true, cnt + 3, s));
         if (!self)
-            SJ_HIP(sjl::launch_keys_fast(dtype, rq, d, L, k, A, scr + off_aw, B, w, tshift,
+            SJ_HIP(sjl::launch_keys_fast(dtype, rq, d, L, k, A, scr + off_aw, B, w,
                                          keys_q, scr + off_ws, false, cnt + 4, s));
     } else {
-        SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, scr + off_aw, B, w, tshift, keys_p, s));
+        SJ_HIP(sjl::launch_keys(dtype, rp, d, L, k, scr + off_aw, B, w, keys_p, s));
         if (!self)
-            SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, tshift, keys_q, s));
+            SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, keys_q, s));
     }
     SJ_HIP(hipEventRecord(c->ev[1], s));
     uint64_t *sorted_p = (uint64_t *)(scr + off_sp), *sorted_q = (uint64_t *)(scr + off_sq);
     uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
-    uint32_t *iota = (uint32_t *)(scr + off_iota);
-    SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, iota, n_p, L, bits, joint,
-                            scr + off_temp, temp_bytes, scr + off_sortw, s));
+    SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, n_p, L, bits, scr + off_temp, s));
     if (!self)
-        SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, iota, n_q, L, bits, joint,
-                                scr + off_temp, temp_bytes, scr + off_sortw, s));
+        SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, n_q, L, bits, scr + off_temp, s));
     sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
                         (unsigned long long *)(scr + off_t0), tcnt, (uint32_t)tcap};
     SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));
@@ -254,5 +240,67 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     if (total > cap)
         return fail(SJ_E_OVERFLOW, "%llu matches exceed the capacity of %llu pairs",
                     (unsigned long long)total, (unsigned long long)cap);
+    return SJ_OK;
+}
+
+// Section 4's parameter choice for the LSH-bucketed join (host only).
+extern "C" double sj_lsh_collision(int32_t w, double sigma, double dist)
+{
+    if (std::isnan(dist) || dist < 0.0 || w < 0)
+        return std::nan("");
+    if (w == 0) {
+        // random hyperplane through the origin: it separates two vectors at
+        // angle theta with probability theta / pi
+        if (dist > M_PI)
+            return std::nan("");
+        return 1.0 - dist / M_PI;
+    }
+    // floor((<a, x> + b) / w) with a ~ N(0, sigma^2 I), b ~ U[0, w): the
+    // projections of two points at distance dist differ by u Z, u = sigma dist,
+    // Z ~ N(0, 1), and collide with probability E[max(0, 1 - u |Z| / w)] =
+    // 1 - 2 Phi(-w / u) - 2 u / (sqrt(2 pi) w) (1 - exp(-w^2 / (2 u^2)))
+    if (!(sigma > 0.0))
+        return std::nan("");
+    const double u = sigma * dist;
+    if (u == 0.0)
+        return 1.0;
+    const double c = (double)w / u;
+    const double phi = 0.5 * std::erfc(c / std::sqrt(2.0));   // Phi(-c)
+    return 1.0 - 2.0 * phi - 2.0 / (std::sqrt(2.0 * M_PI) * c) * (1.0 - std::exp(-0.5 * c * c));
+}
+
+extern "C" int sj_lsh_plan(double p1, double p2, uint64_t n, uint32_t tile, double recall,
+                           uint32_t *k, uint32_t *L_inst, uint32_t *reps)
+{
+    g_err.clear();
+    if (!k || !L_inst || !reps)
+        return fail(SJ_E_INVAL, "NULL output");
+    if (!(p2 > 0.0 && p2 < p1 && p1 < 1.0))
+        return fail(SJ_E_INVAL, "need 0 < p2 < p1 < 1 (p1 = %g, p2 = %g)", p1, p2);
+    if (!(recall > 0.0 && recall < 1.0))
+        return fail(SJ_E_INVAL, "recall %g is not in (0, 1)", recall);
+    if (tile == 0 || n == 0)
+        return fail(SJ_E_INVAL, "tile and n must be positive");
+    // p2^k <= tile / n: a point collides with at most `tile` far points per
+    // table in expectation (one tile of the matrix cores); k = 0 when n <= tile
+    uint32_t kk = 0;
+    const double target = (double)tile / (double)n;
+    double pk = 1.0;
+    while (pk > target) {
+        pk *= p2;
+        if (++kk > 64)
+            return fail(SJ_E_UNSUPPORTED, "more than 64 functions per table needed");
+    }
+    // one instance: L = ceil(1 / p1^k) tables find a pair at the threshold
+    // with probability 1 - (1 - p1^k)^L >= 1 - 1/e
+    const double q = std::pow(p1, (double)kk);
+    const double L = std::ceil(1.0 / q - 1e-9);
+    if (L > 4294967295.0)
+        return fail(SJ_E_UNSUPPORTED, "1 / p1^k = %g tables", 1.0 / q);
+    // R independent instances merged miss it with probability <= e^-R
+    const double R = std::ceil(-std::log(1.0 - recall) - 1e-12);
+    *k = kk;
+    *L_inst = (uint32_t)L;
+    *reps = (uint32_t)(R < 1.0 ? 1.0 : R);
     return SJ_OK;
 }
