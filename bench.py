@@ -249,17 +249,55 @@ def bench_jl(args, w, Pd, ctx):
     }), flush=True)
 
 
+def lsh_plan(args, w):
+    """Section 4's parameters (sj_lsh_plan) for the workload at the recall
+    target of --lsh-plan RECALL[,w]: one function's collision probability p1
+    at the join's threshold and p2 at the workload's typical distance between
+    unrelated points (cosine: orthogonal; squared L2: the median distance of
+    2000 random pairs), the 128-row tile for sqrt(m).  Returns (L, k, w, plan
+    record); L = L_inst * reps, capped at the library's 256 tables."""
+    import math
+    import numpy as np
+    import paper_2006_12608_amd as sj
+    parts = args.lsh_plan.split(",")
+    recall = float(parts[0])
+    wid = int(parts[1]) if len(parts) > 1 else (0 if w.metric == "ip" else 2000)
+    sigma = 32.0   # workloads.lsh_params' projection scale
+    if wid == 0:
+        d1, d2 = math.acos(min(1.0, w.threshold)), math.pi / 2
+    else:
+        rng = np.random.default_rng(5)
+        i, j = rng.integers(0, w.n_p, 2000), rng.integers(0, w.n_q, 2000)
+        x = w.P[i].astype(np.float64)
+        y = w.Q[j].astype(np.float64)
+        d1, d2 = math.sqrt(w.threshold), float(np.median(np.sqrt(((x - y) ** 2).sum(1))))
+    p1, p2 = sj.sj_lsh_collision(wid, sigma, d1), sj.sj_lsh_collision(wid, sigma, d2)
+    st, k, L_inst, reps = sj.sj_lsh_plan(p1, p2, max(w.n_p, w.n_q), 128, recall)
+    if st != sj.SJ_OK:
+        raise SystemExit(f"sj_lsh_plan: {sj.sj_last_error()}")
+    L = min(L_inst * reps, 256)
+    return L, k, wid, {"recall_target": recall, "p1": p1, "p2": p2, "dist_near": d1,
+                       "dist_far": d2, "k": k, "L_inst": L_inst, "reps": reps,
+                       "tables_planned": L_inst * reps, "tables_run": L,
+                       "guaranteed_recall_at_threshold":
+                           1 - (1 - p1 ** k) ** L}
+
+
 def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
     """The LSH-bucketed join of Theorem 3 on the workload: one JSON line with
     its whole-call throughput, the share of the exact join it finds, its
-    candidate pair evaluations and the bucket-join kernel's MFMA fraction on
-    those candidates."""
+    candidate pair evaluations, the bucket-join kernel's MFMA fraction on
+    those candidates, and the all-pairs join's time on the same workload."""
     import numpy as np
     import torch
     import paper_2006_12608_amd as sj
     import workloads
-    parts = [int(v) for v in args.lsh.split(",")]
-    L, k, wid = parts[0], parts[1], parts[2] if len(parts) > 2 else 0
+    plan = None
+    if args.lsh_plan:
+        L, k, wid, plan = lsh_plan(args, w)
+    else:
+        parts = [int(v) for v in args.lsh.split(",")]
+        L, k, wid = parts[0], parts[1], parts[2] if len(parts) > 2 else 0
     h = workloads.lsh_params(1300 + workloads.NAMES.index(args.workload), L, k, w.d, wid)
     A = torch.from_numpy(h.A).cuda()
     B = torch.from_numpy(h.B).cuda() if wid > 0 else None
@@ -292,6 +330,20 @@ def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
     jms = float(np.mean(join_ms))
     flop = 2.0 * n_cand * max(w.d, 1)
     peak = PEAK[w.dtype]
+    # the all-pairs join of the same workload, for the speed-up at this recall
+    fn = sj.sj_join_ip if w.metric == "ip" else sj.sj_join_l2
+    out2 = torch.empty((max(exact_total, 1), 2), dtype=torch.int32, device="cuda")
+    for _ in range(2):
+        fn(ctx, dt, Pd.data_ptr(), w.n_p, Qd.data_ptr(), w.n_q, w.d, w.threshold,
+           out2.data_ptr(), exact_total, 0)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    reps_ap = 3
+    for _ in range(reps_ap):
+        fn(ctx, dt, Pd.data_ptr(), w.n_p, Qd.data_ptr(), w.n_q, w.d, w.threshold,
+           out2.data_ptr(), exact_total, 0)
+    torch.cuda.synchronize()
+    ap_ms = (time.perf_counter() - t1) / reps_ap * 1e3
     print(json.dumps({
         "metric": "pair-evaluations/sec (all-pairs equivalent, LSH-bucketed join)",
         "value": w.n_p * w.n_q / (ms_step / 1e3),
@@ -304,6 +356,9 @@ def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
                    "parallelism": "single GPU"},
         "n_out": int(n_out), "exact_total": int(exact_total),
         "recall": n_out / exact_total if exact_total else None,
+        "all_pairs_ms_per_step": ap_ms,
+        "speedup_vs_all_pairs": ap_ms / ms_step,
+        "plan": plan,
         "candidate_pair_evals": int(n_cand),
         "candidate_fraction": n_cand / (w.n_p * w.n_q),
         "candidate_pair_evals_per_s": n_cand / (ms_step / 1e3),
@@ -338,6 +393,9 @@ def main():
     ap.add_argument("--jl", default=None, metavar="k,zeta",
                     help="time the TCU JL transform (sj_jl) of the workload's P to dimension k "
                          "with Lemma 3's levels for zeta; prints its own JSON line")
+    ap.add_argument("--lsh-plan", default=None, metavar="RECALL[,w]",
+                    help="time the LSH-bucketed join with Section 4's parameters for a recall "
+                         "target (sj_lsh_plan); prints its own JSON line")
     ap.add_argument("--lsh", default=None, metavar="L,k[,w]",
                     help="time the LSH-bucketed join (sj_join_lsh) on the workload instead: "
                          "L tables of k concatenated projections (w = 0: signs; w > 0: "
@@ -378,7 +436,7 @@ def main():
         bench_jl(args, w, Pd, ctx)
         return
     total = sj.count(Pd, Qd, w.threshold, w.metric, ctx=ctx)
-    if args.lsh:
+    if args.lsh or args.lsh_plan:
         bench_lsh(args, w, Pd, Qd, ctx, total)
         return
     out = torch.empty((max(total, 1), 2), dtype=torch.int32, device="cuda")

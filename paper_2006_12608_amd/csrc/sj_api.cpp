@@ -414,8 +414,7 @@ int run(sj_ctx *c, const Request &rq, uint64_t *n_out, const Fixed *fx = nullptr
     if (!blocks) {
         // a self-join computes the upper triangle only and mirrors its pairs
         const bool tri = (self || rq.symmetric) && rq.n_p == rq.n_q;
-        const int mode = tri && plan.family == sjk::FAM_RESIDENT ? sjk::MODE_TRI
-                                                                 : sjk::MODE_SINGLE;
+        const int mode = tri ? sjk::MODE_TRI : sjk::MODE_SINGLE;
         SJ_HIP(sjk::launch_join(plan, rq.dtype, rq.metric, mode, g, s));
         if (rq.timing)
             SJ_HIP(hipEventRecord(c->ev[2], s));

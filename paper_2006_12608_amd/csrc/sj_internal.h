@@ -23,9 +23,9 @@ enum Mode {
                       // (resident kernel only), for an emit pass that reads
                       // the records instead of recomputing
     MODE_TRI = 5      // single pass of a self-join (Q is P) over the upper
-                      // triangle only: Q tiles below a workgroup's rows are
-                      // skipped, each match (i, j) with i < j is written as
-                      // (i, j) and (j, i), and (i, i) once (resident kernel only)
+                      // triangle only: tiles below the diagonal are skipped,
+                      // each match (i, j) with i < j is written as (i, j) and
+                      // (j, i), and (i, i) once
 };
 
 // The matches of one 32x32 block of results, as found by the first pass of

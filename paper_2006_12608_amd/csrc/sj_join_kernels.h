@@ -623,227 +623,267 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, c32 = lane & 31;
     const uint32_t qsplit = g.qsplit;
-    const uint32_t pb = blockIdx.x / qsplit, qs = blockIdx.x - pb * qsplit;
     const uint32_t n_qt = (g.n_q + BN - 1) / BN;
-    // self-join triangle: tiles whose columns all lie below the workgroup's
-    // first row hold no pair (i, j) with i <= j
-    const uint32_t t_lo = MODE == MODE_TRI ? min(pb * BM / BN, n_qt) : 0u;
-    const uint32_t t0 = t_lo + (uint32_t)((uint64_t)qs * (n_qt - t_lo) / qsplit);
-    const uint32_t t1 = t_lo + (uint32_t)((uint64_t)(qs + 1) * (n_qt - t_lo) / qsplit);
-    const uint32_t prow0 = pb * BM + wave * 32 * WMB;
-    const uint32_t ibase = prow0 + 4 * half;
-
-    i32x4 A[WMB][KS];
-#pragma unroll
-    for (int a = 0; a < WMB; ++a)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            A[a][ks] = load_chunk(g.P, prow0 + 32 * a + c32, g.n_p, g.row_bytes,
-                                  32 * ks + 16 * half);
-
-    V nmin = big_val<V>();
-    const V *nrows = nullptr;
-    if constexpr (NEED_NORMS) {
-        nmin = stage_row_norms<DT, WMB>(prow0, lane, s_np[wave], g);
-        nrows = &s_np[wave][4 * half];
-    }
-    const V nb = bound_base<DT, MET>(nmin, g);
-    // Drain the resident-row loads here: otherwise the wait inserted for their
-    // first use inside the tile loop also waits for the next tile's prefetch.
-    __builtin_amdgcn_s_waitcnt(0);
-
-    // Q tiles go straight from global memory into LDS (no staging registers)
-    // with buffer loads: each wave instruction fills 64 consecutive 16-byte
-    // LDS positions; the lane at position p loads chunk p % (CPR + 1) of tile
-    // row p / (CPR + 1) (the pad position reloads chunk 0).  The tile's buffer
-    // descriptor ends at row n_q, so rows past it read zeros (their columns
-    // are never reported); chunks past row_bytes read the row's last chunk
-    // (they meet the zero padding of the resident rows).  (A global_load_lds
-    // would do the same, but the compiler then treats every LDS read of the
-    // loop as unordered and drains them all at each use.)
-    constexpr int NCALL = (TCH + 64 * NW - 1) / (64 * NW);   // direct loads per wave
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
-    uint32_t loff[NCALL];   // this lane's byte offset in the tile, per load
-#pragma unroll
-    for (int kk = 0; kk < NCALL; ++kk) {
-        const int pos = 64 * (kk * NW + wv) + lane;
-        const int cp = pos % (CPR + 1);
-        const uint32_t row = min(pos / (CPR + 1), BN - 1);
-        loff[kk] = row * g.row_bytes + min((uint32_t)(16 * (cp == CPR ? 0 : cp)), g.row_bytes - 16);
-    }
-    // waves whose last load would start past the tile skip it (uniform)
-    const bool last_call = TCH % (64 * NW) == 0 || 64 * ((NCALL - 1) * NW + wv) < TCH;
-    auto stage_issue = [&](uint32_t t, uint8_t *dst) {
-        const uint32_t rows = min(g.n_q - t * BN, (uint32_t)BN);
-        const uint8_t *base = g.Q + (size_t)t * BN * g.row_bytes;
-#pragma unroll
-        for (int kk = 0; kk < NCALL; ++kk) {
-            if (kk == NCALL - 1 && !last_call)
-                break;
-            buffer_load_lds16(base, rows * g.row_bytes, loff[kk], dst + 1024 * (kk * NW + wv));
-        }
-    };
-    auto norm_load = [&](uint32_t t, V &stn) {
-        if constexpr (NEED_NORMS) {
-            if (tid < BN) {
-                const uint32_t jq = t * BN + tid;
-                stn = jq < g.n_q ? ((const V *)g.norm_q)[jq] : big_val<V>();
-            }
-        }
-    };
-    auto norm_store = [&](V *dst, V stn) {
-        if constexpr (NEED_NORMS) {
-            if (tid < BN)
-                dst[tid] = stn;
-        }
-    };
-    if (t0 < t1) {
-        V stn = V(0);
-        stage_issue(t0, s_q0);
-        norm_load(t0, stn);
-        norm_store(s_nq0, stn);
-    }
-    if constexpr (MODE == MODE_RECORD) {
-        if (tid == 0)
-            s_nrec = 0;
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
     WaveOut wo{(lds_pair *)s_out[wave], (uint32_t)OUT_CAP, 0u, 0ull, 0ull,
                (__attribute__((address_space(3))) uint32_t *)&s_nrec};
-    const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
-    // Bound of one wave sub-tile from its running max, then the exact path if
-    // any lane may match.
-    auto check = [&](const acc_t(&a)[WMB], const V(&mb)[WMB], uint32_t jp, V nyp,
-                     uint64_t &run) __attribute__((always_inline)) {
-        const bool may = lane_bound<DT, MET>(max_of<WMB>(mb), nb, nyp, g);
-        if (__builtin_expect(__ballot(may) != 0, 0))
-            exact_blocks<DT, MET, MODE, WMB>(a, mb, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
-    };
-
-    // A tile is a stream of SUBS * KS k-steps (sub-tile s = step / KS).  Each
-    // step issues the LDS read of the B-fragment LOOK steps ahead (a ring of
-    // LOOK + 1 fragments, continued across sub-tiles) and the WMB MFMAs of its
-    // own fragment; with two accumulator sets it also folds 16 WMB / KS results
-    // of the previous sub-tile into that sub-tile's running max, so the
-    // epilogue's VALU work runs beside the matrix cores.  Scheduling barriers
-    // between steps keep this order (left alone, the compiler drains every
-    // read right before its MFMAs).
-    constexpr int NSTEP = SUBS * KS;
-    constexpr int LOOK = KS >= 16 ? 2 : 3;
-    constexpr int RING = LOOK + 1;
-    constexpr int NVAL = 16 * WMB;
-    constexpr int NACC = PIPE ? 2 : 1;
-    acc_t acc[NACC][WMB];
-#pragma unroll
-    for (int c = 0; c < NACC; ++c)
-#pragma unroll
-        for (int a = 0; a < WMB; ++a)
-            acc[c][a] = acc_t{};
-    // Previous sub-tile of the pipeline when it belongs to the previous tile.
-    bool have_prev = false;
-    uint32_t j_prev = 0;
-    V ny_prev = V(0);
-    uint64_t blk_prev = 0, run_prev = 0;
-
-    auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt)
-                    __attribute__((always_inline)) {
-        const bool more = t + 1 < t1;
-        V stn = V(0);
-        if (more) {
-            stage_issue(t + 1, nxt);
-            norm_load(t + 1, stn);
+    // A workgroup sweeps a range of Q tiles for one block of P rows.  In the
+    // self-join triangle (tiles whose columns all lie below a block's first
+    // row hold no pair (i, j) with i <= j) blocks pb and n_pb - 1 - pb are
+    // paired and the workgroup takes its share of the two blocks' tiles, one
+    // block after the other (a segment each), so every workgroup sweeps
+    // about as many tiles.
+    auto segment = [&](int seg) __attribute__((always_inline)) {
+        uint32_t pb, t0, t1;
+        if constexpr (MODE == MODE_TRI) {
+            const uint32_t n_pb = (g.n_p + BM - 1) / BM;
+            const uint32_t pp = blockIdx.x / qsplit, qs = blockIdx.x - pp * qsplit;
+            const uint32_t pa = pp, pz = n_pb - 1 - pp;
+            const uint32_t la = n_qt - min(pa * BM / BN, n_qt);
+            const uint32_t lz = pz != pa ? n_qt - min(pz * BM / BN, n_qt) : 0u;
+            const uint64_t tot = (uint64_t)la + lz;
+            const uint32_t s0 = (uint32_t)((uint64_t)qs * tot / qsplit);
+            const uint32_t s1 = (uint32_t)((uint64_t)(qs + 1) * tot / qsplit);
+            if (seg == 0) {
+                pb = pa;
+                t0 = min(s0, la);
+                t1 = min(s1, la);
+            } else {
+                pb = pz;
+                t0 = max(s0, la) - la;
+                t1 = max(s1, la) - la;
+            }
+            const uint32_t t_lo = min(pb * BM / BN, n_qt);
+            t0 += t_lo;
+            t1 += t_lo;
+            if (t0 >= t1)
+                return;   // uniform: the workgroup's share holds no tile of this block
+        } else {
+            (void)seg;
+            pb = blockIdx.x / qsplit;
+            const uint32_t qs = blockIdx.x - pb * qsplit;
+            t0 = (uint32_t)((uint64_t)qs * n_qt / qsplit);
+            t1 = (uint32_t)((uint64_t)(qs + 1) * n_qt / qsplit);
         }
-        const uint64_t blk = wave_row_block * n_qt + t;
-        uint64_t blk_run = 0;
-        if constexpr (MODE == MODE_EMIT)
-            blk_run = g.block_offsets[blk];
+        const uint32_t prow0 = pb * BM + wave * 32 * WMB;
+        const uint32_t ibase = prow0 + 4 * half;
 
-        // this lane's B-fragment of step q: row 32 (q / KS) + c32, chunk
-        // 2 (q % KS) + half
-        const uint8_t *bq = cur + c32 * LS + 16 * half;
-        i32x4 ring[RING];
-        static_for<0, (LOOK < NSTEP ? LOOK : NSTEP)>([&](auto Q) __attribute__((always_inline)) {
-            constexpr int q = decltype(Q)::value;
-            ring[q] = *(const i32x4 *)(bq + (q / KS) * 32 * LS + (q % KS) * 32);
-        });
-        V ny_sub[SUBS];
-        static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
-            constexpr int s = decltype(S)::value;
-            constexpr int ci = PIPE ? (s & 1) : 0, pi = PIPE ? (ci ^ 1) : 0;
-            ny_sub[s] = V(0);
-            if constexpr (NEED_NORMS)
-                ny_sub[s] = ncur[32 * s + c32];
-            V mb[WMB];
-#pragma unroll
-            for (int a = 0; a < WMB; ++a)
-                mb[a] = V(0);
-            static_for<0, KS>([&](auto K) __attribute__((always_inline)) {
-                constexpr int ks = decltype(K)::value, q = s * KS + ks;
-                if constexpr (q + LOOK < NSTEP) {
-                    constexpr int qn = q + LOOK;
-                    ring[qn % RING] =
-                        *(const i32x4 *)(bq + (qn / KS) * 32 * LS + (qn % KS) * 32);
+        i32x4 A[WMB][KS];
+    #pragma unroll
+        for (int a = 0; a < WMB; ++a)
+    #pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                A[a][ks] = load_chunk(g.P, prow0 + 32 * a + c32, g.n_p, g.row_bytes,
+                                      32 * ks + 16 * half);
+
+        V nmin = big_val<V>();
+        const V *nrows = nullptr;
+        if constexpr (NEED_NORMS) {
+            nmin = stage_row_norms<DT, WMB>(prow0, lane, s_np[wave], g);
+            nrows = &s_np[wave][4 * half];
+        }
+        const V nb = bound_base<DT, MET>(nmin, g);
+        // Drain the resident-row loads here: otherwise the wait inserted for their
+        // first use inside the tile loop also waits for the next tile's prefetch.
+        __builtin_amdgcn_s_waitcnt(0);
+
+        // Q tiles go straight from global memory into LDS (no staging registers)
+        // with buffer loads: each wave instruction fills 64 consecutive 16-byte
+        // LDS positions; the lane at position p loads chunk p % (CPR + 1) of tile
+        // row p / (CPR + 1) (the pad position reloads chunk 0).  The tile's buffer
+        // descriptor ends at row n_q, so rows past it read zeros (their columns
+        // are never reported); chunks past row_bytes read the row's last chunk
+        // (they meet the zero padding of the resident rows).  (A global_load_lds
+        // would do the same, but the compiler then treats every LDS read of the
+        // loop as unordered and drains them all at each use.)
+        constexpr int NCALL = (TCH + 64 * NW - 1) / (64 * NW);   // direct loads per wave
+        const int wv = __builtin_amdgcn_readfirstlane(wave);
+        uint32_t loff[NCALL];   // this lane's byte offset in the tile, per load
+    #pragma unroll
+        for (int kk = 0; kk < NCALL; ++kk) {
+            const int pos = 64 * (kk * NW + wv) + lane;
+            const int cp = pos % (CPR + 1);
+            const uint32_t row = min(pos / (CPR + 1), BN - 1);
+            loff[kk] = row * g.row_bytes + min((uint32_t)(16 * (cp == CPR ? 0 : cp)), g.row_bytes - 16);
+        }
+        // waves whose last load would start past the tile skip it (uniform)
+        const bool last_call = TCH % (64 * NW) == 0 || 64 * ((NCALL - 1) * NW + wv) < TCH;
+        auto stage_issue = [&](uint32_t t, uint8_t *dst) {
+            const uint32_t rows = min(g.n_q - t * BN, (uint32_t)BN);
+            const uint8_t *base = g.Q + (size_t)t * BN * g.row_bytes;
+    #pragma unroll
+            for (int kk = 0; kk < NCALL; ++kk) {
+                if (kk == NCALL - 1 && !last_call)
+                    break;
+                buffer_load_lds16(base, rows * g.row_bytes, loff[kk], dst + 1024 * (kk * NW + wv));
+            }
+        };
+        auto norm_load = [&](uint32_t t, V &stn) {
+            if constexpr (NEED_NORMS) {
+                if (tid < BN) {
+                    const uint32_t jq = t * BN + tid;
+                    stn = jq < g.n_q ? ((const V *)g.norm_q)[jq] : big_val<V>();
                 }
-#pragma unroll
-                for (int a = 0; a < WMB; ++a)
-                    acc[ci][a] = M::mma(A[a][ks], ring[q % RING], ks == 0 ? acc_t{} : acc[ci][a]);
-                if constexpr (PIPE)
-                    fold_max_blk<ks * NVAL / KS, (ks + 1) * NVAL / KS, WMB>(acc[pi], mb);
-                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        auto norm_store = [&](V *dst, V stn) {
+            if constexpr (NEED_NORMS) {
+                if (tid < BN)
+                    dst[tid] = stn;
+            }
+        };
+        if (t0 < t1) {
+            V stn = V(0);
+            stage_issue(t0, s_q0);
+            norm_load(t0, stn);
+            norm_store(s_nq0, stn);
+        }
+        if constexpr (MODE == MODE_RECORD) {
+            if (tid == 0)
+                s_nrec = 0;
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+
+        const uint64_t wave_row_block = (uint64_t)pb * NW + wave;
+        // Bound of one wave sub-tile from its running max, then the exact path if
+        // any lane may match.
+        auto check = [&](const acc_t(&a)[WMB], const V(&mb)[WMB], uint32_t jp, V nyp,
+                         uint64_t &run) __attribute__((always_inline)) {
+            const bool may = lane_bound<DT, MET>(max_of<WMB>(mb), nb, nyp, g);
+            if (__builtin_expect(__ballot(may) != 0, 0))
+                exact_blocks<DT, MET, MODE, WMB>(a, mb, ibase, jp, lane, nb, nyp, nrows, g, run, wo);
+        };
+
+        // A tile is a stream of SUBS * KS k-steps (sub-tile s = step / KS).  Each
+        // step issues the LDS read of the B-fragment LOOK steps ahead (a ring of
+        // LOOK + 1 fragments, continued across sub-tiles) and the WMB MFMAs of its
+        // own fragment; with two accumulator sets it also folds 16 WMB / KS results
+        // of the previous sub-tile into that sub-tile's running max, so the
+        // epilogue's VALU work runs beside the matrix cores.  Scheduling barriers
+        // between steps keep this order (left alone, the compiler drains every
+        // read right before its MFMAs).
+        constexpr int NSTEP = SUBS * KS;
+        constexpr int LOOK = KS >= 16 ? 2 : 3;
+        constexpr int RING = LOOK + 1;
+        constexpr int NVAL = 16 * WMB;
+        constexpr int NACC = PIPE ? 2 : 1;
+        acc_t acc[NACC][WMB];
+    #pragma unroll
+        for (int c = 0; c < NACC; ++c)
+    #pragma unroll
+            for (int a = 0; a < WMB; ++a)
+                acc[c][a] = acc_t{};
+        // Previous sub-tile of the pipeline when it belongs to the previous tile.
+        bool have_prev = false;
+        uint32_t j_prev = 0;
+        V ny_prev = V(0);
+        uint64_t blk_prev = 0, run_prev = 0;
+
+        auto tile = [&](uint32_t t, const uint8_t *cur, uint8_t *nxt, const V *ncur, V *nnxt)
+                        __attribute__((always_inline)) {
+            const bool more = t + 1 < t1;
+            V stn = V(0);
+            if (more) {
+                stage_issue(t + 1, nxt);
+                norm_load(t + 1, stn);
+            }
+            const uint64_t blk = wave_row_block * n_qt + t;
+            uint64_t blk_run = 0;
+            if constexpr (MODE == MODE_EMIT)
+                blk_run = g.block_offsets[blk];
+
+            // this lane's B-fragment of step q: row 32 (q / KS) + c32, chunk
+            // 2 (q % KS) + half
+            const uint8_t *bq = cur + c32 * LS + 16 * half;
+            i32x4 ring[RING];
+            static_for<0, (LOOK < NSTEP ? LOOK : NSTEP)>([&](auto Q) __attribute__((always_inline)) {
+                constexpr int q = decltype(Q)::value;
+                ring[q] = *(const i32x4 *)(bq + (q / KS) * 32 * LS + (q % KS) * 32);
             });
-            if constexpr (PIPE) {
-                if constexpr (s == 0) {
-                    if (have_prev) {
-                        wo.blk = blk_prev;
-                        check(acc[pi], mb, j_prev, ny_prev, run_prev);
-                        if constexpr (counting_mode<MODE>()) {
-                            if (lane == 0)
-                                g.block_counts[blk_prev] = (uint32_t)run_prev;
+            V ny_sub[SUBS];
+            static_for<0, SUBS>([&](auto S) __attribute__((always_inline)) {
+                constexpr int s = decltype(S)::value;
+                constexpr int ci = PIPE ? (s & 1) : 0, pi = PIPE ? (ci ^ 1) : 0;
+                ny_sub[s] = V(0);
+                if constexpr (NEED_NORMS)
+                    ny_sub[s] = ncur[32 * s + c32];
+                V mb[WMB];
+    #pragma unroll
+                for (int a = 0; a < WMB; ++a)
+                    mb[a] = V(0);
+                static_for<0, KS>([&](auto K) __attribute__((always_inline)) {
+                    constexpr int ks = decltype(K)::value, q = s * KS + ks;
+                    if constexpr (q + LOOK < NSTEP) {
+                        constexpr int qn = q + LOOK;
+                        ring[qn % RING] =
+                            *(const i32x4 *)(bq + (qn / KS) * 32 * LS + (qn % KS) * 32);
+                    }
+    #pragma unroll
+                    for (int a = 0; a < WMB; ++a)
+                        acc[ci][a] = M::mma(A[a][ks], ring[q % RING], ks == 0 ? acc_t{} : acc[ci][a]);
+                    if constexpr (PIPE)
+                        fold_max_blk<ks * NVAL / KS, (ks + 1) * NVAL / KS, WMB>(acc[pi], mb);
+                    __builtin_amdgcn_sched_barrier(0);
+                });
+                if constexpr (PIPE) {
+                    if constexpr (s == 0) {
+                        if (have_prev) {
+                            wo.blk = blk_prev;
+                            check(acc[pi], mb, j_prev, ny_prev, run_prev);
+                            if constexpr (counting_mode<MODE>()) {
+                                if (lane == 0)
+                                    g.block_counts[blk_prev] = (uint32_t)run_prev;
+                            }
                         }
+                    } else {
+                        wo.blk = blk;
+                        check(acc[pi], mb, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
                     }
                 } else {
+                    fold_max_blk<0, NVAL, WMB>(acc[0], mb);
                     wo.blk = blk;
-                    check(acc[pi], mb, t * BN + 32 * (s - 1) + c32, ny_sub[s - 1], blk_run);
+                    check(acc[0], mb, t * BN + 32 * s + c32, ny_sub[s], blk_run);
                 }
-            } else {
-                fold_max_blk<0, NVAL, WMB>(acc[0], mb);
-                wo.blk = blk;
-                check(acc[0], mb, t * BN + 32 * s + c32, ny_sub[s], blk_run);
-            }
-        });
-        if constexpr (PIPE) {
-            j_prev = t * BN + 32 * (SUBS - 1) + c32;
-            ny_prev = ny_sub[SUBS - 1];
-            blk_prev = blk;
-            run_prev = blk_run;
-            have_prev = true;
-        } else if constexpr (counting_mode<MODE>()) {
-            if (lane == 0)
-                g.block_counts[blk] = (uint32_t)blk_run;
-        }
-        if (more)
-            norm_store(nnxt, stn);
-        __builtin_amdgcn_s_waitcnt(0);   // this wave's direct loads of tile t+1 landed
-        __syncthreads();
-    };
-    for (uint32_t t = t0; t < t1; t += 2) {
-        tile(t, s_q0, s_q1, s_nq0, s_nq1);
-        if (t + 1 < t1)
-            tile(t + 1, s_q1, s_q0, s_nq1, s_nq0);
-    }
-    if constexpr (PIPE) {
-        if (have_prev) {
-            V mb[WMB];
-            fold_max_blk<0, NVAL, WMB>(acc[NACC - 1], mb);
-            wo.blk = blk_prev;
-            check(acc[NACC - 1], mb, j_prev, ny_prev, run_prev);
-            if constexpr (counting_mode<MODE>()) {
+            });
+            if constexpr (PIPE) {
+                j_prev = t * BN + 32 * (SUBS - 1) + c32;
+                ny_prev = ny_sub[SUBS - 1];
+                blk_prev = blk;
+                run_prev = blk_run;
+                have_prev = true;
+            } else if constexpr (counting_mode<MODE>()) {
                 if (lane == 0)
-                    g.block_counts[blk_prev] = (uint32_t)run_prev;
+                    g.block_counts[blk] = (uint32_t)blk_run;
+            }
+            if (more)
+                norm_store(nnxt, stn);
+            __builtin_amdgcn_s_waitcnt(0);   // this wave's direct loads of tile t+1 landed
+            __syncthreads();
+        };
+        for (uint32_t t = t0; t < t1; t += 2) {
+            tile(t, s_q0, s_q1, s_nq0, s_nq1);
+            if (t + 1 < t1)
+                tile(t + 1, s_q1, s_q0, s_nq1, s_nq0);
+        }
+        if constexpr (PIPE) {
+            if (have_prev) {
+                V mb[WMB];
+                fold_max_blk<0, NVAL, WMB>(acc[NACC - 1], mb);
+                wo.blk = blk_prev;
+                check(acc[NACC - 1], mb, j_prev, ny_prev, run_prev);
+                if constexpr (counting_mode<MODE>()) {
+                    if (lane == 0)
+                        g.block_counts[blk_prev] = (uint32_t)run_prev;
+                }
             }
         }
+    };
+    if constexpr (MODE == MODE_TRI) {
+#pragma nounroll
+        for (int seg = 0; seg < 2; ++seg)
+            segment(seg);
+    } else {
+        segment(0);
     }
     if constexpr (single_mode<MODE>())
         flush_workgroup_out<NW>(wo, wave, lane, g);
@@ -909,6 +949,9 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
     if (in >= hp * hq)
         return;
     const uint32_t pt = gp * G + in / hq, qt = gq * G + in % hq;
+    // self-join triangle: a tile wholly below the diagonal holds no pair i <= j
+    if (MODE == MODE_TRI && pt > qt)
+        return;
     const uint32_t p0 = pt * ST_BM, q0 = qt * ST_BN;
     const uint32_t n_chunks = (g.row_bytes + ST_KC - 1) / ST_KC;
 
@@ -1077,7 +1120,7 @@ __global__ void __launch_bounds__(ST_NW * 64) join_streamed(JoinArgs g)
             exact_blocks<DT, MET, MODE, SA>(blk_acc, mb, ibase, j, lane, nb, ny, nrows, g,
                                             blk_run, wo);
     }
-    if constexpr (MODE == MODE_SINGLE)
+    if constexpr (single_mode<MODE>())
         flush_workgroup_out<ST_NW>(wo, wave, lane, g);
     if constexpr (MODE == MODE_EMIT)
         flush_wave_out<MODE>(wo, lane, g);
@@ -1133,7 +1176,10 @@ hipError_t launch_resident_v(const Plan &p, const JoinArgs &g, hipStream_t st)
     constexpr int KS = ResidentCfg<DT>::KS[V];
     constexpr int WMB = res_wmb<DT, KS>();
     constexpr int BN = res_bn<KS>();
-    hipLaunchKernelGGL((join_resident<DT, MET, MODE, KS, WMB, RES_NW, BN>), dim3(p.grid),
+    // the self-join triangle pairs the blocks of P rows (see join_resident)
+    const uint32_t grid =
+        MODE == MODE_TRI ? (p.grid / p.qsplit + 1) / 2 * p.qsplit : p.grid;
+    hipLaunchKernelGGL((join_resident<DT, MET, MODE, KS, WMB, RES_NW, BN>), dim3(grid),
                        dim3(RES_NW * 64), 0, st, g);
     return hipGetLastError();
 }
@@ -1208,10 +1254,18 @@ hipError_t launch_dtype(const Plan &p, int metric, int mode, const JoinArgs &g, 
         }
     }
     if (mode == MODE_TRI) {
-        // resident kernel only
-        if (p.family != FAM_RESIDENT || (metric != MET_IP && metric != MET_L2))
+        if (metric != MET_IP && metric != MET_L2)
             return hipErrorInvalidValue;
         const bool l2 = metric == MET_L2;
+        if (p.family == FAM_STREAMED) {
+            if (l2)
+                hipLaunchKernelGGL((join_streamed<DT, MET_L2, MODE_TRI>), dim3(p.grid),
+                                   dim3(ST_NW * 64), 0, st, g);
+            else
+                hipLaunchKernelGGL((join_streamed<DT, MET_IP, MODE_TRI>), dim3(p.grid),
+                                   dim3(ST_NW * 64), 0, st, g);
+            return hipGetLastError();
+        }
         switch (p.variant) {
         case 0: return l2 ? launch_resident_v<DT, MET_L2, MODE_TRI, 0>(p, g, st)
                           : launch_resident_v<DT, MET_IP, MODE_TRI, 0>(p, g, st);

@@ -54,41 +54,68 @@ hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, u
 
 // Tile edge of the bucket join (rows of P and of Q per workgroup tile).
 constexpr uint32_t TILE = 128;
-// Low bits of the packed bucket-pair counter that hold the running tile count.
-constexpr int TILE_BITS = 38;
 
-// Bucket pairs: for every table and every key present in both P and Q, one
-// record (t, first sorted position in P, P rows, first sorted position in Q)
-// plus its Q rows and its first tile within its table.  Table t keeps its
-// records in its own region [t tcap, (t + 1) tcap) and its own counters (a
-// cache line each, CSTRIDE words apart, so the tables' atomics do not
-// contend): counters[t CSTRIDE] = records << TILE_BITS | tiles (one packed
-// atomic numbers the records, so first tiles increase with the record), and
-// counters[t CSTRIDE + 1] = pair evaluations.
-constexpr int CSTRIDE = 16;
-struct BucketPairs {
-    uint4 *head;          // {t, p0, np, q0}
-    uint32_t *nq;
-    unsigned long long *tile0;
-    unsigned long long *counters;   // L * CSTRIDE words
-    uint32_t tcap;        // records per table region
+// The buckets P and Q share, as records in key order within each table,
+// tables in order: record r is table t[r] and pq[r] = {p0, np, q0, nq}: P's
+// sorted positions [p0, p0 + np) and Q's [q0, q0 + nq) of that table
+// (positions within the table's segment).
+struct Records {
+    uint32_t *t;
+    uint4 *pq;
 };
 
-hipError_t launch_bucket_pairs(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
-                               uint32_t n_q, uint32_t L, const BucketPairs &bp, hipStream_t s);
+// Per row a 16-byte fingerprint of its keys in the first min(L, 16) tables
+// (byte t: 8 bits of a multiplicative hash of keys[t n + row]), for the
+// bucket join's first-table rule.
+hipError_t launch_fingerprints(const uint64_t *keys, uint32_t n, uint32_t L, uint4 *fp,
+                               hipStream_t s);
+
+// Marks, for every table t and sorted position p of P that starts a bucket
+// whose key Q also has, flag[t n_p + p] = 1 (else 0) with the bucket's sizes
+// and Q's first position in f_np / f_q0 / f_nq at that index; adds the
+// bucket pairs' pair evaluations (sum of np nq) to *n_cand.
+hipError_t launch_bucket_find(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
+                              uint32_t n_q, uint32_t L, uint32_t *flag, uint32_t *f_np,
+                              uint32_t *f_q0, uint32_t *f_nq, unsigned long long *n_cand,
+                              hipStream_t s);
+// Writes the marked positions as records (rec_off: exclusive scan of flag).
+hipError_t launch_bucket_write(uint32_t n_p, uint32_t L, const uint32_t *flag,
+                               const uint32_t *f_np, const uint32_t *f_q0, const uint32_t *f_nq,
+                               const unsigned long long *rec_off, const Records &rec,
+                               hipStream_t s);
+
+// Tiles.  The records are cut into chunks of PACK_CHUNK; within a chunk,
+// consecutive records that each fit one tile (np, nq <= TILE) are packed
+// greedily into groups of at most TILE P rows and TILE Q rows, one tile per
+// group, and every other record is tiled alone by ceil(np / TILE) x
+// ceil(nq / TILE) tiles.  A descriptor is (first record, number of records:
+// 0 for a record tiled alone, with the record's table and rows copied into
+// it, else the group's size) and its first tile.
+// count pass (write = false): per chunk the number of descriptors and of
+// tiles (chunk_desc, chunk_tiles; *overflow set when a chunk's tiles do not
+// fit 32 bits); write pass: the descriptors at desc_off[chunk] with tiles
+// numbered from tile_off[chunk].
+constexpr uint32_t PACK_CHUNK = 256;
+struct Descs {
+    uint4 *head;                  // {first record, count, table (count 0), 0}
+    uint4 *pq;                    // count 0: the record's {p0, np, q0, nq}
+    unsigned long long *tile;     // first tile
+};
+hipError_t launch_pack(const Records &rec, uint32_t n_rec, bool write, uint32_t *chunk_desc,
+                       uint32_t *chunk_tiles, const unsigned long long *desc_off,
+                       const unsigned long long *tile_off, const Descs &desc,
+                       unsigned long long *overflow, hipStream_t s);
 
 struct JoinArgs {
     Rows P, Q;
     uint32_t L;
     const uint32_t *perm_p, *perm_q;      // L x n sorted-position -> row
     const uint64_t *keys_p, *keys_q;      // L x n row -> key (first-table rule)
-    const uint4 *head;
-    const uint32_t *nq;
-    const unsigned long long *tile0;
-    uint32_t tcap;                        // records per table region
+    const uint4 *fp_p, *fp_q;             // per row: launch_fingerprints
+    Records rec;
+    Descs desc;
+    uint32_t n_desc;
     uint64_t n_tiles;
-    uint64_t tbase[65];                   // first tile of each table (tbase[L] = n_tiles)
-    uint32_t nrec[64];                    // records of each table
     float thr_f;                          // as sjk::JoinArgs
     int32_t thr_i;
     const void *norm_p, *norm_q;

@@ -540,40 +540,151 @@ __device__ __forceinline__ uint32_t lower_bound(const uint64_t *s, uint32_t lo, 
     return lo;
 }
 
-// One thread per (sorted position of P, table): the first position of each P
-// bucket looks its key up in Q's sorted keys and, when Q has it, appends the
-// bucket pair.
-__global__ void __launch_bounds__(256) bucket_pairs_kernel(const uint64_t *sorted_p,
-                                                           uint32_t n_p,
-                                                           const uint64_t *sorted_q,
-                                                           uint32_t n_q, BucketPairs bp)
+// Position after the run of `key` that starts at p - 1 (keys ascending):
+// doubling steps, then a binary search in the last step.
+__device__ __forceinline__ uint32_t run_end(const uint64_t *s, uint32_t p, uint32_t n, uint64_t key)
 {
-    const uint32_t p = blockIdx.x * 256 + threadIdx.x;
-    const uint32_t t = blockIdx.y;
-    if (p >= n_p)
-        return;
+    uint32_t lo = p, step = 1;
+    while (lo + step <= n && s[lo + step - 1] == key) {
+        lo += step;
+        step *= 2;
+    }
+    return upper_bound(s, lo, min(lo + step, n), key);
+}
+
+// One thread per (sorted position of P, table): a position that starts a P
+// bucket looks its key up in Q's sorted keys (within the range of Q keys the
+// block's first and last keys bound, found once per block) and, when Q has
+// it, marks the position with the bucket's sizes.
+__global__ void __launch_bounds__(256) bucket_find_kernel(const uint64_t *sorted_p, uint32_t n_p,
+                                                          const uint64_t *sorted_q, uint32_t n_q,
+                                                          uint32_t *flag, uint32_t *f_np,
+                                                          uint32_t *f_q0, uint32_t *f_nq,
+                                                          unsigned long long *n_cand)
+{
+    __shared__ uint32_t s_qa, s_qb;
+    __shared__ unsigned long long s_cand[4];
+    const uint32_t t = blockIdx.y, tid = threadIdx.x;
+    const uint32_t pf = blockIdx.x * 256, p = pf + tid;
     const uint64_t *sp = sorted_p + (size_t)t * n_p;
     const uint64_t *sq = sorted_q + (size_t)t * n_q;
-    const uint64_t key = sp[p];
-    if (p > 0 && sp[p - 1] == key)
+    if (tid == 0)
+        s_qa = lower_bound(sq, 0, n_q, sp[pf]);
+    if (tid == 64)
+        s_qb = upper_bound(sq, 0, n_q, sp[min(pf + 255, n_p - 1)]);
+    __syncthreads();
+    uint64_t cand = 0;
+    if (p < n_p) {
+        const size_t at = (size_t)t * n_p + p;
+        uint32_t fl = 0;
+        const uint64_t key = sp[p];
+        if (p == 0 || sp[p - 1] != key) {
+            const uint32_t q0 = lower_bound(sq, s_qa, s_qb, key);
+            const uint32_t qe = upper_bound(sq, q0, s_qb, key);
+            if (q0 < qe) {
+                const uint32_t np = run_end(sp, p + 1, n_p, key) - p;
+                fl = 1;
+                f_np[at] = np;
+                f_q0[at] = q0;
+                f_nq[at] = qe - q0;
+                cand = (uint64_t)np * (qe - q0);
+            }
+        }
+        flag[at] = fl;
+    }
+    // one atomic per block for the pair evaluations
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        cand += __shfl_xor(cand, o, 64);
+    if ((tid & 63) == 0)
+        s_cand[tid >> 6] = cand;
+    __syncthreads();
+    if (tid == 0) {
+        const unsigned long long c = s_cand[0] + s_cand[1] + s_cand[2] + s_cand[3];
+        if (c)
+            atomicAdd(n_cand, c);
+    }
+}
+
+__global__ void __launch_bounds__(256) bucket_write_kernel(uint32_t n_p, uint64_t total,
+                                                           const uint32_t *flag,
+                                                           const uint32_t *f_np,
+                                                           const uint32_t *f_q0,
+                                                           const uint32_t *f_nq,
+                                                           const unsigned long long *rec_off,
+                                                           Records rec)
+{
+    const uint64_t at = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (at >= total || !flag[at])
         return;
-    const uint32_t pe = upper_bound(sp, p + 1, n_p, key);
-    const uint32_t q0 = lower_bound(sq, 0, n_q, key);
-    const uint32_t qe = upper_bound(sq, q0, n_q, key);
-    if (q0 == qe)
+    const uint64_t r = rec_off[at];
+    rec.t[r] = (uint32_t)(at / n_p);
+    rec.pq[r] = make_uint4((uint32_t)(at % n_p), f_np[at], f_q0[at], f_nq[at]);
+}
+
+// One block per chunk of PACK_CHUNK records: the sizes go to LDS and the
+// first thread walks them in order (greedy packing, see sj_lsh.h).
+__global__ void __launch_bounds__(256) pack_kernel(Records rec, uint32_t n_rec, int write,
+                                                   uint32_t *chunk_desc, uint32_t *chunk_tiles,
+                                                   const unsigned long long *desc_off,
+                                                   const unsigned long long *tile_off, Descs desc,
+                                                   unsigned long long *overflow)
+{
+    static_assert(PACK_CHUNK == 256, "one record per thread");
+    __shared__ uint4 spq[PACK_CHUNK];
+    __shared__ uint32_t st[PACK_CHUNK];
+    const uint32_t c = blockIdx.x, r0 = c * PACK_CHUNK, tid = threadIdx.x;
+    const uint32_t rn = min((uint32_t)PACK_CHUNK, n_rec - r0);
+    if (tid < rn) {
+        spq[tid] = rec.pq[r0 + tid];
+        st[tid] = rec.t[r0 + tid];
+    }
+    __syncthreads();
+    if (tid != 0)
         return;
-    const uint32_t np = pe - p, nq = qe - q0;
-    const uint64_t tiles = (uint64_t)((np + TILE - 1) / TILE) * ((nq + TILE - 1) / TILE);
-    unsigned long long *cnt = bp.counters + (size_t)t * CSTRIDE;
-    const unsigned long long old =
-        atomicAdd(&cnt[0], (1ull << TILE_BITS) | (unsigned long long)tiles);
-    atomicAdd(&cnt[1], (unsigned long long)np * nq);
-    const uint64_t slot = old >> TILE_BITS;
-    if (slot < bp.tcap) {
-        const size_t at = (size_t)t * bp.tcap + slot;
-        bp.head[at] = make_uint4(t, p, np, q0);
-        bp.nq[at] = nq;
-        bp.tile0[at] = old & ((1ull << TILE_BITS) - 1);
+    const uint64_t dbase = write ? desc_off[c] : 0, tbase = write ? tile_off[c] : 0;
+    uint32_t nd = 0;
+    uint64_t nt = 0;
+    uint32_t gs = 0, gp = 0, gq = 0, gc = 0;   // the open group: first, rows, records
+    auto emit = [&](uint32_t first, uint32_t count, uint64_t tiles) {
+        if (write) {
+            desc.head[dbase + nd] = make_uint4(r0 + first, count, count ? 0u : st[first], 0u);
+            if (count == 0)
+                desc.pq[dbase + nd] = spq[first];
+            desc.tile[dbase + nd] = tbase + nt;
+        }
+        ++nd;
+        nt += tiles;
+    };
+    for (uint32_t i = 0; i < rn; ++i) {
+        const uint32_t np = spq[i].y, nq = spq[i].w;
+        if (np > TILE || nq > TILE) {
+            if (gc) {
+                emit(gs, gc, 1);
+                gc = 0;
+            }
+            emit(i, 0, (uint64_t)((np + TILE - 1) / TILE) * ((nq + TILE - 1) / TILE));
+            continue;
+        }
+        if (gc && (gp + np > TILE || gq + nq > TILE)) {
+            emit(gs, gc, 1);
+            gc = 0;
+        }
+        if (gc == 0) {
+            gs = i;
+            gp = gq = 0;
+        }
+        gp += np;
+        gq += nq;
+        ++gc;
+    }
+    if (gc)
+        emit(gs, gc, 1);
+    if (!write) {
+        chunk_desc[c] = nd;
+        chunk_tiles[c] = (uint32_t)min(nt, (uint64_t)0xffffffffu);
+        if (nt > 0xffffffffull)
+            atomicMax(overflow, 1ull);
     }
 }
 
@@ -597,13 +708,17 @@ __device__ __forceinline__ bool matches(typename sjk::Mma<DT>::val_t acc,
     }
 }
 
-// A workgroup of 4 waves takes a contiguous range of the TILE x TILE tiles of
-// the bucket pairs: the tile's rows of P and Q are gathered through the tables'
-// sorted permutations into LDS in chunks of 128 bytes of each row (16-byte
-// chunks, rows padded by one chunk), wave (wr, wc) multiplies its 64 x 64
-// quarter (2 x 2 blocks of 32 x 32: per k-step two A- and two B-fragments for
-// four MFMAs) over the chunk's k-steps, and the epilogue applies the exact
-// test, drops pairs that share a bucket in an earlier table (so every pair is
+// A workgroup of 4 waves takes a contiguous range of the tiles (see the
+// descriptors in sj_lsh.h): a tile of a record tiled alone holds up to TILE
+// of its P rows and TILE of its Q rows; a packed tile holds the P rows and
+// the Q rows of a group of records, each row tagged with its record's place
+// in the group, and only pairs with equal tags (the same bucket) are
+// candidates.  The rows are gathered through the tables' sorted permutations
+// into LDS in chunks of 128 bytes of each row (16-byte chunks, rows padded by
+// one chunk), wave (wr, wc) multiplies its 64 x 64 quarter (2 x 2 blocks of
+// 32 x 32: per k-step two A- and two B-fragments for four MFMAs) over the
+// chunk's k-steps, and the epilogue applies the exact test to the candidates,
+// drops pairs that share a bucket in an earlier table (so every pair is
 // reported once) and appends the rest with one atomic per wave and block.
 template <int DT, int MET>
 __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
@@ -616,69 +731,152 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
     __shared__ i32x4 sA[TILE * CS], sB[TILE * CS];
     __shared__ uint32_t sIP[TILE], sIQ[TILE];
     __shared__ V sNP[TILE], sNQ[TILE];
+    __shared__ uint8_t sGP[TILE], sGQ[TILE];                 // row's record in the group
+    __shared__ uint32_t sRT[TILE];                           // group record's table
+    // used only while a packed tile's row indices are gathered, before the
+    // rows themselves go to sA: the group's row prefix sums and its records'
+    // first positions
+    uint2 *const sR0 = (uint2 *)sA;
+    uint32_t *const sPS = (uint32_t *)(sR0 + TILE), *const sQS = sPS + (TILE + 1);
+    static_assert(2 * TILE + 2 * (TILE + 1) <= TILE * CS * 4, "group tables fit sA");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave >> 1, wc = wave & 1, half = lane >> 5, c32 = lane & 31;
     const uint32_t rb = g.P.row_bytes;   // == g.Q.row_bytes
     const uint32_t lc = tid & 7, lr = tid >> 3;   // load chunk; rows lr + 32 e
 
-    // a contiguous range of tiles per workgroup: one search for its first
-    // tile's bucket pair, then a walk (consecutive tiles of a pair share rows)
+    // a contiguous range of tiles per workgroup: one search for the
+    // descriptor of its first tile, then a walk
     const uint64_t per = (g.n_tiles + gridDim.x - 1) / gridDim.x;
     const uint64_t T0 = (uint64_t)blockIdx.x * per;
     const uint64_t T1 = min(T0 + per, g.n_tiles);
     if (T0 >= T1)
         return;   // the whole workgroup: no barrier is skipped by part of it
-    // the table of the first tile (tables without records have no tiles),
-    // then its record by binary search over the table's first tiles
-    uint32_t tab = 0;
-    while (tab + 1 < g.L && g.tbase[tab + 1] <= T0)
-        ++tab;
-    uint32_t slot = 0;
+    uint32_t dsc = 0;
     {
-        const uint64_t Tl = T0 - g.tbase[tab];
-        const unsigned long long *t0 = g.tile0 + (size_t)tab * g.tcap;
-        uint32_t hi = g.nrec[tab];
-        while (hi - slot > 1) {
-            const uint32_t mid = (slot + hi) >> 1;
-            if (t0[mid] <= Tl)
-                slot = mid;
+        uint32_t hi = g.n_desc;
+        while (hi - dsc > 1) {
+            const uint32_t mid = (dsc + hi) >> 1;
+            if (g.desc.tile[mid] <= T0)
+                dsc = mid;
             else
                 hi = mid;
         }
     }
-    uint64_t local = T0 - g.tbase[tab] - g.tile0[(size_t)tab * g.tcap + slot];
+    uint64_t local = T0 - g.desc.tile[dsc];
     for (uint64_t T = T0; T < T1; ++T) {
-        const size_t rec = (size_t)tab * g.tcap + slot;
-        const uint4 h = g.head[rec];
-        const uint32_t t = h.x, nq = g.nq[rec];
-        const uint32_t ntq = (nq + TILE - 1) / TILE;
-        const uint32_t ntp = (h.z + TILE - 1) / TILE;
-        const uint32_t tp = (uint32_t)(local / ntq), tq = (uint32_t)(local % ntq);
-        const uint32_t rows_p = min(h.z - tp * TILE, TILE), rows_q = min(nq - tq * TILE, TILE);
-        if (++local == (uint64_t)ntp * ntq) {   // the next tile starts the next record
-            local = 0;
-            if (++slot == g.nrec[tab]) {         // ... of the next table with records
-                slot = 0;
-                ++tab;
-                while (tab < g.L && g.nrec[tab] == 0)
-                    ++tab;
+        const uint4 hd = g.desc.head[dsc];
+        const uint32_t first = hd.x, ngrp = hd.y;
+        uint32_t rows_p, rows_q;
+        __syncthreads();   // the previous tile's reads of the LDS tables are done
+        if (ngrp == 0) {
+            // a record tiled alone: sub-tile (tp, tq) of its ntp x ntq tiles
+            const uint32_t t = hd.z;
+            const uint4 rq = g.desc.pq[dsc];
+            const uint32_t np = rq.y, nq = rq.w;
+            const uint32_t ntq = (nq + TILE - 1) / TILE, ntp = (np + TILE - 1) / TILE;
+            const uint32_t tp = (uint32_t)(local / ntq), tq = (uint32_t)(local % ntq);
+            rows_p = min(np - tp * TILE, TILE);
+            rows_q = min(nq - tq * TILE, TILE);
+            if (++local == (uint64_t)ntp * ntq) {
+                local = 0;
+                ++dsc;
             }
-        }
-
-        __syncthreads();   // the previous tile's reads of sIP/sIQ/sA/sB are done
-        if (tid < (int)TILE) {
-            const bool okp = (uint32_t)tid < rows_p;
-            const uint32_t i = okp ? g.perm_p[(size_t)t * g.P.n + h.y + tp * TILE + tid] : 0u;
-            sIP[tid] = i;
-            const bool okq = (uint32_t)tid < rows_q;
-            const uint32_t j = okq ? g.perm_q[(size_t)t * g.Q.n + h.w + tq * TILE + tid] : 0u;
-            sIQ[tid] = j;
-            if constexpr (MET == MET_L2) {
-                sNP[tid] = okp ? ((const V *)g.norm_p)[i] : V(0);
-                sNQ[tid] = okq ? ((const V *)g.norm_q)[j] : V(0);
+            if (tid < (int)TILE) {
+                const bool okp = (uint32_t)tid < rows_p;
+                sIP[tid] = okp ? g.perm_p[(size_t)t * g.P.n + rq.x + tp * TILE + tid] : 0u;
+                const bool okq = (uint32_t)tid < rows_q;
+                sIQ[tid] = okq ? g.perm_q[(size_t)t * g.Q.n + rq.z + tq * TILE + tid] : 0u;
+                sGP[tid] = 0;
+                sGQ[tid] = 0;
+                if (tid == 0)
+                    sRT[0] = t;
+            }
+        } else {
+            // a packed group of ngrp records, one tile: the records' row
+            // counts, prefix-summed by the first two waves (ngrp <= TILE)
+            ++dsc;
+            local = 0;
+            uint32_t np = 0, nq = 0;
+            if (tid < (int)ngrp) {
+                const uint4 rq = g.rec.pq[first + tid];
+                np = rq.y;
+                nq = rq.w;
+                sRT[tid] = g.rec.t[first + tid];
+                sR0[tid] = make_uint2(rq.x, rq.z);
+            }
+            uint32_t ip = np, iq = nq;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t up = __shfl_up(ip, o, 64), uq = __shfl_up(iq, o, 64);
+                if (lane >= o) {
+                    ip += up;
+                    iq += uq;
+                }
+            }
+            if (tid == 63) {
+                sPS[TILE] = ip;   // first wave's totals, for the second wave
+                sQS[TILE] = iq;
+            }
+            __syncthreads();
+            if (tid >= 64 && tid < (int)TILE) {
+                ip += sPS[TILE];
+                iq += sQS[TILE];
+            }
+            __syncthreads();
+            if (tid < (int)TILE) {
+                sPS[tid + 1] = ip;   // inclusive sums: row prefix of record tid + 1
+                sQS[tid + 1] = iq;
+            }
+            if (tid == 0)
+                sPS[0] = sQS[0] = 0;
+            __syncthreads();
+            rows_p = sPS[ngrp];
+            rows_q = sQS[ngrp];
+            if (tid < (int)TILE) {
+                // this thread's P row and Q row: the record holding it (the last
+                // prefix at or below it), then its sorted position
+                uint32_t gi = 0, gj = 0, lo, hi;
+                if ((uint32_t)tid < rows_p) {
+                    lo = 0, hi = ngrp;
+                    while (hi - lo > 1) {
+                        const uint32_t mid = (lo + hi) >> 1;
+                        if (sPS[mid] <= (uint32_t)tid)
+                            lo = mid;
+                        else
+                            hi = mid;
+                    }
+                    gi = lo;
+                    sIP[tid] = g.perm_p[(size_t)sRT[gi] * g.P.n + sR0[gi].x + (tid - sPS[gi])];
+                } else {
+                    sIP[tid] = 0u;
+                }
+                if ((uint32_t)tid < rows_q) {
+                    lo = 0, hi = ngrp;
+                    while (hi - lo > 1) {
+                        const uint32_t mid = (lo + hi) >> 1;
+                        if (sQS[mid] <= (uint32_t)tid)
+                            lo = mid;
+                        else
+                            hi = mid;
+                    }
+                    gj = lo;
+                    sIQ[tid] = g.perm_q[(size_t)sRT[gj] * g.Q.n + sR0[gj].y + (tid - sQS[gj])];
+                } else {
+                    sIQ[tid] = 0u;
+                }
+                sGP[tid] = (uint8_t)gi;
+                sGQ[tid] = (uint8_t)gj;
             }
         }
         __syncthreads();
+        if constexpr (MET == MET_L2) {
+            if (tid < (int)TILE) {
+                sNP[tid] = (uint32_t)tid < rows_p ? ((const V *)g.norm_p)[sIP[tid]] : V(0);
+                sNQ[tid] = (uint32_t)tid < rows_q ? ((const V *)g.norm_q)[sIQ[tid]] : V(0);
+            }
+            __syncthreads();
+        }
+        const bool packed = ngrp != 0;
 
         acc_t acc[2][2];
 #pragma unroll
@@ -727,13 +925,18 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
                 }
         }
 
-        // epilogue, block (a, b): result register r of this lane is (row
-        // wr*64 + 32a + 8(r/4) + 4 half + r%4, column wc*64 + 32b + c32)
+        // epilogue.  Result register r of block (a, b) of this lane is (row
+        // wr*64 + 32a + 8(r/4) + 4 half + r%4, column wc*64 + 32b + c32).
+        // First the exact test of every result (in a packed tile also the
+        // bucket tags of its matches); then, only in a wave with a match, the
+        // first-table rule from the rows' key fingerprints, which the wave
+        // stages in the operand LDS the MFMAs no longer read.
+        uint32_t mk[2][2];
+        bool any = false;
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const uint32_t jl = wc * 64 + 32 * b + c32;
             const bool jok = jl < rows_q;
-            const uint32_t j = sIQ[jl];
             const V ny = MET == MET_L2 ? sNQ[jl] : V(0);
 #pragma unroll
             for (int a = 0; a < 2; ++a) {
@@ -746,48 +949,147 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
                     const bool ok = jok && il < rows_p && matches<DT, MET>(acc[a][b][r], nx, ny, g);
                     m |= ok ? (1u << r) : 0u;
                 }
+                mk[a][b] = m;
+                any |= m != 0;
+            }
+        }
+        __syncthreads();   // every wave's MFMAs are done with sA and sB
+        if (__ballot(any) == 0)
+            continue;
+        uint4 *const wf = (uint4 *)sA + wave * 128;   // fingerprints: 64 P rows, 64 Q rows
+        if (g.L > 1) {
+            const uint32_t pr = wr * 64 + lane, qr = wc * 64 + lane;
+            const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+            wf[lane] = pr < rows_p ? g.fp_p[sIP[pr]] : z4;
+            wf[64 + lane] = qr < rows_q ? g.fp_q[sIQ[qr]] : z4;
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        }
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const uint32_t jl = wc * 64 + 32 * b + c32;
+            const uint32_t j = sIQ[jl];
+            const uint32_t gq = sGQ[jl];
+            const uint32_t t = sRT[gq];   // the pair's table (its bucket's)
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                const uint32_t ib = wr * 64 + 32 * a + 4 * half;
+                uint32_t m = mk[a][b];
                 if (__ballot(m != 0) == 0)
                     continue;
-                if (t > 0 && m != 0) {
+                if (packed) {
+                    // candidates of a packed tile: rows of the same bucket
                     uint32_t mm = m;
                     while (mm) {
                         const int r = __builtin_ctz(mm);
                         mm &= mm - 1;
-                        const uint32_t i = sIP[ib + 8 * (r >> 2) + (r & 3)];
-                        for (uint32_t t2 = 0; t2 < t; ++t2)
-                            if (g.keys_p[(size_t)t2 * g.P.n + i] ==
-                                g.keys_q[(size_t)t2 * g.Q.n + j]) {
-                                m &= ~(1u << r);
-                                break;
-                            }
+                        if (sGP[ib + 8 * (r >> 2) + (r & 3)] != gq)
+                            m &= ~(1u << r);
                     }
                 }
-                const uint32_t cnt = (uint32_t)__builtin_popcount(m);
-                uint32_t tot = 0, pre = 0;
+                if (t > 0 && m != 0) {
+                    // the first-table rule: drop the pair when its keys agree
+                    // in an earlier table.  Tables below 16 by fingerprint
+                    // (a byte per table; equal keys give equal bytes), each
+                    // equal byte confirmed with the keys; later tables by
+                    // their keys, 8 tables per round of independent loads.
+                    const uint4 fj = wf[64 + (jl - wc * 64)];
+                    const uint32_t tf = t < 16 ? t : 16;
+                    uint32_t mm = m;
+                    while (mm) {
+                        const int r = __builtin_ctz(mm);
+                        mm &= mm - 1;
+                        const uint32_t il = ib + 8 * (r >> 2) + (r & 3);
+                        const uint32_t i = sIP[il];
+                        const uint4 fi = wf[il - wr * 64];
+                        const uint32_t xw[4] = {fi.x ^ fj.x, fi.y ^ fj.y, fi.z ^ fj.z, fi.w ^ fj.w};
+                        uint32_t eq = 0;   // bit t2: byte t2 of the fingerprints equal
 #pragma unroll
-                for (int bit = 0; bit < 5; ++bit) {
-                    const uint64_t bits = __ballot((cnt >> bit) & 1);
-                    tot += (uint32_t)__popcll(bits) << bit;
-                    pre += sjk::lanes_below(bits) << bit;
-                }
-                if (tot != 0) {
-                    unsigned long long base = 0;
-                    if (lane == 0)
-                        base = atomicAdd(g.counter, (unsigned long long)tot);
-                    uint64_t pos = sjk::first_lane_u64(base) + pre;
-                    while (m) {
-                        const int r = __builtin_ctz(m);
-                        m &= m - 1;
-                        if (pos < g.cap) {
-                            const uint32_t i = sIP[ib + 8 * (r >> 2) + (r & 3)];
-                            ((sjk::global_pair *)g.pairs)[pos] = sjk::pack_pair(i, j);
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t x = xw[q];
+                            const uint32_t y = ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
+                            eq |= (((y >> 7) & 1u) | ((y >> 14) & 2u) | ((y >> 21) & 4u) |
+                                   ((y >> 28) & 8u)) << (4 * q);
                         }
-                        ++pos;
+                        eq &= tf >= 16 ? 0xffffu : (1u << tf) - 1u;
+                        bool same = false;
+                        while (eq && !same) {
+                            const uint32_t t2 = __builtin_ctz(eq);
+                            eq &= eq - 1;
+                            same = g.keys_p[(size_t)t2 * g.P.n + i] ==
+                                   g.keys_q[(size_t)t2 * g.Q.n + j];
+                        }
+                        for (uint32_t t2 = 16; t2 < t && !same; t2 += 8) {
+#pragma unroll
+                            for (uint32_t u = 0; u < 8; ++u) {
+                                const uint32_t tt = t2 + u < t ? t2 + u : t - 1;
+                                same |= g.keys_p[(size_t)tt * g.P.n + i] ==
+                                        g.keys_q[(size_t)tt * g.Q.n + j];
+                            }
+                        }
+                        if (same)
+                            m &= ~(1u << r);
                     }
+                }
+                mk[a][b] = m;
+            }
+        }
+        // one slot reservation for the wave's matches of the whole tile: the
+        // lanes' counts (at most 64) give the wave's total and each lane's
+        // prefix through seven ballots, and each lane writes its pairs in
+        // (block, register) order
+        const uint32_t cnt = (uint32_t)(__builtin_popcount(mk[0][0]) + __builtin_popcount(mk[1][0]) +
+                                        __builtin_popcount(mk[0][1]) + __builtin_popcount(mk[1][1]));
+        uint32_t tot = 0, pre = 0;
+#pragma unroll
+        for (int bit = 0; bit < 7; ++bit) {
+            const uint64_t bits = __ballot((cnt >> bit) & 1);
+            tot += (uint32_t)__popcll(bits) << bit;
+            pre += sjk::lanes_below(bits) << bit;
+        }
+        if (tot == 0)
+            continue;
+        unsigned long long base = 0;
+        if (lane == 0)
+            base = atomicAdd(g.counter, (unsigned long long)tot);
+        uint64_t pos = sjk::first_lane_u64(base) + pre;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const uint32_t j = sIQ[wc * 64 + 32 * b + c32];
+#pragma unroll
+            for (int a = 0; a < 2; ++a) {
+                const uint32_t ib = wr * 64 + 32 * a + 4 * half;
+                uint32_t m = mk[a][b];
+                while (m) {
+                    const int r = __builtin_ctz(m);
+                    m &= m - 1;
+                    if (pos < g.cap) {
+                        const uint32_t i = sIP[ib + 8 * (r >> 2) + (r & 3)];
+                        ((sjk::global_pair *)g.pairs)[pos] = sjk::pack_pair(i, j);
+                    }
+                    ++pos;
                 }
             }
         }
     }
+}
+
+// Fingerprints of the keys of the first min(L, 16) tables: byte t of fp[row]
+// is the top byte of keys[t n + row] times an odd constant, so rows with equal
+// keys in table t have equal bytes t (and rows with different keys rarely do).
+__global__ void __launch_bounds__(256) fingerprint_kernel(const uint64_t *keys, uint32_t n,
+                                                          uint32_t L, uint4 *fp)
+{
+    const uint32_t row = blockIdx.x * 256 + threadIdx.x;
+    if (row >= n)
+        return;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    const uint32_t tl = L < 16 ? L : 16;
+    for (uint32_t t = 0; t < tl; ++t) {
+        const uint32_t byte = (uint32_t)((keys[(size_t)t * n + row] * 0x9E3779B97F4A7C15ull) >> 56);
+        w[t >> 2] |= byte << (8 * (t & 3));
+    }
+    fp[row] = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 template <int DT>
@@ -953,13 +1255,50 @@ hipError_t launch_widen(int dtype, const int8_t *A, uint32_t n_fn, uint32_t d, v
     return hipGetLastError();
 }
 
-hipError_t launch_bucket_pairs(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
-                               uint32_t n_q, uint32_t L, const BucketPairs &bp, hipStream_t s)
+hipError_t launch_fingerprints(const uint64_t *keys, uint32_t n, uint32_t L, uint4 *fp,
+                               hipStream_t s)
+{
+    if (n == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(fingerprint_kernel, dim3((n + 255) / 256), dim3(256), 0, s, keys, n, L, fp);
+    return hipGetLastError();
+}
+
+hipError_t launch_bucket_find(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
+                              uint32_t n_q, uint32_t L, uint32_t *flag, uint32_t *f_np,
+                              uint32_t *f_q0, uint32_t *f_nq, unsigned long long *n_cand,
+                              hipStream_t s)
 {
     if (n_p == 0 || n_q == 0 || L == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(bucket_pairs_kernel, dim3((n_p + 255) / 256, L), dim3(256), 0, s,
-                       sorted_p, n_p, sorted_q, n_q, bp);
+    hipLaunchKernelGGL(bucket_find_kernel, dim3((n_p + 255) / 256, L), dim3(256), 0, s, sorted_p,
+                       n_p, sorted_q, n_q, flag, f_np, f_q0, f_nq, n_cand);
+    return hipGetLastError();
+}
+
+hipError_t launch_bucket_write(uint32_t n_p, uint32_t L, const uint32_t *flag,
+                               const uint32_t *f_np, const uint32_t *f_q0, const uint32_t *f_nq,
+                               const unsigned long long *rec_off, const Records &rec,
+                               hipStream_t s)
+{
+    const uint64_t total = (uint64_t)n_p * L;
+    if (total == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(bucket_write_kernel, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0,
+                       s, n_p, total, flag, f_np, f_q0, f_nq, rec_off, rec);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack(const Records &rec, uint32_t n_rec, bool write, uint32_t *chunk_desc,
+                       uint32_t *chunk_tiles, const unsigned long long *desc_off,
+                       const unsigned long long *tile_off, const Descs &desc,
+                       unsigned long long *overflow, hipStream_t s)
+{
+    if (n_rec == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(pack_kernel, dim3((n_rec + PACK_CHUNK - 1) / PACK_CHUNK), dim3(256), 0, s,
+                       rec, n_rec, write ? 1 : 0, chunk_desc, chunk_tiles, desc_off, tile_off,
+                       desc, overflow);
     return hipGetLastError();
 }
 

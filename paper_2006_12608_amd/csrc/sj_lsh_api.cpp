@@ -16,9 +16,9 @@ using namespace sjh;
 
 namespace {
 
-// Tables and records are addressed with 32-bit positions and the packed
-// bucket-pair counter keeps 26 bits of record number.
-const uint64_t kMaxTableRows = (uint64_t)1 << (64 - sjl::TILE_BITS);
+// Tables and records are addressed with 32-bit positions.
+const uint64_t kMaxTableRows = (uint64_t)1 << 32;
+const uint32_t kMaxTables = 256;
 
 }  // namespace
 
@@ -41,8 +41,8 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
         return fail(SJ_E_INVAL, "unknown metric %d", metric);
     if (std::isnan(thr))
         return fail(SJ_E_INVAL, "threshold is NaN");
-    if (L < 1 || L > 64)
-        return fail(SJ_E_INVAL, "L = %u tables: 1 <= L <= 64", L);
+    if (L < 1 || L > kMaxTables)
+        return fail(SJ_E_INVAL, "L = %u tables: 1 <= L <= %u", L, kMaxTables);
     if (k > 64)
         return fail(SJ_E_INVAL, "k = %u functions per table: k <= 64", k);
     if (w < 0)
@@ -51,7 +51,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
         return fail(SJ_E_UNSUPPORTED, "d = %u is above the limit for this dtype", d);
     const uint64_t n_max = n_p > n_q ? n_p : n_q;
     if ((uint64_t)L * n_max >= kMaxTableRows)
-        return fail(SJ_E_UNSUPPORTED, "L * max(n_p, n_q) = %llu is not below 2^26",
+        return fail(SJ_E_UNSUPPORTED, "L * max(n_p, n_q) = %llu is not below 2^32",
                     (unsigned long long)L * n_max);
     const size_t row_bytes = (size_t)d * esize(dtype);
     int st;
@@ -83,27 +83,19 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const bool self = P == Q && n_p == n_q;
     const bool l2 = metric == SJ_L2;
     const uint32_t bits = sjl::key_bits(k, w);
-    // records: a region of min(n_p, n_q) per table (a table has at most that
-    // many keys shared by P and Q)
-    const uint64_t tcap = n_p < n_q ? n_p : n_q;
-    const uint64_t bp_cap = (uint64_t)L * tcap;
-    // a table's tiles, sum over its buckets of ceil(p_b / T) ceil(q_b / T),
-    // are at most n_p n_q / T^2 + (n_p + n_q) / T + min(n_p, n_q): they must
-    // fit the packed counter's low TILE_BITS bits
-    {
-        const double T = sjl::TILE;
-        const double most = (double)n_p * n_q / (T * T) + ((double)n_p + n_q) / T + (double)tcap;
-        if (most >= (double)(1ull << sjl::TILE_BITS))
-            return fail(SJ_E_UNSUPPORTED, "n_p = %u, n_q = %u: a table could hold more than 2^%d "
-                        "candidate tiles", n_p, n_q, sjl::TILE_BITS);
-    }
+    // records: at most min(n_p, n_q) per table (a table has at most that
+    // many keys shared by P and Q); packing chunks of them
+    const uint64_t bp_cap = (uint64_t)L * (n_p < n_q ? n_p : n_q);
+    const uint64_t chunk_cap = (bp_cap + sjl::PACK_CHUNK - 1) / sjl::PACK_CHUNK;
+    const uint64_t pos_p = (uint64_t)L * n_p;   // sorted positions of P, all tables
     // one sort workspace, used by P and then by Q
     const size_t temp_bytes = sjl::sort_temp_bytes(n_max, L);
     const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
     // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
-    //          [sorted Q][perm P][perm Q][bucket pairs][counters][sort temp]
-    //          [widened projections]
+    //          [sorted Q][perm P][perm Q][bucket marks, sizes and numbers]
+    //          [records][chunk counts and offsets][descriptors][scan partials]
+    //          [counters][sort temp][widened projections]
     size_t need = 0;
     auto take = [&](size_t bytes) {
         const size_t at = need;
@@ -120,11 +112,26 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_sq = self ? off_sp : take((size_t)L * n_q * 8);
     const size_t off_pp = take((size_t)L * n_p * 4);
     const size_t off_pq = self ? off_pp : take((size_t)L * n_q * 4);
-    const size_t off_head = take((size_t)bp_cap * 16);
-    const size_t off_bnq = take((size_t)bp_cap * 4);
-    const size_t off_t0 = take((size_t)bp_cap * 8);
-    const size_t off_cnt = take(6 * 8);
-    const size_t off_tcnt = take((size_t)L * sjl::CSTRIDE * 8);
+    const size_t off_fpp = take((size_t)n_p * 16);
+    const size_t off_fpq = self ? off_fpp : take((size_t)n_q * 16);
+    const size_t off_flag = take(pos_p * 4);
+    const size_t off_fnp = take(pos_p * 4);
+    const size_t off_fq0 = take(pos_p * 4);
+    const size_t off_fnq = take(pos_p * 4);
+    const size_t off_roff = take(pos_p * 8);
+    const size_t off_rect = take(bp_cap * 4);
+    const size_t off_recpq = take(bp_cap * 16);
+    const size_t off_cdesc = take(chunk_cap * 4);
+    const size_t off_ctile = take(chunk_cap * 4);
+    const size_t off_doff = take(chunk_cap * 8);
+    const size_t off_toff = take(chunk_cap * 8);
+    const size_t off_dhead = take(bp_cap * 16);
+    const size_t off_dpq = take(bp_cap * 16);
+    const size_t off_dtile = take(bp_cap * 8);
+    const size_t off_part = take(sjk::scan_partials_size(pos_p > chunk_cap ? pos_p : chunk_cap) * 8);
+    // counters: [0] pair evaluations, [1] records, [2] descriptors, [3] [4]
+    // the hash's fix queues, [5] tiles, [6] tile overflow
+    const size_t off_cnt = take(8 * 8);
     const size_t off_temp = take(temp_bytes);
     const size_t off_aw = take(a_bytes);
     // keys on the matrix cores where they apply
@@ -139,9 +146,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     sjl::Rows rp{aligned ? (const uint8_t *)P : scr + off_rp, n_p, (uint32_t)krow};
     sjl::Rows rq{aligned ? (const uint8_t *)Q : scr + off_rq, n_q, (uint32_t)krow};
     unsigned long long *cnt = (unsigned long long *)(scr + off_cnt);
-    SJ_HIP(hipMemsetAsync(cnt, 0, 6 * 8, s));
-    unsigned long long *tcnt = (unsigned long long *)(scr + off_tcnt);
-    SJ_HIP(hipMemsetAsync(tcnt, 0, (size_t)L * sjl::CSTRIDE * 8, s));
+    SJ_HIP(hipMemsetAsync(cnt, 0, 8 * 8, s));
     SJ_HIP(hipMemsetAsync(c->d_small, 0, sizeof(unsigned long long), s));
     SJ_HIP(hipEventRecord(c->ev[0], s));
     if (!aligned) {
@@ -169,31 +174,56 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
         if (!self)
             SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, keys_q, s));
     }
+    uint4 *fp_p = (uint4 *)(scr + off_fpp), *fp_q = (uint4 *)(scr + off_fpq);
+    if (L > 1) {
+        SJ_HIP(sjl::launch_fingerprints(keys_p, n_p, L, fp_p, s));
+        if (!self)
+            SJ_HIP(sjl::launch_fingerprints(keys_q, n_q, L, fp_q, s));
+    }
     SJ_HIP(hipEventRecord(c->ev[1], s));
     uint64_t *sorted_p = (uint64_t *)(scr + off_sp), *sorted_q = (uint64_t *)(scr + off_sq);
     uint32_t *perm_p = (uint32_t *)(scr + off_pp), *perm_q = (uint32_t *)(scr + off_pq);
     SJ_HIP(sjl::sort_tables(keys_p, sorted_p, perm_p, n_p, L, bits, scr + off_temp, s));
     if (!self)
         SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, n_q, L, bits, scr + off_temp, s));
-    sjl::BucketPairs bp{(uint4 *)(scr + off_head), (uint32_t *)(scr + off_bnq),
-                        (unsigned long long *)(scr + off_t0), tcnt, (uint32_t)tcap};
-    SJ_HIP(sjl::launch_bucket_pairs(sorted_p, n_p, sorted_q, n_q, L, bp, s));
-    SJ_HIP(hipEventRecord(c->ev[2], s));
-    std::vector<unsigned long long> hc((size_t)L * sjl::CSTRIDE);
-    SJ_HIP(hipMemcpyAsync(hc.data(), tcnt, hc.size() * 8, hipMemcpyDeviceToHost, s));
+    // the buckets P and Q share, as records in key order, then their tiles
+    uint32_t *flag = (uint32_t *)(scr + off_flag);
+    SJ_HIP(sjl::launch_bucket_find(sorted_p, n_p, sorted_q, n_q, L, flag, (uint32_t *)(scr + off_fnp),
+                                   (uint32_t *)(scr + off_fq0), (uint32_t *)(scr + off_fnq), cnt,
+                                   s));
+    unsigned long long *part = (unsigned long long *)(scr + off_part);
+    SJ_HIP(sjk::launch_scan(flag, pos_p, (unsigned long long *)(scr + off_roff), part, cnt + 1, s));
+    const sjl::Records rec{(uint32_t *)(scr + off_rect), (uint4 *)(scr + off_recpq)};
+    SJ_HIP(sjl::launch_bucket_write(n_p, L, flag, (const uint32_t *)(scr + off_fnp),
+                                    (const uint32_t *)(scr + off_fq0),
+                                    (const uint32_t *)(scr + off_fnq),
+                                    (const unsigned long long *)(scr + off_roff), rec, s));
+    SJ_HIP(hipMemcpyAsync(c->h_small, cnt + 1, 8, hipMemcpyDeviceToHost, s));
     SJ_HIP(hipStreamSynchronize(s));
+    const uint64_t n_rec = c->h_small[0];
+    const uint64_t n_chunk = (n_rec + sjl::PACK_CHUNK - 1) / sjl::PACK_CHUNK;
+    const sjl::Descs desc{(uint4 *)(scr + off_dhead), (uint4 *)(scr + off_dpq),
+                          (unsigned long long *)(scr + off_dtile)};
+    uint32_t *cdesc = (uint32_t *)(scr + off_cdesc), *ctile = (uint32_t *)(scr + off_ctile);
+    unsigned long long *doff = (unsigned long long *)(scr + off_doff);
+    unsigned long long *toff = (unsigned long long *)(scr + off_toff);
+    SJ_HIP(sjl::launch_pack(rec, (uint32_t)n_rec, false, cdesc, ctile, nullptr, nullptr, desc,
+                            cnt + 6, s));
+    if (n_chunk) {
+        SJ_HIP(sjk::launch_scan(cdesc, n_chunk, doff, part, cnt + 2, s));
+        SJ_HIP(sjk::launch_scan(ctile, n_chunk, toff, part, cnt + 5, s));
+    }
+    SJ_HIP(sjl::launch_pack(rec, (uint32_t)n_rec, true, cdesc, ctile, doff, toff, desc, cnt + 6,
+                            s));
+    SJ_HIP(hipEventRecord(c->ev[2], s));
+    unsigned long long hc[8];
+    SJ_HIP(hipMemcpyAsync(hc, cnt, sizeof hc, hipMemcpyDeviceToHost, s));
+    SJ_HIP(hipStreamSynchronize(s));
+    if (hc[6])
+        return fail(SJ_E_UNSUPPORTED, "a chunk of buckets needs more than 2^32 tiles");
 
     sjl::JoinArgs g = {};
-    uint64_t n_tiles = 0, cand = 0;
-    for (uint32_t t = 0; t < L; ++t) {
-        const unsigned long long packed = hc[(size_t)t * sjl::CSTRIDE];
-        g.tbase[t] = n_tiles;
-        g.nrec[t] = (uint32_t)(packed >> sjl::TILE_BITS);
-        n_tiles += packed & ((1ull << sjl::TILE_BITS) - 1);
-        cand += hc[(size_t)t * sjl::CSTRIDE + 1];
-    }
-    g.tbase[L] = n_tiles;
-
+    const uint64_t n_tiles = hc[5], cand = hc[0];
     g.P = rp;
     g.Q = rq;
     g.L = L;
@@ -201,10 +231,11 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     g.perm_q = perm_q;
     g.keys_p = keys_p;
     g.keys_q = keys_q;
-    g.head = bp.head;
-    g.nq = bp.nq;
-    g.tile0 = bp.tile0;
-    g.tcap = (uint32_t)tcap;
+    g.fp_p = fp_p;
+    g.fp_q = fp_q;
+    g.rec = rec;
+    g.desc = desc;
+    g.n_desc = (uint32_t)hc[2];
     g.n_tiles = n_tiles;
     if (dtype == SJ_I8) {
         if (!l2) {

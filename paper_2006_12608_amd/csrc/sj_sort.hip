@@ -22,7 +22,7 @@
 namespace sjl {
 
 constexpr int SORT_T = 256;                    // threads per block (4 waves)
-constexpr int SORT_IPT = 16;                   // entries per thread
+constexpr int SORT_IPT = 8;                    // entries per thread
 constexpr int SORT_TILE = SORT_T * SORT_IPT;   // entries per block
 constexpr int SORT_BITS = 8;                   // digit width
 constexpr int SORT_BINS = 1 << SORT_BITS;
@@ -40,10 +40,17 @@ __global__ void __launch_bounds__(SORT_T) sort_hist(const uint64_t *keys, uint32
     __syncthreads();
     const uint64_t base = (uint64_t)seg * n;
     const uint32_t lo = blk * SORT_TILE, hi = min(lo + (uint32_t)SORT_TILE, n);
-    for (uint32_t i = lo + tid; i < hi; i += SORT_T) {
-        const uint32_t dg = (uint32_t)(keys[base + i] >> shift) & mask;
-        atomicAdd(&cnt[wave][dg], 1u);
+    // all of this thread's keys are loaded before the first count
+    uint32_t dg[SORT_IPT];
+#pragma unroll
+    for (int r = 0; r < SORT_IPT; ++r) {
+        const uint32_t i = lo + r * SORT_T + tid;
+        dg[r] = i < hi ? (uint32_t)(keys[base + i] >> shift) & mask : 0xffffffffu;
     }
+#pragma unroll
+    for (int r = 0; r < SORT_IPT; ++r)
+        if (dg[r] != 0xffffffffu)
+            atomicAdd(&cnt[wave][dg[r]], 1u);
     __syncthreads();
     uint32_t c = 0;
 #pragma unroll
@@ -80,7 +87,7 @@ __device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t *s_w)
 
 // One pass: entries of kin / vin (vin null: the row index, i.e. the entry's
 // position in its segment) to kout / vout in stable order of their digit.
-// Wave w of a block owns the block's entries [1024 w, 1024 w + 1024) and takes
+// Wave w of a block owns the block's entries [PER_WAVE w, PER_WAVE (w + 1)) and takes
 // them 64 at a time in order, so a digit's rank within the block is (its
 // count in earlier waves) + (its count in this wave's earlier rounds) + (the
 // lanes below with the same digit).

@@ -334,3 +334,39 @@ def test_lsh_full_size_quantised_sampled_rows():
     say("rows", rows.size, "exact", ex.total, "found", ref.total, "candidates", cand,
         "pairs", g.shape[0])
     assert ref.total >= 30
+
+
+@pytest.mark.parametrize("name,wid,dist_far", [("cos_f16_262144x256", 0, None),
+                                               ("l2_i8_1048576x64", 2000, 101.2)])
+def test_lsh_merged_instances_from_the_plan(name, wid, dist_far):
+    """Section 4's parameters from sj_lsh_plan (recall target 0.9), and its
+    high-probability scheme: the planned number of instances, each with its
+    own draws, run as one call with all their tables (the first-table rule
+    merges them).  The result equals the union of the oracle's LSH joins of
+    the instances taken one by one, with no pair twice, and every planted
+    pair the union holds."""
+    import math
+    import paper_2006_12608_amd as sj
+    wl = workloads.make_config(name, n=2500)
+    if wid == 0:
+        p1 = sj.sj_lsh_collision(0, 1.0, math.acos(wl.threshold))
+        p2 = sj.sj_lsh_collision(0, 1.0, math.pi / 2)
+    else:
+        p1 = sj.sj_lsh_collision(wid, 32.0, math.sqrt(wl.threshold))
+        p2 = sj.sj_lsh_collision(wid, 32.0, dist_far)
+    st, k, L_inst, reps = sj.sj_lsh_plan(p1, p2, wl.n_p, 128, 0.9)
+    assert st == sj.SJ_OK
+    k = max(k, 1)
+    L_inst = min(L_inst, 256 // reps)
+    insts = [workloads.lsh_params(2000 + 7 * r, L=L_inst, k=k, d=wl.d, w=wid) for r in range(reps)]
+    h = workloads.LshParams(L_inst * reps, k, np.concatenate([x.A for x in insts]),
+                            np.concatenate([x.B for x in insts]), wid)
+    say("plan", name, "p1", p1, "p2", p2, "k", k, "L_inst", L_inst, "reps", reps)
+    g, ref, exact, cand, _ = run_lsh(wl, h, check_cand=False)
+    assert np.unique(keys(g)).size == g.shape[0]
+    union = set()
+    for x in insts:
+        union |= set(map(tuple, oracle.lsh_join(wl.metric, wl.dtype, wl.P, wl.Q, wl.threshold,
+                                                x.L, x.k, x.A, x.B, x.w).tolist()))
+    assert set(map(tuple, np.asarray(ref).tolist())) == union
+    say("found", len(union), "of", exact.total)

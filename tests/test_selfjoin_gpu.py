@@ -85,3 +85,36 @@ def test_self_join_triangle_full_size_sampled_rows():
     s = keys(g)
     mirrored = keys(g[:, ::-1].copy())
     assert np.array_equal(np.sort(mirrored), s)
+
+
+@pytest.mark.parametrize("dtype,d,metric,n", [("bf16", 300, "ip", 700), ("f16", 600, "l2", 530),
+                                              ("bf16", 1024, "ip", 600), ("i8", 600, "ip", 777),
+                                              ("i8", 1024, "l2", 513)])
+def test_self_join_triangle_streamed(dtype, d, metric, n):
+    """Rows of more than 512 bytes take the K-streamed kernel: its single pass
+    skips the 256 x 256 tiles below the diagonal and mirrors the pairs of the
+    others; the set equals the oracle's and the two-pass mode's (ragged last
+    tiles on both sides)."""
+    w = self_case(51 + d, n, d, dtype, metric, 0.99)
+    P = to_device(w.P, dtype)
+    say("self streamed", dtype, d, metric, n, w.threshold)
+    g = sorted_pairs(gpu_join(metric, P, P, w.threshold))
+    ref = oracle.join(metric, dtype, w.P, w.P, w.threshold)
+    compare(g, ref, False)
+    s = set(map(tuple, g.tolist()))
+    assert all((j, i) in s for (i, j) in s)
+    g2 = sorted_pairs(gpu_join(metric, P, P, w.threshold, two_pass=True))
+    assert np.array_equal(keys(g2), keys(g))
+
+
+@pytest.mark.parametrize("dtype,d,n", [("i8", 64, 5000), ("bf16", 128, 4100), ("f16", 40, 2600)])
+def test_self_join_triangle_block_pairing(dtype, d, n):
+    """Several blocks of P rows (odd and even counts): the triangle's
+    workgroups pair block pb with block n_pb - 1 - pb, and every pair is
+    still found once per orientation."""
+    w = self_case(61 + d, n, d, dtype, "ip", 0.998)
+    P = to_device(w.P, dtype)
+    say("self pairing", dtype, d, n, w.threshold)
+    g = sorted_pairs(gpu_join("ip", P, P, w.threshold))
+    ref = oracle.join("ip", dtype, w.P, w.P, w.threshold)
+    compare(g, ref, False)
