@@ -225,17 +225,32 @@ int sj_join_noalloc(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t 
  * Afterwards sj_get_stats reports kernel = 3, ms_norms = repacking, norms and
  * hashing, ms_scan = the sorts and the bucket pairing, ms_join = the
  * bucket join.
- * Limits: 1 <= L <= 64, 0 <= k <= 64 (k = 0: one bucket per table, the exact
- * join), L * max(n_p, n_q) < 2^26; other arguments, outputs and errors as
+ * Limits: 1 <= L <= 256, 0 <= k <= 64 (k = 0: one bucket per table, the exact
+ * join), L * max(n_p, n_q) < 2^32; other arguments, outputs and errors as
  * sj_join_ip.  *n_cand (host, may be NULL) receives the number of pair
  * evaluations made (the sum over tables and shared buckets of |P bucket| x
- * |Q bucket|).  Device scratch grows to about L * (n_p + n_q) * 64 bytes,
- * plus L * max(n_p, n_q) * 32 when a key's bits and the table index together
- * exceed 64 (the sort by key, then by table, keeps its own buffers). */
+ * |Q bucket|).  Device scratch grows to about L * (n_p + n_q) * 70 bytes plus
+ * 16 bytes per row of P and of Q. */
 int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p, const void *Q,
                 uint32_t n_q, uint32_t d, double thr, uint32_t L, uint32_t k, const int8_t *A,
                 const int32_t *B, int32_t w, uint32_t *pairs, uint64_t cap, uint64_t *n_out,
                 uint64_t *n_cand);
+
+/* The grouping step of sj_join_lsh on its own (Section 4: the points of each
+ * table grouped by their bucket).  keys (device, L*n uint64, table-major: keys[t*n
+ * + i] is row i's bucket key in table t; each key below 2^bits, bits <= 64,
+ * else the grouping is unspecified) is left unchanged; perm (device, L*n uint32,
+ * caller-owned) receives for each table t the rows 0..n-1 ordered so that rows
+ * of equal keys are contiguous and in increasing row order.  The order of the
+ * groups is a function of the key values and `bits` alone (ascending key when
+ * bits <= 32, the ascending order of a fixed bijective mix of the key
+ * otherwise), so key sets sorted by separate calls list their common keys in
+ * the same relative order: sj_join_lsh pairs P's buckets with Q's by merging
+ * two such orders.  Errors: SJ_E_INVAL (NULL context, bits > 64, misaligned
+ * pointers), SJ_E_UNSUPPORTED (L * n >= 2^32), SJ_E_DEVICE; L * n = 0 does
+ * nothing.  Device scratch grows to about L * n * 20 bytes. */
+int sj_lsh_sort(sj_ctx *ctx, const uint64_t *keys, uint32_t n, uint32_t L, uint32_t bits,
+                uint32_t *perm);
 
 /* Collision probability of one function of the LSH families of sj_join_lsh
  * for two points at distance `dist`: w == 0 (random-hyperplane signs): dist

@@ -3,7 +3,7 @@ Tensor Core Units", Section 4, brute-force method): Python binding of libsj.so.
 
 The raw C-ABI entry points are exposed under their C names (sj_create,
 sj_join_ip, sj_join_l2, sj_count, sj_join_noalloc, sj_normalize,
-sj_join_hamming, sj_join_lsh, sj_lsh_collision, sj_lsh_plan, sj_jl, sj_destroy,
+sj_join_hamming, sj_join_lsh, sj_lsh_sort, sj_lsh_collision, sj_lsh_plan, sj_jl, sj_destroy,
 sj_get_stats, sj_last_error) with plain integer pointers; `join_ip`, `join_l2`, `count` and
 `join_lsh` (the LSH-bucketed join of Theorem 3) are conveniences over PyTorch
 device tensors.  This module only marshals
@@ -70,6 +70,8 @@ def _load():
                                 ctypes.c_int32, vp, u64, ctypes.POINTER(u64),
                                 ctypes.POINTER(u64)]
     lib.sj_join_lsh.restype = i32
+    lib.sj_lsh_sort.argtypes = [vp, vp, u32, u32, u32, vp]
+    lib.sj_lsh_sort.restype = i32
     lib.sj_lsh_collision.argtypes = [ctypes.c_int32, dbl, dbl]
     lib.sj_lsh_collision.restype = dbl
     lib.sj_lsh_plan.argtypes = [dbl, dbl, u64, u32, dbl, ctypes.POINTER(u32), ctypes.POINTER(u32),
@@ -160,6 +162,10 @@ def sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, thr, L, k, A, B, w, pairs
     st = lib.sj_join_lsh(ctx, metric, dtype, P, n_p, Q, n_q, d, float(thr), L, k, A, B, int(w),
                          pairs, cap, ctypes.byref(n), ctypes.byref(nc))
     return st, n.value, nc.value
+
+
+def sj_lsh_sort(ctx, keys, n, L, bits, perm) -> int:
+    return lib.sj_lsh_sort(ctx, keys, n, L, bits, perm)
 
 
 def sj_lsh_collision(w: int, sigma: float, dist: float) -> float:
@@ -384,6 +390,25 @@ def join_lsh(P, Q, thr: float, metric: str = "ip", *, L: int, k: int, A, B=None,
     if st != SJ_OK:
         raise SjError(st, sj_last_error(), n)
     return out[:n], nc
+
+
+def lsh_sort(keys, bits: int, ctx=None):
+    """The LSH join's grouping step (sj_lsh_sort): keys is an (L, n) int64
+    device tensor of bucket keys (read as uint64, each below 2**bits).  Returns
+    an (L, n) int32 tensor: per table the rows with equal keys contiguous and
+    in increasing order, the groups in an order fixed by the key values."""
+    import torch
+    if keys.dim() != 2 or keys.dtype != torch.int64 or not keys.is_cuda or \
+            not keys.is_contiguous():
+        raise ValueError("keys must be a contiguous (L, n) int64 device tensor")
+    L, n = keys.shape
+    perm = torch.empty((L, n), dtype=torch.int32, device=keys.device)
+    ctx = ctx or context(keys.device.index)
+    st = sj_lsh_sort(ctx, keys.data_ptr() if keys.numel() else None, n, L, int(bits),
+                     perm.data_ptr() if perm.numel() else None)
+    if st != SJ_OK:
+        raise SjError(st, sj_last_error())
+    return perm
 
 
 def jl_transform(X, shapes, As, ctx=None):

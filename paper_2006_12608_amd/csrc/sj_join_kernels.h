@@ -635,8 +635,15 @@ __global__ void __launch_bounds__(NW * 64) join_resident(JoinArgs g)
     auto segment = [&](int seg) __attribute__((always_inline)) {
         uint32_t pb, t0, t1;
         if constexpr (MODE == MODE_TRI) {
+            // Workgroups are dealt to the 8 XCDs in turn; numbered XCD-major,
+            // the ones on one XCD take neighbouring block pairs, whose sweeps
+            // meet the same Q tiles within a few dozen tiles of each other
+            // and so share that XCD's L2.
+            const uint32_t G = gridDim.x;
+            const uint32_t bid = G % 8 == 0 ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8
+                                            : blockIdx.x;
             const uint32_t n_pb = (g.n_p + BM - 1) / BM;
-            const uint32_t pp = blockIdx.x / qsplit, qs = blockIdx.x - pp * qsplit;
+            const uint32_t pp = bid / qsplit, qs = bid - pp * qsplit;
             const uint32_t pa = pp, pz = n_pb - 1 - pp;
             const uint32_t la = n_qt - min(pa * BM / BN, n_qt);
             const uint32_t lz = pz != pa ? n_qt - min(pz * BM / BN, n_qt) : 0u;

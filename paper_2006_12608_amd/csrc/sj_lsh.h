@@ -44,10 +44,12 @@ hipError_t launch_keys_fast(int dtype, const Rows &r, uint32_t d, uint32_t L, ui
                             unsigned long long *nfix, hipStream_t s);
 
 // Sorts each table's keys with the row indices as values (n rows per table):
-// sorted[t * n + p], perm[t * n + p] = the p-th smallest key of table t and its
-// row, rows of equal keys in increasing order (a stable radix sort over the
-// keys' low `bits` bits, tables as segments; sj_sort.hip).  `temp` must hold
-// sort_temp_bytes(n, L) bytes; `keys` is not modified.
+// sorted[t * n + p], perm[t * n + p] = the p-th smallest sort key of table t
+// and its row, rows of equal keys in increasing order, where the sort key is
+// the key itself when `bits` <= 32 and a fixed bijective mix of it otherwise
+// (sj_sort.hip): equal sort keys are exactly equal keys, and every operand is
+// sorted in the same order.  `temp` must hold sort_temp_bytes(n, L) bytes;
+// `keys` is not modified.
 size_t sort_temp_bytes(uint32_t n, uint32_t L);
 hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, uint32_t n,
                        uint32_t L, uint32_t bits, void *temp, hipStream_t s);
@@ -106,8 +108,21 @@ hipError_t launch_pack(const Records &rec, uint32_t n_rec, bool write, uint32_t 
                        const unsigned long long *tile_off, const Descs &desc,
                        unsigned long long *overflow, hipStream_t s);
 
+// Row records (rows of rb <= REC_ROW bytes): per row one 128-byte line
+// holding the row zero-padded to a multiple of 32 bytes (the k-steps' reads),
+// then fingerprint bytes of its keys in the first min(L, F) tables, F = 112 -
+// that length (byte 16 rec_fp_chunk(rb) + t for table t, as in
+// launch_fingerprints; zero past L), and its squared norm (bytes 112..115:
+// int32 for int8 rows, float otherwise; zero for inner products, norm null),
+// so that the bucket join gathers each row with one request.
+constexpr uint32_t REC_ROW = 96, REC_BYTES = 128;
+__host__ __device__ constexpr uint32_t rec_fp_chunk(uint32_t rb) { return (rb + 31) / 32 * 2; }
+hipError_t launch_rowrec(const Rows &r, const void *norm, const uint64_t *keys, uint32_t L,
+                         uint8_t *out, hipStream_t s);
+
 struct JoinArgs {
     Rows P, Q;
+    const uint8_t *rec_p, *rec_q;         // row records, or null (rows, norms, fp)
     uint32_t L;
     const uint32_t *perm_p, *perm_q;      // L x n sorted-position -> row
     const uint64_t *keys_p, *keys_q;      // L x n row -> key (first-table rule)

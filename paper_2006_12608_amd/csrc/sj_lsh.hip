@@ -720,7 +720,9 @@ __device__ __forceinline__ bool matches(typename sjk::Mma<DT>::val_t acc,
 // chunk's k-steps, and the epilogue applies the exact test to the candidates,
 // drops pairs that share a bucket in an earlier table (so every pair is
 // reported once) and appends the rest with one atomic per wave and block.
-template <int DT, int MET>
+// With row records (REC) each row comes with its fingerprint and norm in one
+// 128-byte line: the load of a row's 8 chunks brings all three into LDS.
+template <int DT, int MET, bool REC>
 __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
 {
     typedef sjk::Mma<DT> M;
@@ -733,6 +735,11 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
     __shared__ V sNP[TILE], sNQ[TILE];
     __shared__ uint8_t sGP[TILE], sGQ[TILE];                 // row's record in the group
     __shared__ uint32_t sRT[TILE];                           // group record's table
+    // With row records each wave stages up to OUTW of its pairs here and
+    // reserves their slots with one atomic per flush (the records leave room
+    // in LDS); otherwise it reserves once per tile with matches.
+    constexpr uint32_t OUTW = REC ? 64 : 1;
+    __shared__ uint64_t sOut[4][OUTW];
     // used only while a packed tile's row indices are gathered, before the
     // rows themselves go to sA: the group's row prefix sums and its records'
     // first positions
@@ -743,6 +750,10 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
     const int wr = wave >> 1, wc = wave & 1, half = lane >> 5, c32 = lane & 31;
     const uint32_t rb = g.P.row_bytes;   // == g.Q.row_bytes
     const uint32_t lc = tid & 7, lr = tid >> 3;   // load chunk; rows lr + 32 e
+    // tables with a fingerprint byte: a record's chunks fc0 .. 6 hold 16 each
+    // (fc0: past the k-steps' 32-byte reads of the row); otherwise the first 16
+    const uint32_t fc0 = rec_fp_chunk(rb);
+    const uint32_t FT = REC ? 16 * (7 - fc0) : 16u;
 
     // a contiguous range of tiles per workgroup: one search for the
     // descriptor of its first tile, then a walk
@@ -763,6 +774,19 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
         }
     }
     uint64_t local = T0 - g.desc.tile[dsc];
+    uint32_t staged = 0;   // wave-uniform: pairs in sOut[wave]
+    // one reservation for the wave's staged pairs, then each lane writes a
+    // share of them
+    auto flush = [&]() {
+        unsigned long long base = 0;
+        if (lane == 0)
+            base = atomicAdd(g.counter, (unsigned long long)staged);
+        base = sjk::first_lane_u64(base);
+        for (uint32_t l = lane; l < staged; l += 64)
+            if (base + l < g.cap)
+                ((sjk::global_pair *)g.pairs)[base + l] = sOut[wave][l];
+        staged = 0;
+    };
     for (uint64_t T = T0; T < T1; ++T) {
         const uint4 hd = g.desc.head[dsc];
         const uint32_t first = hd.x, ngrp = hd.y;
@@ -869,7 +893,7 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
             }
         }
         __syncthreads();
-        if constexpr (MET == MET_L2) {
+        if constexpr (MET == MET_L2 && !REC) {
             if (tid < (int)TILE) {
                 sNP[tid] = (uint32_t)tid < rows_p ? ((const V *)g.norm_p)[sIP[tid]] : V(0);
                 sNQ[tid] = (uint32_t)tid < rows_q ? ((const V *)g.norm_q)[sIQ[tid]] : V(0);
@@ -887,26 +911,50 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
         // rows are addressed through the tile's indices in LDS at every load
         // (no per-thread row pointers: fewer registers, four waves per SIMD)
         for (uint32_t kc = 0; kc < rb; kc += 128) {
-            const uint32_t off = kc + 16 * lc;
-            const i32x4 z = {0, 0, 0, 0};
-            const bool in = off < rb;
-            i32x4 la[LPT], lb[LPT];
+            if constexpr (REC) {
+                // whole records straight into LDS (one pass: rows of at most
+                // REC_ROW bytes).  A wave's load fills 64 consecutive 16-byte
+                // positions; position p holds chunk p % CS of the record of
+                // tile row p / CS (the pad position reloads chunk 0).  Rows
+                // past the tile's (index 0) load row 0: their results are
+                // never read.
+                constexpr int NLD = TILE * CS / 64;
 #pragma unroll
-            for (int e = 0; e < LPT; ++e) {
-                const uint32_t rr = lr + 32 * e;
-                la[e] = rr < rows_p && in
-                            ? *(const i32x4 *)(g.P.X + (size_t)sIP[rr] * rb + off) : z;
-                lb[e] = rr < rows_q && in
-                            ? *(const i32x4 *)(g.Q.X + (size_t)sIQ[rr] * rb + off) : z;
-            }
-            if (kc)
-                __syncthreads();   // the previous chunk's fragments are read
+                for (int k = 0; k < (NLD + 3) / 4; ++k) {
+                    const int kk = 4 * k + wave;
+                    if (kk < NLD) {
+                        const uint32_t pos = 64 * kk + lane, row = pos / CS, ch = pos % CS;
+                        const uint32_t cb = 16 * (ch == CS - 1 ? 0 : ch);
+                        sjk::buffer_load_lds16(g.rec_p, g.P.n * REC_BYTES, sIP[row] * REC_BYTES + cb,
+                                               (uint8_t *)sA + 1024 * kk);
+                        sjk::buffer_load_lds16(g.rec_q, g.Q.n * REC_BYTES, sIQ[row] * REC_BYTES + cb,
+                                               (uint8_t *)sB + 1024 * kk);
+                    }
+                }
+                __builtin_amdgcn_s_waitcnt(0);   // this wave's loads landed
+                __syncthreads();
+            } else {
+                const uint32_t off = kc + 16 * lc;
+                const i32x4 z = {0, 0, 0, 0};
+                const bool in = off < rb;
+                i32x4 la[LPT], lb[LPT];
 #pragma unroll
-            for (int e = 0; e < LPT; ++e) {
-                sA[(lr + 32 * e) * CS + lc] = la[e];
-                sB[(lr + 32 * e) * CS + lc] = lb[e];
+                for (int e = 0; e < LPT; ++e) {
+                    const uint32_t rr = lr + 32 * e;
+                    la[e] = rr < rows_p && in
+                                ? *(const i32x4 *)(g.P.X + (size_t)sIP[rr] * rb + off) : z;
+                    lb[e] = rr < rows_q && in
+                                ? *(const i32x4 *)(g.Q.X + (size_t)sIQ[rr] * rb + off) : z;
+                }
+                if (kc)
+                    __syncthreads();   // the previous chunk's fragments are read
+#pragma unroll
+                for (int e = 0; e < LPT; ++e) {
+                    sA[(lr + 32 * e) * CS + lc] = la[e];
+                    sB[(lr + 32 * e) * CS + lc] = lb[e];
+                }
+                __syncthreads();
             }
-            __syncthreads();
             const uint32_t nks = min(4u, (rb - kc + 31) / 32);
 #pragma unroll
             for (uint32_t ks = 0; ks < 4; ++ks)
@@ -931,13 +979,27 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
         // bucket tags of its matches); then, only in a wave with a match, the
         // first-table rule from the rows' key fingerprints, which the wave
         // stages in the operand LDS the MFMAs no longer read.
+        // A record's norm is the first word of its chunk 7, its fingerprints
+        // chunks fc0..6 (the MFMAs read only the row's chunks).
+        auto norm_p = [&](uint32_t il) {
+            if constexpr (REC)
+                return *(const V *)&sA[il * CS + 7];
+            else
+                return sNP[il];
+        };
+        auto norm_q = [&](uint32_t jl) {
+            if constexpr (REC)
+                return *(const V *)&sB[jl * CS + 7];
+            else
+                return sNQ[jl];
+        };
         uint32_t mk[2][2];
         bool any = false;
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const uint32_t jl = wc * 64 + 32 * b + c32;
             const bool jok = jl < rows_q;
-            const V ny = MET == MET_L2 ? sNQ[jl] : V(0);
+            const V ny = MET == MET_L2 ? norm_q(jl) : V(0);
 #pragma unroll
             for (int a = 0; a < 2; ++a) {
                 const uint32_t ib = wr * 64 + 32 * a + 4 * half;
@@ -945,7 +1007,7 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const uint32_t il = ib + 8 * (r >> 2) + (r & 3);
-                    const V nx = MET == MET_L2 ? sNP[il] : V(0);
+                    const V nx = MET == MET_L2 ? norm_p(il) : V(0);
                     const bool ok = jok && il < rows_p && matches<DT, MET>(acc[a][b][r], nx, ny, g);
                     m |= ok ? (1u << r) : 0u;
                 }
@@ -953,11 +1015,12 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
                 any |= m != 0;
             }
         }
-        __syncthreads();   // every wave's MFMAs are done with sA and sB
+        if constexpr (!REC)
+            __syncthreads();   // every wave's MFMAs are done with sA and sB
         if (__ballot(any) == 0)
             continue;
         uint4 *const wf = (uint4 *)sA + wave * 128;   // fingerprints: 64 P rows, 64 Q rows
-        if (g.L > 1) {
+        if (!REC && g.L > 1) {
             const uint32_t pr = wr * 64 + lane, qr = wc * 64 + lane;
             const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
             wf[lane] = pr < rows_p ? g.fp_p[sIP[pr]] : z4;
@@ -989,37 +1052,44 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
                 }
                 if (t > 0 && m != 0) {
                     // the first-table rule: drop the pair when its keys agree
-                    // in an earlier table.  Tables below 16 by fingerprint
-                    // (a byte per table; equal keys give equal bytes), each
-                    // equal byte confirmed with the keys; later tables by
-                    // their keys, 8 tables per round of independent loads.
-                    const uint4 fj = wf[64 + (jl - wc * 64)];
-                    const uint32_t tf = t < 16 ? t : 16;
+                    // in an earlier table.  Tables below FT by fingerprint (a
+                    // byte per table; equal keys give equal bytes), each equal
+                    // byte confirmed with the keys; later tables by their
+                    // keys, 8 tables per round of independent loads.
+                    const uint32_t tf = t < FT ? t : FT;
                     uint32_t mm = m;
                     while (mm) {
                         const int r = __builtin_ctz(mm);
                         mm &= mm - 1;
                         const uint32_t il = ib + 8 * (r >> 2) + (r & 3);
                         const uint32_t i = sIP[il];
-                        const uint4 fi = wf[il - wr * 64];
-                        const uint32_t xw[4] = {fi.x ^ fj.x, fi.y ^ fj.y, fi.z ^ fj.z, fi.w ^ fj.w};
-                        uint32_t eq = 0;   // bit t2: byte t2 of the fingerprints equal
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const uint32_t x = xw[q];
-                            const uint32_t y = ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
-                            eq |= (((y >> 7) & 1u) | ((y >> 14) & 2u) | ((y >> 21) & 4u) |
-                                   ((y >> 28) & 8u)) << (4 * q);
-                        }
-                        eq &= tf >= 16 ? 0xffffu : (1u << tf) - 1u;
                         bool same = false;
-                        while (eq && !same) {
-                            const uint32_t t2 = __builtin_ctz(eq);
-                            eq &= eq - 1;
-                            same = g.keys_p[(size_t)t2 * g.P.n + i] ==
-                                   g.keys_q[(size_t)t2 * g.Q.n + j];
+                        for (uint32_t c = 0; 16 * c < tf && !same; ++c) {
+                            const uint4 fi = REC ? ((const uint4 *)sA)[il * CS + fc0 + c]
+                                                 : wf[il - wr * 64];
+                            const uint4 fj = REC ? ((const uint4 *)sB)[jl * CS + fc0 + c]
+                                                 : wf[64 + (jl - wc * 64)];
+                            const uint32_t xw[4] = {fi.x ^ fj.x, fi.y ^ fj.y, fi.z ^ fj.z,
+                                                    fi.w ^ fj.w};
+                            uint32_t eq = 0;   // bit u: byte u (table 16 c + u) equal
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                const uint32_t x = xw[q];
+                                const uint32_t y =
+                                    ~(((x & 0x7f7f7f7fu) + 0x7f7f7f7fu) | x | 0x7f7f7f7fu);
+                                eq |= (((y >> 7) & 1u) | ((y >> 14) & 2u) | ((y >> 21) & 4u) |
+                                       ((y >> 28) & 8u)) << (4 * q);
+                            }
+                            const uint32_t rem = tf - 16 * c;
+                            eq &= rem >= 16 ? 0xffffu : (1u << rem) - 1u;
+                            while (eq && !same) {
+                                const uint32_t t2 = 16 * c + __builtin_ctz(eq);
+                                eq &= eq - 1;
+                                same = g.keys_p[(size_t)t2 * g.P.n + i] ==
+                                       g.keys_q[(size_t)t2 * g.Q.n + j];
+                            }
                         }
-                        for (uint32_t t2 = 16; t2 < t && !same; t2 += 8) {
+                        for (uint32_t t2 = FT; t2 < t && !same; t2 += 8) {
 #pragma unroll
                             for (uint32_t u = 0; u < 8; ++u) {
                                 const uint32_t tt = t2 + u < t ? t2 + u : t - 1;
@@ -1049,6 +1119,32 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
         }
         if (tot == 0)
             continue;
+        if constexpr (REC) {
+            if (staged + tot > OUTW) {
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                flush();
+            }
+            if (tot <= OUTW) {
+                // stage: each lane's pairs at its prefix, in (block, register) order
+                uint32_t at = staged + pre;
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const uint32_t j = sIQ[wc * 64 + 32 * b + c32];
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        const uint32_t ib = wr * 64 + 32 * a + 4 * half;
+                        uint32_t m = mk[a][b];
+                        while (m) {
+                            const int r = __builtin_ctz(m);
+                            m &= m - 1;
+                            sOut[wave][at++] = sjk::pack_pair(sIP[ib + 8 * (r >> 2) + (r & 3)], j);
+                        }
+                    }
+                }
+                staged += tot;
+                continue;
+            }
+        }
         unsigned long long base = 0;
         if (lane == 0)
             base = atomicAdd(g.counter, (unsigned long long)tot);
@@ -1072,6 +1168,12 @@ __global__ void __launch_bounds__(256, 4) join_kernel(JoinArgs g)
             }
         }
     }
+    if constexpr (REC) {
+        if (staged) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            flush();
+        }
+    }
 }
 
 // Fingerprints of the keys of the first min(L, 16) tables: byte t of fp[row]
@@ -1090,6 +1192,38 @@ __global__ void __launch_bounds__(256) fingerprint_kernel(const uint64_t *keys, 
         w[t >> 2] |= byte << (8 * (t & 3));
     }
     fp[row] = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Row records (sj_lsh.h): thread per row (the lanes' key loads are
+// coalesced over consecutive rows).  Chunk c in fc0 .. 6 holds the
+// fingerprint bytes of tables 16 (c - fc0) .. + 15 (byte u: the top byte of
+// the table's key times an odd constant), chunk 7 the norm.
+__global__ void __launch_bounds__(256) rowrec_kernel(Rows r, const uint32_t *norm,
+                                                     const uint64_t *keys, uint32_t L, i32x4 *out)
+{
+    const uint32_t row = blockIdx.x * 256 + threadIdx.x;
+    if (row >= r.n)
+        return;
+    const uint32_t fc0 = rec_fp_chunk(r.row_bytes);
+    i32x4 *o = out + (size_t)row * (REC_BYTES / 16);
+    for (uint32_t c = 0; c < REC_BYTES / 16; ++c) {
+        i32x4 v = {0, 0, 0, 0};
+        if (16 * c < r.row_bytes) {
+            v = *(const i32x4 *)(r.X + (size_t)row * r.row_bytes + 16 * c);
+        } else if (c >= fc0 && c < 7) {
+            const uint32_t t0 = 16 * (c - fc0);
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
+            for (uint32_t u = 0; u < 16 && t0 + u < L; ++u) {
+                const uint32_t byte =
+                    (uint32_t)((keys[(size_t)(t0 + u) * r.n + row] * 0x9E3779B97F4A7C15ull) >> 56);
+                w[u >> 2] |= byte << (8 * (u & 3));
+            }
+            v = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+        } else if (c == 7 && norm) {
+            v[0] = (int)norm[row];
+        }
+        o[c] = v;
+    }
 }
 
 template <int DT>
@@ -1113,7 +1247,10 @@ hipError_t launch_join_t(const JoinArgs &g, int num_cus, hipStream_t s)
 {
     const uint64_t want = (uint64_t)num_cus * 8;
     const uint32_t grid = (uint32_t)(g.n_tiles < want ? g.n_tiles : want);
-    hipLaunchKernelGGL((join_kernel<DT, MET>), dim3(grid), dim3(256), 0, s, g);
+    if (g.rec_p)
+        hipLaunchKernelGGL((join_kernel<DT, MET, true>), dim3(grid), dim3(256), 0, s, g);
+    else
+        hipLaunchKernelGGL((join_kernel<DT, MET, false>), dim3(grid), dim3(256), 0, s, g);
     return hipGetLastError();
 }
 
@@ -1261,6 +1398,18 @@ hipError_t launch_fingerprints(const uint64_t *keys, uint32_t n, uint32_t L, uin
     if (n == 0)
         return hipSuccess;
     hipLaunchKernelGGL(fingerprint_kernel, dim3((n + 255) / 256), dim3(256), 0, s, keys, n, L, fp);
+    return hipGetLastError();
+}
+
+hipError_t launch_rowrec(const Rows &r, const void *norm, const uint64_t *keys, uint32_t L,
+                         uint8_t *out, hipStream_t s)
+{
+    if (r.n == 0)
+        return hipSuccess;
+    if (r.row_bytes > REC_ROW)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(rowrec_kernel, dim3((r.n + 255) / 256), dim3(256), 0, s, r,
+                       (const uint32_t *)norm, keys, L, (i32x4 *)out);
     return hipGetLastError();
 }
 

@@ -93,7 +93,8 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
     // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
-    //          [sorted Q][perm P][perm Q][bucket marks, sizes and numbers]
+    //          [sorted Q][perm P][perm Q][fingerprints P, Q][row records P, Q]
+    //          [bucket marks, sizes and numbers]
     //          [records][chunk counts and offsets][descriptors][scan partials]
     //          [counters][sort temp][widened projections]
     size_t need = 0;
@@ -112,8 +113,14 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_sq = self ? off_sp : take((size_t)L * n_q * 8);
     const size_t off_pp = take((size_t)L * n_p * 4);
     const size_t off_pq = self ? off_pp : take((size_t)L * n_q * 4);
-    const size_t off_fpp = take((size_t)n_p * 16);
-    const size_t off_fpq = self ? off_fpp : take((size_t)n_q * 16);
+    // short rows travel to the bucket join as records with their norm and
+    // fingerprints (one cache line per row); longer ones with 16 fingerprint
+    // bytes per row in an array of their own
+    const bool use_rec = krow <= sjl::REC_ROW && n_max * sjl::REC_BYTES <= 0xffffffffull;
+    const size_t off_fpp = use_rec ? 0 : take((size_t)n_p * 16);
+    const size_t off_fpq = use_rec || self ? off_fpp : take((size_t)n_q * 16);
+    const size_t off_recp = use_rec ? take((size_t)n_p * sjl::REC_BYTES) : 0;
+    const size_t off_recq = use_rec && !self ? take((size_t)n_q * sjl::REC_BYTES) : off_recp;
     const size_t off_flag = take(pos_p * 4);
     const size_t off_fnp = take(pos_p * 4);
     const size_t off_fq0 = take(pos_p * 4);
@@ -175,7 +182,12 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
             SJ_HIP(sjl::launch_keys(dtype, rq, d, L, k, scr + off_aw, B, w, keys_q, s));
     }
     uint4 *fp_p = (uint4 *)(scr + off_fpp), *fp_q = (uint4 *)(scr + off_fpq);
-    if (L > 1) {
+    if (use_rec) {
+        SJ_HIP(sjl::launch_rowrec(rp, l2 ? scr + off_np : nullptr, keys_p, L, scr + off_recp, s));
+        if (!self)
+            SJ_HIP(sjl::launch_rowrec(rq, l2 ? scr + off_nq : nullptr, keys_q, L,
+                                      scr + off_recq, s));
+    } else if (L > 1) {
         SJ_HIP(sjl::launch_fingerprints(keys_p, n_p, L, fp_p, s));
         if (!self)
             SJ_HIP(sjl::launch_fingerprints(keys_q, n_q, L, fp_q, s));
@@ -231,8 +243,10 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     g.perm_q = perm_q;
     g.keys_p = keys_p;
     g.keys_q = keys_q;
-    g.fp_p = fp_p;
-    g.fp_q = fp_q;
+    g.fp_p = use_rec ? nullptr : fp_p;
+    g.fp_q = use_rec ? nullptr : fp_q;
+    g.rec_p = use_rec ? scr + off_recp : nullptr;
+    g.rec_q = use_rec ? scr + off_recq : nullptr;
     g.rec = rec;
     g.desc = desc;
     g.n_desc = (uint32_t)hc[2];
@@ -271,6 +285,43 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     if (total > cap)
         return fail(SJ_E_OVERFLOW, "%llu matches exceed the capacity of %llu pairs",
                     (unsigned long long)total, (unsigned long long)cap);
+    return SJ_OK;
+}
+
+// The grouping of the LSH-bucketed join's tables on its own (Section 4: the
+// points of each table grouped by bucket); contract in include/sj.h.
+extern "C" int sj_lsh_sort(sj_ctx *c, const uint64_t *keys, uint32_t n, uint32_t L,
+                           uint32_t bits, uint32_t *perm)
+{
+    g_err.clear();
+    if (!c)
+        return fail(SJ_E_INVAL, "context is NULL");
+    if (bits > 64)
+        return fail(SJ_E_INVAL, "bits = %u: at most 64", bits);
+    const uint64_t total = (uint64_t)L * n;
+    if (total >= kMaxTableRows)
+        return fail(SJ_E_UNSUPPORTED, "L * n = %llu is not below 2^32",
+                    (unsigned long long)total);
+    c->stats = sj_stats{};
+    if (total == 0)
+        return SJ_OK;
+    int st;
+    if ((st = check_device_ptr(c, keys, total * 8, "keys")) != SJ_OK)
+        return st;
+    if ((st = check_device_ptr(c, perm, total * 4, "perm")) != SJ_OK)
+        return st;
+    if ((uintptr_t)keys % 8 != 0 || (uintptr_t)perm % 4 != 0)
+        return fail(SJ_E_INVAL, "keys must be 8-byte and perm 4-byte aligned");
+    const size_t off_sorted = 0;
+    const size_t off_temp = align_up(total * 8);
+    if ((st = grow_scratch(c, off_temp + sjl::sort_temp_bytes(n, L))) != SJ_OK)
+        return st;
+    uint8_t *scr = (uint8_t *)c->scratch;
+    hipStream_t s = c->stream;
+    SJ_HIP(hipSetDevice(c->device));
+    SJ_HIP(sjl::sort_tables(keys, (uint64_t *)(scr + off_sorted), perm, n, L, bits,
+                            scr + off_temp, s));
+    SJ_HIP(hipStreamSynchronize(s));
     return SJ_OK;
 }
 

@@ -2,9 +2,18 @@
 // table are grouped by bucket): every table's n keys sorted with their rows,
 // on gfx950.
 //
-// A stable least-significant-digit radix sort over 8-bit digits, run on all L
-// tables at once: each table is a segment of n entries, each segment is cut
-// into blocks of SORT_TILE entries, and every pass is
+// Only the grouping of equal keys matters, so a table's keys are sorted in
+// the order of a bijective mix of them, m(key), when they use more than 32
+// bits: 32-bit sort keys (the key itself, or the top half of m(key)) are
+// sorted with their rows, the full m(key) of every sorted position is then
+// gathered through the permutation, and the rare runs whose top halves are
+// equal but whose m differ are put in the order of m by a local sort.  The
+// outputs are the sorted m(key) (or keys) and their rows; equal outputs are
+// exactly equal keys, and P and Q are sorted in one order.
+//
+// The 32-bit sort is a stable least-significant-digit radix sort over 8-bit
+// digits, run on all L tables at once: each table is a segment of n entries,
+// each segment is cut into blocks of SORT_TILE entries, and every pass is
 //   sort_hist:    per (segment, digit, block) counts of the pass's digit;
 //   exclusive scan of the counts laid out [segment][digit][block] (segment s
 //                 then starts at s n, since every segment holds n entries):
@@ -14,8 +23,8 @@
 //                 per digit continues the rank across the wave's rounds), puts
 //                 them in digit order in LDS and writes each digit's run to its
 //                 position, so a block's stores are contiguous runs.
-// Bound by HBM: each pass reads the keys twice and the rows once and writes
-// both (28 bytes per entry).
+// Bound by HBM: each pass reads the sort keys twice and the rows once and
+// writes both (20 bytes per entry).
 #include "sj_internal.h"
 #include "sj_lsh.h"
 
@@ -29,7 +38,7 @@ constexpr int SORT_BINS = 1 << SORT_BITS;
 static_assert(SORT_BINS == SORT_T, "one thread per digit in the block-wide steps");
 
 // Counts of the digit (key >> shift) & mask in block `blk` of segment `seg`.
-__global__ void __launch_bounds__(SORT_T) sort_hist(const uint64_t *keys, uint32_t n, uint32_t bps,
+__global__ void __launch_bounds__(SORT_T) sort_hist(const uint32_t *keys, uint32_t n, uint32_t bps,
                                                     uint32_t shift, uint32_t mask, uint32_t *hist)
 {
     __shared__ uint32_t cnt[SORT_T / 64][SORT_BINS];
@@ -45,7 +54,7 @@ __global__ void __launch_bounds__(SORT_T) sort_hist(const uint64_t *keys, uint32
 #pragma unroll
     for (int r = 0; r < SORT_IPT; ++r) {
         const uint32_t i = lo + r * SORT_T + tid;
-        dg[r] = i < hi ? (uint32_t)(keys[base + i] >> shift) & mask : 0xffffffffu;
+        dg[r] = i < hi ? (keys[base + i] >> shift) & mask : 0xffffffffu;
     }
 #pragma unroll
     for (int r = 0; r < SORT_IPT; ++r)
@@ -91,13 +100,13 @@ __device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t *s_w)
 // them 64 at a time in order, so a digit's rank within the block is (its
 // count in earlier waves) + (its count in this wave's earlier rounds) + (the
 // lanes below with the same digit).
-__global__ void __launch_bounds__(SORT_T) sort_scatter(const uint64_t *kin, const uint32_t *vin,
-                                                       uint64_t *kout, uint32_t *vout, uint32_t n,
+__global__ void __launch_bounds__(SORT_T) sort_scatter(const uint32_t *kin, const uint32_t *vin,
+                                                       uint32_t *kout, uint32_t *vout, uint32_t n,
                                                        uint32_t bps, uint32_t shift,
                                                        uint32_t nbits,
                                                        const unsigned long long *offs)
 {
-    __shared__ uint64_t s_k[SORT_TILE];
+    __shared__ uint32_t s_k[SORT_TILE];
     __shared__ uint32_t s_v[SORT_TILE];
     __shared__ uint32_t s_run[SORT_T / 64][SORT_BINS];
     __shared__ uint32_t s_start[SORT_BINS];
@@ -114,20 +123,20 @@ __global__ void __launch_bounds__(SORT_T) sort_scatter(const uint64_t *kin, cons
     __syncthreads();
 
     constexpr int PER_WAVE = SORT_TILE / (SORT_T / 64);
-    uint64_t key[SORT_IPT];
+    uint32_t key[SORT_IPT];
     uint32_t val[SORT_IPT], rank[SORT_IPT];
 #pragma unroll
     for (int r = 0; r < SORT_IPT; ++r) {
         const uint32_t li = wave * PER_WAVE + r * 64 + lane;
         const bool valid = li < cnt;
-        key[r] = valid ? kin[base + li] : 0ull;
+        key[r] = valid ? kin[base + li] : 0u;
         val[r] = valid ? (vin ? vin[base + li] : lo + li) : 0u;
     }
 #pragma unroll
     for (int r = 0; r < SORT_IPT; ++r) {
         const uint32_t li = wave * PER_WAVE + r * 64 + lane;
         const bool valid = li < cnt;
-        const uint32_t dg = (uint32_t)(key[r] >> shift) & mask;
+        const uint32_t dg = (key[r] >> shift) & mask;
         uint64_t peers = __ballot(valid);
         for (uint32_t bit = 0; bit < nbits; ++bit) {
             const bool set = (dg >> bit) & 1u;
@@ -162,7 +171,7 @@ __global__ void __launch_bounds__(SORT_T) sort_scatter(const uint64_t *kin, cons
     for (int r = 0; r < SORT_IPT; ++r) {
         const uint32_t li = wave * PER_WAVE + r * 64 + lane;
         if (li < cnt) {
-            const uint32_t dg = (uint32_t)(key[r] >> shift) & mask;
+            const uint32_t dg = (key[r] >> shift) & mask;
             const uint32_t pos = s_start[dg] + s_run[wave][dg] + rank[r];
             if (pos < (uint32_t)SORT_TILE) {   // always: the ranks are a permutation
                 s_k[pos] = key[r];
@@ -175,14 +184,100 @@ __global__ void __launch_bounds__(SORT_T) sort_scatter(const uint64_t *kin, cons
     for (int j = 0; j < SORT_IPT; ++j) {
         const uint32_t p = j * SORT_T + tid;
         if (p < cnt) {
-            const uint64_t k = s_k[p];
-            const uint32_t dg = (uint32_t)(k >> shift) & mask;
+            const uint32_t k = s_k[p];
+            const uint32_t dg = (k >> shift) & mask;
             const unsigned long long at = s_off[dg] + (p - s_start[dg]);
             if (at < (unsigned long long)n * gridDim.x / bps) {   // within L n
                 kout[at] = k;
                 vout[at] = s_v[p];
             }
         }
+    }
+}
+
+// A bijection of 64-bit keys (a multiplication by an odd constant, then an
+// xor of the high half into the low half, both invertible).
+__device__ __forceinline__ uint64_t mix_key(uint64_t k)
+{
+    k *= 0x9E3779B97F4A7C15ull;
+    return k ^ (k >> 32);
+}
+
+// The 32-bit sort keys: the key itself (keys of at most 32 bits) or the top
+// half of its mix.
+__global__ void __launch_bounds__(256) sort_key_kernel(const uint64_t *keys, uint64_t total,
+                                                       int wide, uint32_t *sk)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < total)
+        sk[i] = wide ? (uint32_t)(mix_key(keys[i]) >> 32) : (uint32_t)keys[i];
+}
+
+// The sorted outputs through the permutation: the key (or its mix) of the
+// row at every sorted position; with wide keys also clears the run marks.
+__global__ void __launch_bounds__(256) gather_key_kernel(const uint64_t *keys, uint32_t n,
+                                                         uint64_t total, int wide,
+                                                         const uint32_t *perm, uint64_t *sorted,
+                                                         uint32_t *mark)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total)
+        return;
+    const uint64_t seg = i / n;
+    const uint64_t k = keys[seg * n + perm[i]];
+    sorted[i] = wide ? mix_key(k) : k;
+    if (wide)
+        mark[i] = 0;
+}
+
+// Wide keys, after the gather: a break is a position whose mixed key differs
+// from its predecessor's within a run of equal top halves.  The run's first
+// break walks back to the run's first position and marks it.  Only `sk` and
+// `sorted` are read, and nothing else writes them here.
+__global__ void __launch_bounds__(256) break_kernel(const uint32_t *sk, const uint64_t *sorted,
+                                                    uint32_t n, uint64_t total, uint32_t *mark)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total)
+        return;
+    const uint64_t s0 = i / n * n;
+    if (i == s0 || sk[i - 1] != sk[i] || sorted[i - 1] == sorted[i])
+        return;
+    uint64_t a = i - 1;
+    while (a > s0 && sk[a - 1] == sk[i]) {
+        if (sorted[a - 1] != sorted[a])
+            return;   // an earlier break marks the run
+        --a;
+    }
+    mark[a] = 1;
+}
+
+// Sorts every marked run by the mixed key, stably (insertion sort: distinct
+// keys share a top half with probability 2^-32, so marked runs are rare; the
+// cost is quadratic in a marked run's length).  Runs are disjoint and each
+// has one first position, so no two threads write the same entries.
+__global__ void __launch_bounds__(256) fixup_kernel(const uint32_t *sk, const uint32_t *mark,
+                                                    uint32_t n, uint64_t total, uint64_t *sorted,
+                                                    uint32_t *perm)
+{
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total || !mark[i])
+        return;
+    const uint64_t end = (i / n + 1) * n;
+    uint64_t e = i + 1;
+    while (e < end && sk[e] == sk[i])
+        ++e;
+    for (uint64_t a = i + 1; a < e; ++a) {
+        const uint64_t k = sorted[a];
+        const uint32_t v = perm[a];
+        uint64_t b = a;
+        while (b > i && sorted[b - 1] > k) {
+            sorted[b] = sorted[b - 1];
+            perm[b] = perm[b - 1];
+            --b;
+        }
+        sorted[b] = k;
+        perm[b] = v;
     }
 }
 
@@ -194,7 +289,7 @@ size_t sort_temp_bytes(uint32_t n, uint32_t L)
     const uint64_t total = (uint64_t)n * L;
     const uint64_t counts = (uint64_t)L * SORT_BINS * blocks_per_segment(n);
     auto up = [](uint64_t x) { return (x + 255) & ~(uint64_t)255; };
-    return up(total * 8) + up(total * 4) + up(counts * 4) + up(counts * 8) +
+    return 2 * up(total * 4) + up(total * 4) + up(counts * 4) + up(counts * 8) +
            up(sjk::scan_partials_size(counts) * 8) + 256;
 }
 
@@ -208,31 +303,36 @@ hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, u
     const uint64_t counts = (uint64_t)L * SORT_BINS * bps;
     auto up = [](uint64_t x) { return (x + 255) & ~(uint64_t)255; };
     uint8_t *t = (uint8_t *)temp;
-    uint64_t *tk = (uint64_t *)t;
-    uint32_t *tv = (uint32_t *)(t + up(total * 8));
-    uint32_t *hist = (uint32_t *)(t + up(total * 8) + up(total * 4));
-    unsigned long long *offs =
-        (unsigned long long *)(t + up(total * 8) + up(total * 4) + up(counts * 4));
+    uint32_t *ska = (uint32_t *)t;                             // sort keys, two buffers
+    uint32_t *skb = (uint32_t *)(t + up(total * 4));
+    uint32_t *tv = (uint32_t *)(t + 2 * up(total * 4));        // rows, second buffer
+    uint32_t *hist = (uint32_t *)(t + 3 * up(total * 4));
+    unsigned long long *offs = (unsigned long long *)((uint8_t *)hist + up(counts * 4));
     unsigned long long *part = (unsigned long long *)((uint8_t *)offs + up(counts * 8));
     unsigned long long *tot =
         (unsigned long long *)((uint8_t *)part + up(sjk::scan_partials_size(counts) * 8));
-    // at least one pass (with no key bits it is a stable copy that also writes
-    // the rows)
-    const uint32_t passes = bits == 0 ? 1u : (bits + SORT_BITS - 1) / SORT_BITS;
+    const bool wide = bits > 32;
+    const uint32_t sbits = wide ? 32u : bits;
+    const dim3 g1((uint32_t)((total + 255) / 256));
+    hipLaunchKernelGGL(sort_key_kernel, g1, dim3(256), 0, s, keys, total, wide ? 1 : 0, ska);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    // at least one pass (with no key bits it is a stable copy that also
+    // writes the rows); the last pass leaves the rows in `perm`
+    const uint32_t passes = sbits == 0 ? 1u : (sbits + SORT_BITS - 1) / SORT_BITS;
     const uint32_t grid = L * bps;
-    const uint64_t *kin = keys;
+    const uint32_t *kin = ska;
     const uint32_t *vin = nullptr;
     for (uint32_t pass = 0; pass < passes; ++pass) {
         const uint32_t shift = pass * SORT_BITS;
-        const uint32_t nbits = bits == 0 ? 0u : min((uint32_t)SORT_BITS, bits - shift);
-        // the last pass lands in the outputs
+        const uint32_t nbits = sbits == 0 ? 0u : min((uint32_t)SORT_BITS, sbits - shift);
         const bool to_out = ((passes - 1 - pass) & 1u) == 0;
-        uint64_t *kout = to_out ? sorted : tk;
+        uint32_t *kout = kin == ska ? skb : ska;
         uint32_t *vout = to_out ? perm : tv;
         hipLaunchKernelGGL(sort_hist, dim3(grid), dim3(SORT_T), 0, s, kin, n, bps, shift,
                            (1u << nbits) - 1u, hist);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess)
+        if ((e = hipGetLastError()) != hipSuccess)
             return e;
         if ((e = sjk::launch_scan(hist, counts, offs, part, tot, s)) != hipSuccess)
             return e;
@@ -243,7 +343,19 @@ hipError_t sort_tables(const uint64_t *keys, uint64_t *sorted, uint32_t *perm, u
         kin = kout;
         vin = vout;
     }
-    return hipSuccess;
+    // the rows' second buffer is free after the last pass: the run marks
+    hipLaunchKernelGGL(gather_key_kernel, g1, dim3(256), 0, s, keys, n, total, wide ? 1 : 0, perm,
+                       sorted, tv);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (wide) {
+        hipLaunchKernelGGL(break_kernel, g1, dim3(256), 0, s, kin, sorted, n, total, tv);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(fixup_kernel, g1, dim3(256), 0, s, kin, tv, n, total, sorted, perm);
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 }  // namespace sjl

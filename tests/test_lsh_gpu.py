@@ -92,6 +92,9 @@ def case(seed, n_p, n_q, d, dtype, metric, thr, lo=-4, hi=4, real=False):
     ("i8", "l2", 400.0, 48, 300),
     ("bf16", "l2", 420.0, 96, 400),
     ("f16", "l2", 500.0, 40, 350),
+    ("i8", "l2", 600.0, 96, 400),     # 96-byte rows: the longest that travel as records
+    ("f16", "l2", 500.0, 48, 350),
+    ("i8", "l2", 600.0, 97, 400),     # 112-byte padded rows: gathered without records
 ])
 def test_lsh_parity_integer(dtype, metric, thr, d, wid):
     w = case(700 + d, 333, 290, d, dtype, metric, thr)
@@ -127,10 +130,10 @@ def test_lsh_buckets_span_tiles_and_ragged():
 
 
 def test_lsh_quantised_wide_keys_many_rows():
-    """Seven quantised values of 9 bits and 8 tables (63 + 3 bits: the table
-    does not fit above the key, so the entries are sorted by key and then
-    stably by table) on 6000 int8 rows of the squared-L2 workload: the sorts
-    span many radix blocks."""
+    """Seven quantised values of 9 bits and 8 tables (63-bit keys: sorted by
+    the top half of their mix, then the rare runs whose halves collide by the
+    whole mix) on 6000 int8 rows of the squared-L2 workload: the sorts span
+    many radix blocks."""
     wl = workloads.make_config("l2_i8_1048576x64", n=6000)
     h = workloads.lsh_params(1303, L=8, k=7, d=wl.d, w=2000)
     g, ref, exact, cand, _ = run_lsh(wl, h)
@@ -148,6 +151,18 @@ def test_lsh_k0_is_exact_join():
     assert np.array_equal(full, g)
 
 
+@pytest.mark.parametrize("metric,thr,k,wid", [("l2", 200.0, 0, 0), ("l2", 180.0, 1, 120),
+                                             ("ip", 2.0, 2, 0)])
+def test_lsh_dense_matches(metric, thr, k, wid):
+    """Short int8 rows (joined as row records) with thresholds that most pairs
+    pass: waves find from a few to thousands of pairs per tile, so the pairs
+    go both through the per-wave staging (many flushes) and straight out."""
+    w = case(51 + k, 700, 650, 16, "i8", metric, thr, -3, 3)
+    h = workloads.lsh_params(52 + k, L=3, k=k, d=16, w=wid)
+    g, ref, exact, *_ = run_lsh(w, h)
+    assert len(ref) > w.n_p * w.n_q // 10
+
+
 def test_lsh_self_join_same_pointer():
     w = case(45, 300, 300, 32, "i8", "l2", 300.0, -5, 5)
     w.Q = w.P
@@ -159,13 +174,17 @@ def test_lsh_self_join_same_pointer():
     assert all((j, i) in s for (i, j) in s)          # symmetric
 
 
-def test_lsh_many_tables_first_table_rule():
+@pytest.mark.parametrize("d,L,thr", [(16, 24, 6.0), (64, 56, 64.0), (80, 20, 72.0),
+                                     (96, 24, 78.0), (128, 24, 90.0)])
+def test_lsh_many_tables_first_table_rule(d, L, thr):
     """Many tables and few functions: most pairs collide in several tables;
-    each must still be reported once."""
-    w = case(47, 260, 240, 16, "i8", "ip", 6.0, -3, 3)
-    h = workloads.lsh_params(48, L=24, k=2, d=16)
+    each must still be reported once.  Short rows carry fingerprints of the
+    first 112 - (row bytes rounded up to 32) tables in their records (80, 48
+    and 16 tables here, later tables by their keys); 128-byte rows carry 16."""
+    w = case(47 + d, 260, 240, d, "i8", "ip", thr, -3, 3)
+    h = workloads.lsh_params(48 + d, L=L, k=2, d=d)
     g, ref, *_ = run_lsh(w, h)
-    assert len(g) == len(ref)
+    assert len(g) == len(ref) > 0
 
 
 def test_lsh_overflow_and_errors():
