@@ -92,11 +92,7 @@ def kernel_source_hash(prefixes=JOIN_SOURCES) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_for(key: str, prefixes=JOIN_SOURCES):
-    """HBM bytes per launch from the committed rocprofv3 counter summary (key:
-    the workload name for its join or first-pass kernel, "<workload>:emit" for
-    its emit-from-bits kernel), if it was taken on the current kernel sources;
-    otherwise None."""
+def _counter_record(key: str, prefixes=JOIN_SOURCES):
     p = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(p):
         return None
@@ -106,7 +102,28 @@ def traffic_for(key: str, prefixes=JOIN_SOURCES):
         return None
     if not rec or rec.get("kernel_sha") != kernel_source_hash(prefixes):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
+
+
+def traffic_for(key: str, prefixes=JOIN_SOURCES):
+    """HBM bytes per launch from the committed rocprofv3 counter summary (key:
+    the workload name for its join or first-pass kernel, "<workload>:emit" for
+    its emit-from-bits kernel), if it was taken on the current kernel sources;
+    otherwise None."""
+    rec = _counter_record(key, prefixes)
+    return rec.get("hbm_bytes_per_launch") if rec else None
+
+
+def busy_for(key: str):
+    """The join kernel's matrix-core busy fraction and clock (GHz) from the
+    committed rocprofv3 counters (SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE)
+    of this workload, if taken on the current kernel sources; otherwise
+    None.  Their product over 2.4 GHz is the fraction of the spec peak."""
+    rec = _counter_record(key)
+    if not rec or "mfma_busy" not in rec:
+        return None
+    return {"mfma_busy": rec["mfma_busy"], "clock_ghz": rec["clock_ghz"],
+            "source": "profiles/join_resident_mfma_busy_and_clock_counters.md"}
 
 
 def measured_mfma_peak(dtype: str, duration_ms: float, operands=None, waves_per_simd: int = 2):
@@ -507,7 +524,8 @@ def main():
                      "traffic": traffic,
                      "kernel": "join_resident" if w.d * (1 if w.dtype == "i8" else 2) <= 512
                      else "join_streamed",
-                     "kernel_ms": kms},
+                     "kernel_ms": kms,
+                     "counters": None if w.self_join or two_pass else busy_for(args.workload)},
         "effective_tflops_step": flop / (ms_step / 1e3) / 1e12,
         "pct_peak_step": flop / (ms_step / 1e3) / 1e12 / peak,
         "n_out": int(n_out),
@@ -568,7 +586,7 @@ def kernel_fraction(name: str, stream, ctx, steps: int = 10):
     return {"kernel_ms": kms, "achieved": achieved, "peak": PEAK[w.dtype],
             "unit": "TOP/s" if w.dtype == "i8" else "TFLOP/s",
             "frac": achieved / PEAK[w.dtype], "n_out": int(n), "dtype": w.dtype,
-            "steps": steps}
+            "steps": steps, "counters": busy_for(name)}
 
 
 def mfma_loop(args):
