@@ -78,6 +78,9 @@ JOIN_SOURCES = ("sj_api", "sj_aux", "sj_internal", "sj_join")
 # Sources of the TCU JL transform (its own counter record).
 JL_SOURCES = ("sj_jl", "sj_host")
 
+# Sources of the LSH-bucketed join (it uses the join's MMA helpers too).
+LSH_SOURCES = ("sj_lsh", "sj_sort", "sj_aux", "sj_internal", "sj_host", "sj_join")
+
 
 def kernel_source_hash(prefixes=JOIN_SOURCES) -> str:
     """Hash of the code of the source files whose names start with one of
@@ -334,7 +337,7 @@ def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    hash_ms, sort_ms, join_ms = [], [], []
+    hash_ms, sort_ms, join_ms, rows = [], [], [], 0
     t0 = time.perf_counter()
     for _ in range(args.steps):
         n_out, n_cand = step()
@@ -342,11 +345,17 @@ def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
         hash_ms.append(s.ms_norms)
         sort_ms.append(s.ms_scan)
         join_ms.append(s.ms_join)
+        rows = s.lsh_rows
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) / args.steps * 1e3
     jms = float(np.mean(join_ms))
     flop = 2.0 * n_cand * max(w.d, 1)
     peak = PEAK[w.dtype]
+    # the bucket join's algorithmic bytes: every row of every shared bucket
+    # read once per table (with its norm for L2), the pairs written
+    esz = 1 if w.dtype == "i8" else 2
+    alg_bytes = rows * (w.d * esz + (4 if w.metric == "l2" else 0)) + 8 * n_out
+    lsh_key = f"lsh:{w.name}:{L},{k},{wid}"
     # the all-pairs join of the same workload, for the speed-up at this recall
     fn = sj.sj_join_ip if w.metric == "ip" else sj.sj_join_l2
     out2 = torch.empty((max(exact_total, 1), 2), dtype=torch.int32, device="cuda")
@@ -381,10 +390,14 @@ def bench_lsh(args, w, Pd, Qd, ctx, exact_total):
         "candidate_pair_evals_per_s": n_cand / (ms_step / 1e3),
         "phases_ms": {"hash": float(np.mean(hash_ms)), "sort_and_pairs": float(np.mean(sort_ms)),
                       "bucket_join": jms},
-        "roofline": {"bound": "mfma", "kernel": "lsh join_kernel", "kernel_ms": jms,
-                     "achieved": flop / (jms / 1e3) / 1e12, "peak": peak,
-                     "unit": "TOP/s" if w.dtype == "i8" else "TFLOP/s",
-                     "frac": flop / (jms / 1e3) / 1e12 / peak, "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": "lsh join_kernel", "kernel_ms": jms,
+                     "achieved": alg_bytes / (jms / 1e3) / 1e9, "peak": 8000.0, "unit": "GB/s",
+                     "frac": alg_bytes / (jms / 1e3) / 1e9 / 8000.0,
+                     "algorithmic_bytes": int(alg_bytes), "bucket_rows": int(rows),
+                     "traffic": traffic_for(lsh_key, LSH_SOURCES),
+                     "mfma_achieved": flop / (jms / 1e3) / 1e12, "mfma_peak": peak,
+                     "mfma_unit": "TOP/s" if w.dtype == "i8" else "TFLOP/s",
+                     "mfma_frac": flop / (jms / 1e3) / 1e12 / peak},
     }), flush=True)
 
 

@@ -121,6 +121,9 @@ typedef struct sj_stats {
     uint32_t emit_from_bits; /* two-pass: 1 when the second pass read the first
                                 pass's match bits (or match records) instead
                                 of recomputing the product                    */
+    uint64_t lsh_rows;     /* sj_join_lsh: the sum over tables and shared
+                              buckets of |P bucket| + |Q bucket| (the rows
+                              the bucket join must read at least once)       */
 } sj_stats;
 
 /* Create a context on `device` (a gfx950 GPU), bound to `stream` (a

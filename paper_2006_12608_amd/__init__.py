@@ -39,7 +39,7 @@ class sj_stats(ctypes.Structure):
                 ("ms_join", ctypes.c_double), ("ms_count", ctypes.c_double),
                 ("ms_scan", ctypes.c_double), ("ms_emit", ctypes.c_double),
                 ("kernel", ctypes.c_uint32), ("timed", ctypes.c_uint32),
-                ("emit_from_bits", ctypes.c_uint32)]
+                ("emit_from_bits", ctypes.c_uint32), ("lsh_rows", ctypes.c_uint64)]
 
 
 def _load():

@@ -74,10 +74,15 @@ hipError_t launch_fingerprints(const uint64_t *keys, uint32_t n, uint32_t L, uin
 
 // Marks, for every table t and sorted position p of P that starts a bucket
 // whose key Q also has, flag[t n_p + p] = 1 (else 0) with the bucket's sizes
-// and Q's first position in f_np / f_q0 / f_nq at that index; adds the
-// bucket pairs' pair evaluations (sum of np nq) to *n_cand.
+// and Q's first position in f_np / f_q0 / f_nq at that index; writes the
+// bucket pairs' pair evaluations (sum of np nq) to n_cand[0] and their rows
+// (sum of np + nq) to n_cand[7].  ws: bucket_find_ws_bytes(n_p, L) bytes.
+inline size_t bucket_find_ws_bytes(uint32_t n_p, uint32_t L)
+{
+    return (size_t)((n_p + 255) / 256) * L * 24;
+}
 hipError_t launch_bucket_find(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
-                              uint32_t n_q, uint32_t L, uint32_t *flag, uint32_t *f_np,
+                              uint32_t n_q, uint32_t L, void *ws, uint32_t *flag, uint32_t *f_np,
                               uint32_t *f_q0, uint32_t *f_nq, unsigned long long *n_cand,
                               hipStream_t s);
 // Writes the marked positions as records (rec_off: exclusive scan of flag).

@@ -552,35 +552,84 @@ __device__ __forceinline__ uint32_t run_end(const uint64_t *s, uint32_t p, uint3
     return upper_bound(s, lo, min(lo + step, n), key);
 }
 
+// Per table and block of 256 sorted positions of P, the range of Q's sorted
+// positions whose keys lie between the block's first and last keys: qr[t nb +
+// b] = {first position with key >= the block's first, first with key > its
+// last} (one thread each, so the searches of every block run at once).
+__global__ void __launch_bounds__(256) qrange_kernel(const uint64_t *sorted_p, uint32_t n_p,
+                                                     const uint64_t *sorted_q, uint32_t n_q,
+                                                     uint32_t L, uint2 *qr)
+{
+    const uint32_t nb = (n_p + 255) / 256;
+    const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (uint64_t)nb * L)
+        return;
+    const uint32_t t = (uint32_t)(i / nb), b = (uint32_t)(i - (uint64_t)t * nb);
+    const uint64_t *sp = sorted_p + (size_t)t * n_p;
+    const uint64_t *sq = sorted_q + (size_t)t * n_q;
+    const uint32_t pf = 256 * b;
+    qr[i] = make_uint2(lower_bound(sq, 0, n_q, sp[pf]),
+                       upper_bound(sq, 0, n_q, sp[min(pf + 255, n_p - 1)]));
+}
+
 // One thread per (sorted position of P, table): a position that starts a P
-// bucket looks its key up in Q's sorted keys (within the range of Q keys the
-// block's first and last keys bound, found once per block) and, when Q has
-// it, marks the position with the bucket's sizes.
+// bucket looks its key up in Q's sorted keys within the block's range
+// (qrange_kernel), staged in LDS when it holds at most QCAP keys, and, when Q
+// has the key, marks the position with the bucket's sizes.
+constexpr uint32_t QCAP = 2048;
+
 __global__ void __launch_bounds__(256) bucket_find_kernel(const uint64_t *sorted_p, uint32_t n_p,
                                                           const uint64_t *sorted_q, uint32_t n_q,
-                                                          uint32_t *flag, uint32_t *f_np,
-                                                          uint32_t *f_q0, uint32_t *f_nq,
-                                                          unsigned long long *n_cand)
+                                                          const uint2 *qr, uint32_t *flag,
+                                                          uint32_t *f_np, uint32_t *f_q0,
+                                                          uint32_t *f_nq, ulonglong2 *part)
 {
-    __shared__ uint32_t s_qa, s_qb;
-    __shared__ unsigned long long s_cand[4];
+    __shared__ uint64_t s_q[QCAP];
+    __shared__ unsigned long long s_cand[4], s_rows[4];
     const uint32_t t = blockIdx.y, tid = threadIdx.x;
     const uint32_t pf = blockIdx.x * 256, p = pf + tid;
     const uint64_t *sp = sorted_p + (size_t)t * n_p;
     const uint64_t *sq = sorted_q + (size_t)t * n_q;
-    if (tid == 0)
-        s_qa = lower_bound(sq, 0, n_q, sp[pf]);
-    if (tid == 64)
-        s_qb = upper_bound(sq, 0, n_q, sp[min(pf + 255, n_p - 1)]);
-    __syncthreads();
-    uint64_t cand = 0;
+    const uint2 range = qr[(size_t)t * gridDim.x + blockIdx.x];
+    const uint32_t qa = range.x, qb = range.y;
+    const bool staged = qb - qa <= QCAP;   // uniform
+    if (staged) {
+        for (uint32_t i = tid; i < qb - qa; i += 256)
+            s_q[i] = sq[qa + i];
+        __syncthreads();
+    }
+    uint64_t cand = 0, rows = 0;
     if (p < n_p) {
         const size_t at = (size_t)t * n_p + p;
         uint32_t fl = 0;
         const uint64_t key = sp[p];
         if (p == 0 || sp[p - 1] != key) {
-            const uint32_t q0 = lower_bound(sq, s_qa, s_qb, key);
-            const uint32_t qe = upper_bound(sq, q0, s_qb, key);
+            uint32_t q0, qe;
+            if (staged) {
+                // first position with key >= key, then first with key > key
+                uint32_t lo = 0, hi = qb - qa;
+                while (lo < hi) {
+                    const uint32_t mid = lo + (hi - lo) / 2;
+                    if (s_q[mid] < key)
+                        lo = mid + 1;
+                    else
+                        hi = mid;
+                }
+                uint32_t e = lo;
+                hi = qb - qa;
+                while (e < hi) {
+                    const uint32_t mid = e + (hi - e) / 2;
+                    if (s_q[mid] <= key)
+                        e = mid + 1;
+                    else
+                        hi = mid;
+                }
+                q0 = qa + lo;
+                qe = qa + e;
+            } else {
+                q0 = lower_bound(sq, qa, qb, key);
+                qe = upper_bound(sq, q0, qb, key);
+            }
             if (q0 < qe) {
                 const uint32_t np = run_end(sp, p + 1, n_p, key) - p;
                 fl = 1;
@@ -588,21 +637,60 @@ __global__ void __launch_bounds__(256) bucket_find_kernel(const uint64_t *sorted
                 f_q0[at] = q0;
                 f_nq[at] = qe - q0;
                 cand = (uint64_t)np * (qe - q0);
+                rows = (uint64_t)np + (qe - q0);
             }
         }
         flag[at] = fl;
     }
-    // one atomic per block for the pair evaluations
+    // the block's pair evaluations and rows, summed by sum_parts_kernel (one
+    // counter updated by every block serialises the blocks on its address)
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1)
+    for (int o = 32; o > 0; o >>= 1) {
         cand += __shfl_xor(cand, o, 64);
-    if ((tid & 63) == 0)
+        rows += __shfl_xor(rows, o, 64);
+    }
+    if ((tid & 63) == 0) {
         s_cand[tid >> 6] = cand;
+        s_rows[tid >> 6] = rows;
+    }
+    __syncthreads();
+    if (tid == 0)
+        part[(size_t)t * gridDim.x + blockIdx.x] =
+            make_ulonglong2(s_cand[0] + s_cand[1] + s_cand[2] + s_cand[3],
+                            s_rows[0] + s_rows[1] + s_rows[2] + s_rows[3]);
+}
+
+// One block of 1024 threads: out[0] = sum of the parts' pair evaluations,
+// out[7] = sum of their rows (the counters' slots; written, not added to).
+__global__ void __launch_bounds__(1024) sum_parts_kernel(const ulonglong2 *part, uint64_t n,
+                                                         unsigned long long *out)
+{
+    __shared__ unsigned long long s_c[16], s_r[16];
+    const uint32_t tid = threadIdx.x;
+    unsigned long long c = 0, r = 0;
+    for (uint64_t i = tid; i < n; i += 1024) {
+        const ulonglong2 v = part[i];
+        c += v.x;
+        r += v.y;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        c += __shfl_xor(c, o, 64);
+        r += __shfl_xor(r, o, 64);
+    }
+    if ((tid & 63) == 0) {
+        s_c[tid >> 6] = c;
+        s_r[tid >> 6] = r;
+    }
     __syncthreads();
     if (tid == 0) {
-        const unsigned long long c = s_cand[0] + s_cand[1] + s_cand[2] + s_cand[3];
-        if (c)
-            atomicAdd(n_cand, c);
+        unsigned long long tc = 0, tr = 0;
+        for (int w = 0; w < 16; ++w) {
+            tc += s_c[w];
+            tr += s_r[w];
+        }
+        out[0] = tc;
+        out[7] = tr;
     }
 }
 
@@ -1414,14 +1502,29 @@ hipError_t launch_rowrec(const Rows &r, const void *norm, const uint64_t *keys, 
 }
 
 hipError_t launch_bucket_find(const uint64_t *sorted_p, uint32_t n_p, const uint64_t *sorted_q,
-                              uint32_t n_q, uint32_t L, uint32_t *flag, uint32_t *f_np,
+                              uint32_t n_q, uint32_t L, void *ws, uint32_t *flag, uint32_t *f_np,
                               uint32_t *f_q0, uint32_t *f_nq, unsigned long long *n_cand,
                               hipStream_t s)
 {
     if (n_p == 0 || n_q == 0 || L == 0)
         return hipSuccess;
-    hipLaunchKernelGGL(bucket_find_kernel, dim3((n_p + 255) / 256, L), dim3(256), 0, s, sorted_p,
-                       n_p, sorted_q, n_q, flag, f_np, f_q0, f_nq, n_cand);
+    const uint32_t nb = (n_p + 255) / 256;
+    const uint64_t nr = (uint64_t)nb * L;
+    // workspace: the block sums, then the block ranges of Q
+    ulonglong2 *part = (ulonglong2 *)ws;
+    uint2 *qr = (uint2 *)(part + nr);
+    hipLaunchKernelGGL(qrange_kernel, dim3((uint32_t)((nr + 255) / 256)), dim3(256), 0, s,
+                       sorted_p, n_p, sorted_q, n_q, L, qr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(bucket_find_kernel, dim3(nb, L), dim3(256), 0, s, sorted_p, n_p, sorted_q,
+                       n_q, (const uint2 *)qr, flag, f_np, f_q0, f_nq, part);
+    e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(1024), 0, s, (const ulonglong2 *)ws,
+                       (uint64_t)nb * L, n_cand);
     return hipGetLastError();
 }
 

@@ -3,6 +3,7 @@
 // hash -> sort -> bucket pairs -> bucket join on the context's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -89,7 +90,8 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const uint64_t chunk_cap = (bp_cap + sjl::PACK_CHUNK - 1) / sjl::PACK_CHUNK;
     const uint64_t pos_p = (uint64_t)L * n_p;   // sorted positions of P, all tables
     // one sort workspace, used by P and then by Q
-    const size_t temp_bytes = sjl::sort_temp_bytes(n_max, L);
+    const size_t temp_bytes = std::max(sjl::sort_temp_bytes(n_max, L),
+                                       sjl::bucket_find_ws_bytes(n_p, L));
     const size_t a_bytes = sjl::widened_bytes(dtype, L, k, d);
 
     // scratch: [rows P][rows Q][norms P][norms Q][keys P][keys Q][sorted P]
@@ -137,7 +139,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     const size_t off_dtile = take(bp_cap * 8);
     const size_t off_part = take(sjk::scan_partials_size(pos_p > chunk_cap ? pos_p : chunk_cap) * 8);
     // counters: [0] pair evaluations, [1] records, [2] descriptors, [3] [4]
-    // the hash's fix queues, [5] tiles, [6] tile overflow
+    // the hash's fix queues, [5] tiles, [6] tile overflow, [7] bucket rows
     const size_t off_cnt = take(8 * 8);
     const size_t off_temp = take(temp_bytes);
     const size_t off_aw = take(a_bytes);
@@ -200,9 +202,10 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
         SJ_HIP(sjl::sort_tables(keys_q, sorted_q, perm_q, n_q, L, bits, scr + off_temp, s));
     // the buckets P and Q share, as records in key order, then their tiles
     uint32_t *flag = (uint32_t *)(scr + off_flag);
-    SJ_HIP(sjl::launch_bucket_find(sorted_p, n_p, sorted_q, n_q, L, flag, (uint32_t *)(scr + off_fnp),
-                                   (uint32_t *)(scr + off_fq0), (uint32_t *)(scr + off_fnq), cnt,
-                                   s));
+    // (its per-block sums in the sorts' workspace, free by now)
+    SJ_HIP(sjl::launch_bucket_find(sorted_p, n_p, sorted_q, n_q, L, scr + off_temp, flag,
+                                   (uint32_t *)(scr + off_fnp), (uint32_t *)(scr + off_fq0),
+                                   (uint32_t *)(scr + off_fnq), cnt, s));
     unsigned long long *part = (unsigned long long *)(scr + off_part);
     SJ_HIP(sjk::launch_scan(flag, pos_p, (unsigned long long *)(scr + off_roff), part, cnt + 1, s));
     const sjl::Records rec{(uint32_t *)(scr + off_rect), (uint4 *)(scr + off_recpq)};
@@ -279,6 +282,7 @@ extern "C" int sj_join_lsh(sj_ctx *c, int metric, int dtype, const void *P, uint
     c->stats.ms_join = elapsed_ms(c->ev[2], c->ev[3]);
     c->stats.kernel = 3;
     c->stats.timed = 1;
+    c->stats.lsh_rows = hc[7];
     *n_out = total;
     if (n_cand)
         *n_cand = cand;

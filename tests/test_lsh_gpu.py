@@ -46,18 +46,20 @@ def lsh_device(h):
     return A, B
 
 
-def expected_candidates(w, h):
+def expected_candidates(w, h, rows=False):
     """Sum over tables and keys of (#P rows with the key) x (#Q rows with it),
-    from the oracle's keys."""
+    from the oracle's keys; with rows=True also the sum of (#P rows + #Q rows)
+    over the keys both have."""
     kp = oracle.lsh_keys(w.dtype, w.P, h.L, h.k, h.A, h.B, h.w)
     kq = oracle.lsh_keys(w.dtype, w.Q, h.L, h.k, h.A, h.B, h.w)
-    tot = 0
+    tot = nrows = 0
     for t in range(h.L):
         up, cp = np.unique(kp[t], return_counts=True)
         uq, cq = np.unique(kq[t], return_counts=True)
         _, ip, iq = np.intersect1d(up, uq, return_indices=True)
         tot += int((cp[ip].astype(np.int64) * cq[iq]).sum())
-    return tot
+        nrows += int(cp[ip].sum() + cq[iq].sum())
+    return (tot, nrows) if rows else tot
 
 
 def run_lsh(w, h, thr=None, self_join=False, check_cand=True):
@@ -75,7 +77,9 @@ def run_lsh(w, h, thr=None, self_join=False, check_cand=True):
     ref = oracle.JoinResult(ref_pairs, len(ref_pairs), exact.band_pairs, exact.band_match)
     info = compare(g, ref, w.real_valued)
     if check_cand:
-        assert cand == expected_candidates(w, h)
+        e_cand, e_rows = expected_candidates(w, h, rows=True)
+        assert cand == e_cand
+        assert sj.sj_get_stats(sj.context(Pd.device.index)).lsh_rows == e_rows
     return g, ref_pairs, exact, cand, info
 
 
