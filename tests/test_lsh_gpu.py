@@ -311,12 +311,11 @@ def test_lsh_full_size_sampled_rows():
     assert ref.total >= 16
 
 
-def test_lsh_quantised_joint_sort_full_key():
-    """Six quantised values of 10 bits and 16 tables (60 key bits + 4 table
-    bits = 64: the table number sits in the top bits of one joint sort key,
-    the benchmark's configuration on the int8 squared-L2 workload) on 6000
-    rows of that workload: parity with the oracle's LSH join and its
-    candidate count."""
+def test_lsh_quantised_benchmark_parameters():
+    """Six quantised values of 10 bits and 16 tables (60-bit keys: sorted by
+    the top half of their mix; the benchmark's configuration on the int8
+    squared-L2 workload) on 6000 rows of that workload: parity with the
+    oracle's LSH join, its candidate count and its bucket rows."""
     wl = workloads.make_config("l2_i8_1048576x64", n=6000)
     h = workloads.lsh_params(1303, L=16, k=6, d=wl.d, w=2000)
     g, ref, exact, cand, _ = run_lsh(wl, h)
