@@ -68,7 +68,8 @@ enum sj_metric { SJ_IP = 0, SJ_L2 = 1 };
 enum sj_status {
     SJ_OK = 0,
     SJ_E_INVAL = -1,       /* bad argument: NULL or non-device pointer, buffer
-                              smaller than its shape, NaN threshold, bad enum */
+                              smaller than its shape, NaN threshold, bad enum,
+                              a flag the function does not take */
     SJ_E_OVERFLOW = -2,    /* more matches than `cap`: *n_out holds the exact
                               total and the contents of `pairs` are not a valid
                               answer */

@@ -579,6 +579,8 @@ int sj_join_ip(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
                unsigned flags)
 {
     g_err.clear();
+    if (flags & ~(unsigned)(SJ_FLAG_TWO_PASS | SJ_FLAG_TIMING | SJ_FLAG_RECOMPUTE | SJ_FLAG_COSINE))
+        return fail(SJ_E_INVAL, "unknown flags 0x%x", flags);
     Request rq{SJ_IP, dtype, P, Q, n_p, n_q, d, s, pairs, cap,
                (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
                (flags & SJ_FLAG_RECOMPUTE) != 0};
@@ -663,6 +665,9 @@ int sj_join_l2(sj_ctx *ctx, int dtype, const void *P, uint32_t n_p, const void *
                unsigned flags)
 {
     g_err.clear();
+    if (flags & ~(unsigned)(SJ_FLAG_TWO_PASS | SJ_FLAG_TIMING | SJ_FLAG_RECOMPUTE))
+        return fail(SJ_E_INVAL, "flags 0x%x: sj_join_l2 takes SJ_FLAG_TWO_PASS, SJ_FLAG_TIMING "
+                    "and SJ_FLAG_RECOMPUTE", flags);
     Request rq{SJ_L2, dtype, P, Q, n_p, n_q, d, r2, pairs, cap,
                (flags & SJ_FLAG_TWO_PASS) != 0, false, (flags & SJ_FLAG_TIMING) != 0,
                (flags & SJ_FLAG_RECOMPUTE) != 0};

@@ -83,6 +83,13 @@ def test_bad_values_are_rejected(env):
     st, _ = sj.sj_join_ip(ctx, sj.SJ_I8, big.data_ptr(), 1, big.data_ptr(), 1, 40000, 0.0,
                           out.data_ptr(), 64)
     assert st == sj.SJ_E_UNSUPPORTED
+    # flags a function does not take: unknown bits, and the cosine front end on L2
+    st, _ = sj.sj_join_ip(ctx, sj.SJ_I8, P.data_ptr(), 8, P.data_ptr(), 8, 16, 0.0,
+                          out.data_ptr(), 64, 16)
+    assert st == sj.SJ_E_INVAL, sj.sj_last_error()
+    st, _ = sj.sj_join_l2(ctx, sj.SJ_I8, P.data_ptr(), 8, P.data_ptr(), 8, 16, 0.0,
+                          out.data_ptr(), 64, sj.SJ_FLAG_COSINE)
+    assert st == sj.SJ_E_INVAL, sj.sj_last_error()
     n = ctypes.c_uint64(0)
     assert sj.lib.sj_join_ip(ctx, sj.SJ_I8, P.data_ptr(), 8, P.data_ptr(), 8, 16, 0.0,
                              out.data_ptr(), 64, None, 0) == sj.SJ_E_INVAL
