@@ -299,8 +299,9 @@ int sj_lsh_plan(double p1, double p2, uint64_t n, uint32_t tile, double recall, 
  * device scratch of at most 2 n max_i(r_i k_i) floats).  The JL guarantee
  * (norms kept within 1 +- eps with probability 1 - delta) is a property of
  * the caller's A_i (e.g. i.i.d. N(0, 1/k_i) entries), not of this call.
- * Errors as sj_join_ip (SJ_E_INVAL for a broken size chain); afterwards
- * sj_get_stats reports ms_join = the transform's GPU time. */
+ * Errors as sj_join_ip (SJ_E_INVAL for a broken size chain, SJ_E_UNSUPPORTED
+ * for k_i or c_i above 65536 or a level of more than 2^48 values n r_i k_i);
+ * afterwards sj_get_stats reports ms_join = the transform's GPU time. */
 int sj_jl(sj_ctx *ctx, int dtype, const void *X, uint32_t n, uint32_t d, uint32_t levels,
           const uint32_t *shape, const float *A, float *Y);
 

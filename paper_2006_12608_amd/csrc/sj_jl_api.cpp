@@ -37,6 +37,11 @@ extern "C" int sj_jl(sj_ctx *c, int dtype, const void *X, uint32_t n, uint32_t d
             return fail(SJ_E_UNSUPPORTED, "level %u: k or c above 65536", i + 1);
         a_elems += k * cc;
         len = r * k;
+        // n * len elements per level (and 4 n len bytes) must not wrap: at
+        // most 2^48, far beyond any device memory
+        if (len > ((uint64_t)1 << 48) / (n ? n : 1))
+            return fail(SJ_E_UNSUPPORTED, "level %u: n * r * k = %u * %llu elements is too large",
+                        i + 1, n, (unsigned long long)len);
         if (i + 1 < levels)
             tmp = tmp > (uint64_t)n * len ? tmp : (uint64_t)n * len;
     }

@@ -138,6 +138,11 @@ def test_jl_errors():
     st = sj.sj_jl(ctx, sj.SJ_F16, X.data_ptr(), 10, 24, 1, [(65536, 24, 1)], bigA.data_ptr(),
                   Y.data_ptr())
     assert st == sj.SJ_E_INVAL      # Y holds far less than 10 x 65536 floats
+    # a size chain whose last level would hold 10 x 2^47 values (more than
+    # 2^48): rejected before any buffer is sized from it
+    huge = [(65536, 24, 1), (65536, 1, 65536), (65536, 2, 1 << 31)]
+    st = sj.sj_jl(ctx, sj.SJ_F16, X.data_ptr(), 10, 24, 3, huge, A.data_ptr(), Y.data_ptr())
+    assert st == sj.SJ_E_UNSUPPORTED, sj.sj_last_error()
     st = sj.sj_jl(ctx, sj.SJ_F16, X.data_ptr(), 0, 24, 1, [(5, 24, 1)], A.data_ptr(),
                   Y.data_ptr())
     assert st == sj.SJ_OK
