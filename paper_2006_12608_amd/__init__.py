@@ -223,6 +223,12 @@ def dtype_code(t) -> int:
     return codes[t.dtype]
 
 
+def _metric_code(metric: str) -> int:
+    if metric not in ("ip", "l2"):
+        raise ValueError(f"metric must be 'ip' or 'l2', not {metric!r}")
+    return SJ_IP if metric == "ip" else SJ_L2
+
+
 def _check_pair(P, Q):
     if P.dim() != 2 or Q.dim() != 2 or P.shape[1] != Q.shape[1]:
         raise ValueError("P and Q must be 2-D with the same number of columns")
@@ -237,8 +243,8 @@ def _check_pair(P, Q):
 def count(P, Q, threshold: float, metric: str = "ip", ctx=None) -> int:
     """Number of matching pairs (sj_count)."""
     _check_pair(P, Q)
+    m = _metric_code(metric)
     ctx = ctx or context(P.device.index)
-    m = SJ_IP if metric == "ip" else SJ_L2
     st, n = sj_count(ctx, m, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0],
                      P.shape[1], threshold)
     if st != SJ_OK:
@@ -371,8 +377,8 @@ def join_lsh(P, Q, thr: float, metric: str = "ip", *, L: int, k: int, A, B=None,
     if B is not None and (B.dtype != torch.int32 or not B.is_cuda or not B.is_contiguous()
                           or B.numel() != L * k):
         raise ValueError(f"B must be a contiguous ({L * k},) int32 device tensor")
+    m = _metric_code(metric)
     ctx = ctx or context(P.device.index)
-    m = SJ_IP if metric == "ip" else SJ_L2
     args = (ctx, m, dtype_code(P), P.data_ptr(), P.shape[0], Q.data_ptr(), Q.shape[0],
             P.shape[1], thr, L, k, A.data_ptr() if A.numel() else None,
             None if B is None else B.data_ptr(), w)

@@ -163,3 +163,14 @@ def test_zero_dimension_reading(env):
         assert sj.join_l2(P0, Q0, -1e-30, two_pass=two_pass, ctx=ctx).shape[0] == 0
     assert sj.count(P0, Q0, -5.0, "ip", ctx=ctx) == 63
     assert sj.count(P0, Q0, 3.0, "l2", ctx=ctx) == 63
+
+
+def test_unknown_metric_is_rejected(env):
+    sj, ctx, torch = env
+    say("unknown metric")
+    P = torch.zeros((8, 16), dtype=torch.int8, device="cuda")
+    with pytest.raises(ValueError, match="metric"):
+        sj.count(P, P, 0.0, "cos", ctx)
+    A = torch.zeros((2, 16), dtype=torch.int8, device="cuda")
+    with pytest.raises(ValueError, match="metric"):
+        sj.join_lsh(P, P, 0.0, "L2", L=1, k=2, A=A, ctx=ctx)
