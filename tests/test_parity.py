@@ -185,6 +185,45 @@ def test_extreme_thresholds(dtype):
         assert sj.count(Pd, Qd, huge, metric) == 130 * 70
 
 
+@pytest.mark.parametrize("dtype,metric", [("i8", "l2"), ("i8", "ip"), ("f16", "ip"),
+                                          ("bf16", "l2")])
+def test_maximum_d(dtype, metric):
+    """The longest rows the library takes (d = 32768 int8, 65536 fp16 / bf16:
+    the K-streamed kernel over 256 or 1024 chunks of 128 bytes), 40 x 300 rows
+    (ragged against the 256-row tiles), both modes.  int8 row 0 of P is all
+    127, row 1 of P and rows 0 and 1 of Q all -128, and the thresholds include
+    the largest squared distance int8 rows of this length can have (32768 *
+    255^2 = 2130739200, inside int32: every pair matches, row pair (0, 0) as a
+    tie) and the largest inner product (32768 * 128^2: row pairs (1, 0) and
+    (1, 1) only)."""
+    d = 32768 if dtype == "i8" else 65536
+    lo, hi = (-128, 127) if dtype == "i8" else (-4, 4)
+    rng = np.random.default_rng(5150 + 2 * (dtype == "i8") + (metric == "l2"))
+    Pv = rng.integers(lo, hi + 1, size=(40, d))
+    Qv = rng.integers(lo, hi + 1, size=(300, d))
+    if dtype == "i8":
+        Pv[0], Qv[0], Pv[1], Qv[1] = 127, -128, -128, -128
+    x, y = Pv.astype(np.float64), Qv.astype(np.float64)   # sums stay below 2^53: exact
+    if metric == "ip":
+        thrs = [float(np.quantile(x @ y.T, 0.9, method="nearest"))]
+        if dtype == "i8":
+            thrs.append(float(32768 * 128 * 128))
+    else:
+        D = (x * x).sum(1)[:, None] + (y * y).sum(1)[None, :] - 2 * (x @ y.T)
+        thrs = [float(np.quantile(D, 0.1, method="nearest"))]
+        if dtype == "i8":
+            thrs.append(float(32768 * 255 * 255))
+    w = workloads.Workload(f"maxd_{dtype}_{d}", metric, dtype, workloads.encode(Pv, dtype),
+                           workloads.encode(Qv, dtype), 0.0, np.zeros((0, 2), np.int64))
+    for thr in thrs:
+        for two_pass in (False, True):
+            _, g, ref = run_case(w, thr=thr, two_pass=two_pass)
+            if dtype == "i8" and thr == 32768 * 255 * 255:
+                assert g.shape[0] == 40 * 300
+            if dtype == "i8" and thr == 32768 * 128 * 128:
+                assert g.tolist() == [[1, 0], [1, 1]]
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 600), ("f16", 1024), ("i8", 700)])
 def test_streamed_dense_output(dtype, d):
     """The K-streamed kernel with every pair matching (each wave's staging
