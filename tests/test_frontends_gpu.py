@@ -145,7 +145,8 @@ def _bits_device(X):
 @pytest.mark.parametrize("d,n_p,n_q,two_pass", [(1, 40, 33, False), (8, 300, 517, True),
                                                 (45, 513, 129, False), (64, 700, 600, True),
                                                 (100, 257, 300, False), (256, 300, 301, True),
-                                                (300, 270, 333, False), (1000, 130, 140, True)])
+                                                (300, 270, 333, False), (1000, 130, 140, True),
+                                                (16384, 33, 70, False), (16384, 33, 70, True)])
 def test_hamming_join(d, n_p, n_q, two_pass):
     import paper_2006_12608_amd as sj
     rng = np.random.default_rng(700 + d)
