@@ -110,6 +110,22 @@ def test_lsh_parity_integer(dtype, metric, thr, d, wid):
     assert cand < w.n_p * w.n_q * h.L
 
 
+@pytest.mark.parametrize("dtype,d,L,k,wid,metric,thr", [
+    # 1200-byte rows: the keys from 512-byte segments of the rows in LDS, the
+    # functions in passes of 16; the bucket join gathers 10 chunks per row
+    ("f16", 600, 5, 20, 0, "ip", 150.0),
+    ("i8", 1100, 3, 6, 900, "l2", 4000.0),    # 1104-byte rows, quantised hashes
+    # 70 tables of 8 signs (560 functions): more than the matrix-core hash takes
+    ("bf16", 64, 70, 8, 0, "ip", 20.0),
+])
+def test_lsh_general_hash_long_rows_many_functions(dtype, d, L, k, wid, metric, thr):
+    w = case(800 + d + L, 300, 280, d, dtype, metric, thr)
+    w.Q[:40] = w.P[100:140]
+    h = workloads.lsh_params(950 + d + L, L=L, k=k, d=d, w=wid)
+    g, ref, exact, cand, _ = run_lsh(w, h)
+    assert 40 <= len(ref) <= exact.total
+
+
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 def test_lsh_parity_real_cosine(dtype):
     """Unit rows (real-valued), sign hashes: identical outside the band."""
