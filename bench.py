@@ -439,7 +439,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the join shards "
-              "by rows of P across GPUs, which this build does not run", file=sys.stderr)
+              "by rows of P across GPUs, which is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
