@@ -167,6 +167,25 @@ def test_jl_full_size_sampled_rows():
     assert (np.abs(nrm - 1) <= 0.5).mean() > 0.99
 
 
+def test_jl_most_levels():
+    """32 levels, the most one call takes: row lengths 12 -> 8 -> 12 -> ...
+    through (k, c, r) = (2, 3, 4) and (3, 2, 4), each factor a signed selection
+    (one +-1 per row), so every value stays a small integer and the result
+    must equal the oracle's exactly."""
+    rng = np.random.default_rng(3232)
+    shapes = [(2, 3, 4) if i % 2 == 0 else (3, 2, 4) for i in range(32)]
+    As = []
+    for (k, c, r) in shapes:
+        A = np.zeros((k, c))
+        A[np.arange(k), rng.integers(0, c, size=k)] = rng.choice([-1.0, 1.0], size=k)
+        As.append(A)
+    X = workloads.encode(rng.integers(-4, 5, size=(301, 12)), "f16")
+    say("jl 32 levels")
+    Y = run(X, "f16", shapes, As)
+    assert Y.shape == (301, 12)
+    assert np.array_equal(Y, jl.transform(values("f16", X), shapes, As))
+
+
 @pytest.mark.parametrize("dtype,n,d,shapes", [
     ("f16", 1, 6, [(3, 6, 1)]),                      # one row, one level
     ("bf16", 129, 15, [(2, 5, 3), (7, 6, 1)]),       # odd sizes: no 4-entry loads

@@ -195,12 +195,13 @@ def test_lsh_self_join_same_pointer():
 
 
 @pytest.mark.parametrize("d,L,thr", [(16, 24, 6.0), (64, 56, 64.0), (80, 20, 72.0),
-                                     (96, 24, 78.0), (128, 24, 90.0)])
+                                     (96, 24, 78.0), (128, 24, 90.0), (32, 256, 20.0)])
 def test_lsh_many_tables_first_table_rule(d, L, thr):
     """Many tables and few functions: most pairs collide in several tables;
     each must still be reported once.  Short rows carry fingerprints of the
     first 112 - (row bytes rounded up to 32) tables in their records (80, 48
-    and 16 tables here, later tables by their keys); 128-byte rows carry 16."""
+    and 16 tables here, later tables by their keys); 128-byte rows carry 16.
+    256 tables is the most one call takes (its hash on the general kernel)."""
     w = case(47 + d, 260, 240, d, "i8", "ip", thr, -3, 3)
     h = workloads.lsh_params(48 + d, L=L, k=2, d=d)
     g, ref, *_ = run_lsh(w, h)
