@@ -250,9 +250,10 @@ int sj_join_lsh(sj_ctx *ctx, int metric, int dtype, const void *P, uint32_t n_p,
  * bits <= 32, the ascending order of a fixed bijective mix of the key
  * otherwise), so key sets sorted by separate calls list their common keys in
  * the same relative order: sj_join_lsh pairs P's buckets with Q's by merging
- * two such orders.  Errors: SJ_E_INVAL (NULL context, bits > 64, misaligned
- * pointers), SJ_E_UNSUPPORTED (L * n >= 2^32), SJ_E_DEVICE; L * n = 0 does
- * nothing.  Device scratch grows to about L * n * 20 bytes. */
+ * two such orders.  Errors: SJ_E_INVAL (NULL context, bits > 64, NULL,
+ * non-device, undersized or misaligned keys / perm), SJ_E_UNSUPPORTED (L * n
+ * >= 2^32), SJ_E_NOMEM (scratch), SJ_E_HIP (a runtime call failed); L * n = 0
+ * does nothing.  Device scratch grows to about L * n * 20 bytes. */
 int sj_lsh_sort(sj_ctx *ctx, const uint64_t *keys, uint32_t n, uint32_t L, uint32_t bits,
                 uint32_t *perm);
 
