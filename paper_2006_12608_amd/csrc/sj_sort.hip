@@ -252,10 +252,13 @@ __global__ void __launch_bounds__(256) break_kernel(const uint32_t *sk, const ui
     mark[a] = 1;
 }
 
-// Sorts every marked run by the mixed key, stably (insertion sort: distinct
-// keys share a top half with probability 2^-32, so marked runs are rare; the
-// cost is quadratic in a marked run's length).  Runs are disjoint and each
-// has one first position, so no two threads write the same entries.
+// Sorts every marked run by the mixed key, stably (insertion sort).  Two
+// distinct keys share a top half with probability 2^-32, so D distinct keys in
+// a table give about D^2 / 2^33 marked runs (about 100 at D = 10^6), each
+// joining the rows of two buckets; the cost of a run is its number of
+// inversions, at most the product of the two buckets' sizes.  Runs are
+// disjoint and each has one first position, so no two threads write the same
+// entries.
 __global__ void __launch_bounds__(256) fixup_kernel(const uint32_t *sk, const uint32_t *mark,
                                                     uint32_t n, uint64_t total, uint64_t *sorted,
                                                     uint32_t *perm)
